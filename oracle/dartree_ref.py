@@ -1,0 +1,339 @@
+"""Plain, slow CPU oracle of DARTree fixed-width draft-tree construction.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring): nothing on the product
+path may import, call or link this module.
+
+What it computes (paper: Sec. 3.2 "Depth-Wise Parallel Supertree Construction",
+Algorithm 1 "DARTree Construction", Sec. 3.3 "Deferred Best-First Pruning",
+eq. (5) and Lemma 1), for each request independently:
+
+  root level S_0 = {empty prefix}, state r_0, score 0              (Alg. 1, init)
+  for d = 1 .. L:                                                 (Alg. 1, depth loop)
+      for every parent j of S_{d-1}:
+          t_j = A r_j                                  (correction head, state part)
+          a_j = rnd(tanh(t_j + H_d))                   (correction feature)
+          z_j = L_d^base + U a_j                       (corrected logits, full vocab)
+          l_j = log_softmax(z_j / tau)                 (log q~_d(. | u_<d), tau = T or 1)
+          C_j = top-k ids of z_j by (z desc, id asc)   (per-parent candidate set)
+      candidates (j, v in C_j), score s = (s_j + l_j[v]) + beta   (eq. (5), one step)
+      S_d = first n_d candidates by (s desc, j asc, v asc)        (global top-W)
+      r_child = rnd(tanh(t_j + e * U[v])), e = fp32(sqrt(h))      (state update)
+  T = first min(B, |S|) nodes of S by (s desc, depth asc, slot asc)   (top-B, Lemma 1)
+  emit T in canonical breadth-first order with parent indices and the
+  ancestor-or-self tree-attention mask (Sec. 2.3 "Tree Verification").
+
+Readings where the paper is silent (each is listed in the design doc):
+  * the head form g and the state update (Alg. 1 gives only g(H_d, r(u_<d)) and
+    "r(u_1:d) from r(u_<d) and u_d"): the Elman residual head above;
+  * the candidate set is the per-parent top-k of the full-vocabulary corrected
+    logits (the "Full" vocabulary variant of Appendix D) with branching cap k;
+  * tau = T for T > 0 and tau = 1 at T = 0 (q_T is defined for T > 0 only);
+  * rounding points: with bf16 inputs, a and r are rounded to bf16 (through
+    fp32, nearest-even) because they are operands of bf16 matrix products;
+    everything else is fp64 here.  With fp32 inputs nothing is rounded;
+  * n_d = min(W, n_{d-1} * k); "global" top-W is per request;
+  * tie-breaks: top-k (z desc, id asc); top-W (s desc, parent slot asc, id asc);
+    top-B (s desc, depth asc, slot asc) - "depth asc" is Lemma 1's "ancestors
+    are preferred under ties";
+  * the root is not a node of T and does not count toward B.
+
+Parity status: every function here is pinned by the CPU tests (brute force,
+Lemma 1's heap, the sequential-heap algorithm of Sec. 3.1, special cases and
+library routines).  The head form itself is this oracle's reading of a passage
+the paper leaves open; its arithmetic is pinned by scalar-loop evaluation only.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Callable, Optional
+
+import numpy as np
+
+FP32 = 0
+BF16 = 1
+
+
+# ----------------------------------------------------------------------------
+# Parameters and decoded inputs
+# ----------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class Params:
+    """Alg. 1 inputs that are not tensors: depth L (= gamma), width W, branching
+    cap k, budget B, temperature T and depth bonus beta (<= 0, Lemma 1)."""
+
+    batch: int
+    vocab: int
+    hidden: int
+    depth: int
+    width: int
+    branch: int
+    budget: int
+    temperature: float
+    depth_bonus: float
+    precision: int
+
+    @staticmethod
+    def of(cfg) -> "Params":
+        return Params(cfg.batch, cfg.vocab, cfg.hidden, cfg.depth, cfg.width,
+                      cfg.branch, cfg.budget, float(cfg.temperature),
+                      float(cfg.depth_bonus), int(cfg.precision))
+
+    @property
+    def tau(self) -> float:
+        return self.temperature if self.temperature > 0 else 1.0
+
+    @property
+    def embed_scale(self) -> float:
+        """e = fp32(sqrt(h)), the scale of the token input of the state update."""
+        return float(np.float32(np.sqrt(np.float64(self.hidden))))
+
+    def level_sizes(self) -> list[int]:
+        n, out = 1, []
+        for _ in range(self.depth):
+            n = min(self.width, n * min(self.branch, self.vocab))
+            out.append(n)
+        return out
+
+
+def _decode(x: np.ndarray, precision: int) -> np.ndarray:
+    """Input values as fp64: bf16 bit patterns are widened exactly."""
+    if precision == BF16:
+        return (np.asarray(x, np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    return np.asarray(x, np.float32).astype(np.float64)
+
+
+@dataclasses.dataclass
+class Decoded:
+    p: Params
+    Lb: np.ndarray  # [b][L][V]
+    H: np.ndarray   # [b][L][h]
+    r0: np.ndarray  # [b][h]
+    A: np.ndarray   # [h][h]
+    U: np.ndarray   # [V][h]
+
+
+def prepare(inputs, params: Optional[Params] = None) -> Decoded:
+    """Decode one round's inputs (any object with Lb, H, r0, A, U and cfg)."""
+    p = params if params is not None else Params.of(inputs.cfg)
+    return Decoded(p, np.asarray(inputs.Lb, np.float32).astype(np.float64),
+                   _decode(inputs.H, p.precision), _decode(inputs.r0, p.precision),
+                   _decode(inputs.A, p.precision), _decode(inputs.U, p.precision))
+
+
+def rnd_bf16(x: np.ndarray) -> np.ndarray:
+    """fp64 -> fp32 (nearest-even) -> bf16 (nearest-even), returned as fp64."""
+    u = np.asarray(x, np.float64).astype(np.float32).view(np.uint32)
+    u = (u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))) & np.uint32(0xFFFF0000)
+    return u.view(np.float32).astype(np.float64)
+
+
+def _rounder(precision: int) -> Callable[[np.ndarray], np.ndarray]:
+    return rnd_bf16 if precision == BF16 else (lambda x: x)
+
+
+# ----------------------------------------------------------------------------
+# One depth (Alg. 1, loop body)
+# ----------------------------------------------------------------------------
+
+def head_features(r: np.ndarray, A: np.ndarray, H_d: np.ndarray, precision: int):
+    """Correction head, state part: t_j = A r_j and a_j = rnd(tanh(t_j + H_d)).
+
+    ``r`` is [R][h] (one parent state per row); returns (t, a), both [R][h].
+    """
+    t = r @ A.T
+    a = _rounder(precision)(np.tanh(t + H_d[None, :]))
+    return t, a
+
+
+def vocab_logits(a: np.ndarray, U: np.ndarray, Lb_d: np.ndarray, chunk: int = 16384) -> np.ndarray:
+    """Corrected logits over the whole vocabulary: z_j = L_d^base + U a_j ([R][V])."""
+    R, V = a.shape[0], U.shape[0]
+    z = np.empty((R, V), np.float64)
+    for c in range(0, V, chunk):
+        z[:, c:c + chunk] = Lb_d[None, c:c + chunk] + a @ U[c:c + chunk].T
+    return z
+
+
+def log_softmax(z: np.ndarray, tau: float) -> np.ndarray:
+    """log q_T: (z - m)/tau - log sum_v exp((z_v - m)/tau), row-wise."""
+    m = z.max(axis=-1, keepdims=True)
+    y = (z - m) / tau
+    return y - np.log(np.exp(y).sum(axis=-1, keepdims=True))
+
+
+def topk_ids(z_row: np.ndarray, k: int) -> np.ndarray:
+    """The first k ids of one row ordered by (z desc, id asc)."""
+    V = z_row.shape[0]
+    k = min(k, V)
+    kth = np.partition(z_row, V - k)[V - k]          # k-th largest value
+    cand = np.nonzero(z_row >= kth)[0]               # contains every id of the top-k
+    order = np.lexsort((cand, -z_row[cand]))
+    return cand[order[:k]]
+
+
+def select_level(parent: np.ndarray, token: np.ndarray, score: np.ndarray, n_keep: int) -> np.ndarray:
+    """Indices of the first n_keep candidates by (score desc, parent asc, token asc)."""
+    order = np.lexsort((token, parent, -score))
+    return order[:n_keep]
+
+
+def path_score(s_parent: np.ndarray, logp: np.ndarray, beta: float) -> np.ndarray:
+    """Eq. (5) one depth at a time: s(u_1:d) = (s(u_<d) + log q~_d(u_d)) + beta."""
+    return (s_parent + logp) + beta
+
+
+def child_states(t_parent: np.ndarray, U_tok: np.ndarray, e: float, precision: int) -> np.ndarray:
+    """State update r(u_1:d) = rnd(tanh(t(u_<d) + e * U[u_d])) for kept children."""
+    return _rounder(precision)(np.tanh(t_parent + e * U_tok))
+
+
+# ----------------------------------------------------------------------------
+# Whole construction
+# ----------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class Level:
+    """S_d of one request: n_d nodes in slot order."""
+
+    token: np.ndarray    # int64 [n_d]
+    parent: np.ndarray   # int64 [n_d], slot in S_{d-1} (0 = the root at d = 1)
+    score: np.ndarray    # fp64 [n_d], s_beta(u_1:d)
+    # per-parent rows of this depth (for comparison with a second implementation)
+    lse: Optional[np.ndarray] = None        # [n_{d-1}] log sum_v exp(z_v / tau)
+    cand_ids: Optional[np.ndarray] = None   # [n_{d-1}][k] top-k ids of each parent
+    cand_logp: Optional[np.ndarray] = None  # [n_{d-1}][k] their log q~
+    logp: Optional[np.ndarray] = None       # [n_{d-1}][V] full log q~ (kept on demand)
+
+
+@dataclasses.dataclass
+class Supertree:
+    p: Params
+    levels: list  # levels[i][d-1] = Level of request i at depth d
+
+
+Chooser = Callable[..., np.ndarray]
+
+
+def _default_choose(req: int, d: int, parent, token, score, n_keep: int, level_rows) -> np.ndarray:
+    return select_level(parent, token, score, n_keep)
+
+
+def build_supertree(dec: Decoded, requests=None, choose: Optional[Chooser] = None,
+                    choose_topk: Optional[Callable] = None, keep_logp: bool = False) -> Supertree:
+    """Alg. 1's depth loop for every request (slow: full fp64 vocabulary products).
+
+    ``choose`` / ``choose_topk`` let a caller replace the two selections (used
+    to follow another implementation's choices); by default the oracle makes
+    its own.  ``choose_topk(req, d, j, z_row, logp_row, k)`` returns the ids of
+    parent j's candidate set.
+    """
+    p = dec.p
+    choose = choose or _default_choose
+    tau, e, beta = p.tau, p.embed_scale, p.depth_bonus
+    k = min(p.branch, p.vocab)
+    sizes = p.level_sizes()
+    reqs = range(p.batch) if requests is None else requests
+    out = []
+    for b in reqs:
+        r = dec.r0[b][None, :]            # states of S_0
+        s = np.zeros(1)                   # scores of S_0
+        levels = []
+        for d in range(1, p.depth + 1):
+            t, a = head_features(r, dec.A, dec.H[b, d - 1], p.precision)
+            z = vocab_logits(a, dec.U, dec.Lb[b, d - 1])
+            lp = log_softmax(z, tau)
+            m = z.max(axis=1)
+            lse = m / tau + np.log(np.exp((z - m[:, None]) / tau).sum(axis=1))
+            R = z.shape[0]
+            cids = np.empty((R, k), np.int64)
+            for j in range(R):
+                cids[j] = (choose_topk(b, d, j, z[j], lp[j], k) if choose_topk
+                           else topk_ids(z[j], k))
+            clp = np.take_along_axis(lp, cids, axis=1)
+            par = np.repeat(np.arange(R), k)
+            tok = cids.reshape(-1)
+            sc = path_score(s[par], clp.reshape(-1), beta)
+            keep = choose(b, d, par, tok, sc, sizes[d - 1], None)
+            lvl = Level(token=tok[keep], parent=par[keep], score=sc[keep], lse=lse,
+                        cand_ids=cids, cand_logp=clp, logp=lp if keep_logp else None)
+            levels.append(lvl)
+            r = child_states(t[lvl.parent], dec.U[lvl.token], e, p.precision)
+            s = lvl.score
+        out.append(levels)
+    return Supertree(p, out)
+
+
+def prune(levels: list, budget: int):
+    """Global top-B over the supertree by (s desc, depth asc, slot asc).
+
+    Returns the kept nodes as a list of (depth, slot) in that order.
+    """
+    depth = np.concatenate([np.full(len(l.token), d + 1) for d, l in enumerate(levels)])
+    slot = np.concatenate([np.arange(len(l.token)) for l in levels])
+    score = np.concatenate([l.score for l in levels])
+    order = np.lexsort((slot, depth, -score))[:min(budget, len(score))]
+    return [(int(depth[i]), int(slot[i])) for i in order]
+
+
+@dataclasses.dataclass
+class Tree:
+    """Emitted verification trees of a batch (pad slots: -1 / -1 / 0 / -inf / 0)."""
+
+    tokens: np.ndarray     # int32 [b][B]
+    parents: np.ndarray    # int32 [b][B], output index of the parent, -1 under the root
+    depths: np.ndarray     # int32 [b][B], 1..L
+    scores: np.ndarray     # fp64 [b][B]
+    mask: np.ndarray       # uint64 [b][B][ceil(B/64)], bit j of row i: j is an ancestor-or-self of i
+    num_nodes: np.ndarray  # int32 [b]
+
+
+def emit_tree(levels: list, kept, budget: int):
+    """Flatten the kept nodes of one request in canonical breadth-first order.
+
+    Order: depth asc, then the parent's output index asc, then token asc.
+    The ancestor-or-self mask row of a node is its parent's row plus itself.
+    """
+    words = (budget + 63) // 64
+    tokens = np.full(budget, -1, np.int32)
+    parents = np.full(budget, -1, np.int32)
+    depths = np.zeros(budget, np.int32)
+    scores = np.full(budget, -np.inf)
+    mask = np.zeros((budget, words), np.uint64)
+    out_index = {}  # (depth, slot) -> output index
+    kept_by_depth = {}
+    for (d, sl) in kept:
+        kept_by_depth.setdefault(d, []).append(sl)
+    n = 0
+    for d in sorted(kept_by_depth):
+        lvl = levels[d - 1]
+        rows = []
+        for sl in kept_by_depth[d]:
+            pidx = -1 if d == 1 else out_index[(d - 1, int(lvl.parent[sl]))]
+            rows.append((pidx, int(lvl.token[sl]), sl))
+        rows.sort()
+        for pidx, tok, sl in rows:
+            out_index[(d, sl)] = n
+            tokens[n], parents[n], depths[n], scores[n] = tok, pidx, d, lvl.score[sl]
+            if pidx >= 0:
+                mask[n] = mask[pidx]
+            mask[n, n // 64] |= np.uint64(1) << np.uint64(n % 64)
+            n += 1
+    return tokens, parents, depths, scores, mask, n
+
+
+def build_tree(dec: Decoded, requests=None) -> tuple[Tree, Supertree]:
+    """Alg. 1 end to end: supertree, top-B prune, emitted trees."""
+    st = build_supertree(dec, requests)
+    return emit_batch(st), st
+
+
+def emit_batch(st: Supertree, kept_sets=None) -> Tree:
+    B = st.p.budget
+    outs = []
+    for i, levels in enumerate(st.levels):
+        kept = prune(levels, B) if kept_sets is None else kept_sets[i]
+        outs.append(emit_tree(levels, kept, B))
+    return Tree(tokens=np.stack([o[0] for o in outs]), parents=np.stack([o[1] for o in outs]),
+                depths=np.stack([o[2] for o in outs]), scores=np.stack([o[3] for o in outs]),
+                mask=np.stack([o[4] for o in outs]), num_nodes=np.array([o[5] for o in outs], np.int32))

@@ -1,0 +1,279 @@
+"""Pins of the CPU oracle: each function raises AssertionError when the oracle
+disagrees with something fixed independently of it (a second algorithm from
+the paper, brute force, a library routine, a closed form or an invariant).
+
+They are collected as a list so that ``test_oracle_mutants`` can run the whole
+set against deliberately broken copies of the oracle's functions.  Every pin
+looks the oracle up through the module object at call time.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import scipy.special
+import torch
+
+import oracle.dartree_ref as R
+from paper_2608_13524_amd import workloads as W
+from tests import independent as I
+
+TOL = 1e-9
+
+
+def tiny(**kw) -> W.Config:
+    base = dict(name="pin", batch=1, vocab=5, hidden=8, depth=3, width=4, branch=3,
+                budget=6, temperature=0.0, precision=W.FP32, seed=11, sigma_w=0.5,
+                sigma_l=1.0, n_boost=2, boost_max=2.0)
+    base.update(kw)
+    return W.Config(**base)
+
+
+def run_oracle(cfg, inputs=None):
+    inputs = inputs if inputs is not None else W.make_inputs(cfg)
+    dec = R.prepare(inputs)
+    tree, st = R.build_tree(dec)
+    return inputs, tree, st
+
+
+def _paths_and_scores(tree, b):
+    paths = I.tree_paths(tree.tokens[b], tree.parents[b], tree.num_nodes[b])
+    return {p: float(tree.scores[b][i]) for i, p in enumerate(paths)}
+
+
+def _check_against_paths(tree, b, expected: dict, budget: int, tol=TOL):
+    """The emitted arrays of request b equal the canonical flattening of the
+    expected {path: score} set, and scores agree."""
+    tok, par, dep, mask, n = I.canonical_arrays(list(expected), budget)
+    assert int(tree.num_nodes[b]) == n, (int(tree.num_nodes[b]), n)
+    assert np.array_equal(tree.tokens[b], tok), (tree.tokens[b], tok)
+    assert np.array_equal(tree.parents[b], par), (tree.parents[b], par)
+    assert np.array_equal(tree.depths[b], dep)
+    assert np.array_equal(tree.mask[b], mask)
+    got = _paths_and_scores(tree, b)
+    for p, s in expected.items():
+        assert abs(got[p] - s) <= tol, (p, got[p], s)
+
+
+# ---------------------------------------------------------------------------
+# Building blocks
+# ---------------------------------------------------------------------------
+
+def pin_log_softmax_library():
+    """log q_T against scipy's log_softmax of z / tau; normalisation; shift."""
+    rng = np.random.default_rng(1)
+    z = rng.normal(0, 3, size=(4, 37))
+    for tau in (1.0, 0.7, 2.5):
+        got = R.log_softmax(z, tau)
+        assert np.allclose(got, scipy.special.log_softmax(z / tau, axis=-1), atol=1e-12)
+        assert np.allclose(np.exp(got).sum(axis=-1), 1.0, atol=1e-12)
+        assert np.allclose(R.log_softmax(z + 5.0, tau), got, atol=1e-12)
+        assert np.all(got <= 0)
+
+
+def pin_topk_sorted():
+    """Per-row top-k against a full sort by (z desc, id asc), with many ties."""
+    rng = np.random.default_rng(2)
+    for trial in range(20):
+        z = np.round(rng.normal(0, 1, size=23) * 2) / 2  # coarse values: ties
+        for k in (1, 3, 8, 23):
+            want = [v for _, v in sorted((-x, v) for v, x in enumerate(z))][:k]
+            assert list(R.topk_ids(z, k)) == want, (z, k)
+
+
+def pin_select_sorted():
+    """Top-W against a full sort by (score desc, parent asc, token asc)."""
+    rng = np.random.default_rng(3)
+    for trial in range(20):
+        n = 30
+        parent = rng.integers(0, 5, size=n)
+        token = rng.permutation(100)[:n]
+        score = np.round(rng.normal(0, 1, size=n) * 2) / 2
+        for keep in (1, 7, 30):
+            idx = R.select_level(parent, token, score, keep)
+            want = sorted(range(n), key=lambda i: (-score[i], parent[i], token[i]))[:keep]
+            assert list(idx) == want
+
+
+def pin_bf16_rounding():
+    """Oracle rounding point against torch's float32 -> bfloat16 conversion."""
+    rng = np.random.default_rng(4)
+    x = np.concatenate([rng.normal(0, 1, 5000), rng.normal(0, 1e-3, 1000),
+                        # exact halfway cases between two bf16 values
+                        (np.arange(1, 200) * 2 + 1) * 2.0 ** -8 / 2 + 1.0])
+    want = torch.from_numpy(x).to(torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(R.rnd_bf16(x), want)
+
+
+def pin_head_scalar():
+    """Head arithmetic (t, a, z, log q~, next state) against scalar loops."""
+    for prec in (W.FP32, W.BF16):
+        cfg = tiny(precision=prec, vocab=7, hidden=8, depth=3, seed=5)
+        inp = W.make_inputs(cfg)
+        dec = R.prepare(inp)
+        head = I.ScalarHead(inp, cfg)
+        rng = np.random.default_rng(6)
+        r = [float(x) for x in rng.normal(0, 1, cfg.hidden)]
+        if prec == W.BF16:
+            r = [I._bf16(x) for x in r]
+        for d in (1, 3):
+            t, a = R.head_features(np.array([r]), dec.A, dec.H[0, d - 1], prec)
+            z = R.vocab_logits(a, dec.U, dec.Lb[0, d - 1])
+            lp = R.log_softmax(z, cfg.temperature or 1.0)
+            ts, zs, lps = head.step(0, d, r)
+            assert np.allclose(t[0], ts, atol=1e-12)
+            assert np.allclose(z[0], zs, atol=1e-9), (z[0], zs)
+            assert np.allclose(lp[0], lps, atol=1e-9)
+            for v in (0, 4):
+                rc = R.child_states(t[0][None, :], dec.U[v][None, :], R.Params.of(cfg).embed_scale, prec)
+                assert np.allclose(rc[0], head.child(ts, v), atol=1e-9)
+
+
+# ---------------------------------------------------------------------------
+# Whole construction
+# ---------------------------------------------------------------------------
+
+def pin_prune_is_heap():
+    """Lemma 1: top-B over the supertree == best-first heap pops, in order;
+    the kept set is prefix-closed."""
+    for seed, prec in ((7, W.FP32), (8, W.BF16), (9, W.FP32)):
+        cfg = tiny(seed=seed, precision=prec, vocab=6, depth=4, width=5, branch=3, budget=9)
+        inp, tree, st = run_oracle(cfg)
+        levels = st.levels[0]
+        kept = R.prune(levels, cfg.budget)
+        assert kept == I.heap_best_first(levels, cfg.budget)
+        ks = set(kept)
+        for (d, sl) in kept:
+            if d > 1:
+                assert (d - 1, int(levels[d - 1].parent[sl])) in ks
+
+
+def pin_brute_force():
+    """k = V and W >= V^L (no truncation): the tree is the global top-B over
+    every prefix, each scored along its own path."""
+    for seed, prec, T in ((12, W.FP32, 0.0), (13, W.BF16, 0.0), (14, W.FP32, 0.7)):
+        cfg = tiny(seed=seed, precision=prec, vocab=4, depth=3, width=64, branch=4,
+                   budget=11, temperature=T)
+        inp, tree, st = run_oracle(cfg)
+        want = I.brute_force(I.ScalarHead(inp, cfg), 0, cfg.budget, cfg.depth_bonus)
+        _check_against_paths(tree, 0, want, cfg.budget)
+
+
+def pin_sequential_heap():
+    """W >= B with the same branching cap: the tree equals node-at-a-time
+    correction with a best-first heap (Sec. 3.1)."""
+    for seed, prec in ((15, W.FP32), (16, W.BF16), (17, W.FP32)):
+        cfg = tiny(seed=seed, precision=prec, vocab=7, depth=4, width=8, branch=3, budget=8)
+        inp, tree, st = run_oracle(cfg)
+        want = I.sequential_heap(I.ScalarHead(inp, cfg), 0, cfg.budget, cfg.branch, cfg.depth_bonus)
+        _check_against_paths(tree, 0, want, cfg.budget)
+
+
+def pin_zeroed_correction():
+    """U = 0: every node of depth d sees the drafter marginal softmax(Lb_d / tau),
+    and the tree is DDTree's top-B by factorised mass plus beta*d."""
+    for T in (0.0, 0.7):
+        cfg = tiny(seed=18, vocab=4, depth=3, width=64, branch=4, budget=10, temperature=T)
+        inp = W.make_inputs(cfg)
+        inp.U[:] = 0
+        inp, tree, st = run_oracle(cfg, inp)
+        want, logq = I.marginal_top_b(inp.Lb[0], T or 1.0, cfg.depth, cfg.budget, cfg.depth_bonus)
+        _check_against_paths(tree, 0, want, cfg.budget)
+        for d, lvl in enumerate(st.levels[0], start=1):
+            for j in range(lvl.cand_ids.shape[0]):
+                assert np.allclose(lvl.cand_logp[j], [logq[d - 1][v] for v in lvl.cand_ids[j]], atol=1e-12)
+
+
+def pin_greedy_chain():
+    """W = 1 (and separately k = 1): the tree is the corrected single chain."""
+    for kw in (dict(width=1, branch=3), dict(width=4, branch=1)):
+        cfg = tiny(seed=19, vocab=9, depth=5, budget=16, **kw)
+        inp, tree, st = run_oracle(cfg)
+        path, scores = I.greedy_chain(I.ScalarHead(inp, cfg), 0, cfg.depth_bonus)
+        want = {path[:d]: scores[d - 1] for d in range(1, len(path) + 1)}
+        _check_against_paths(tree, 0, want, cfg.budget)
+
+
+def pin_whole_supertree():
+    """B >= |S| (DARTree (fixed)): every supertree node is emitted once."""
+    cfg = tiny(seed=20, vocab=6, depth=3, width=3, branch=2, budget=50)
+    inp, tree, st = run_oracle(cfg)
+    assert int(tree.num_nodes[0]) == sum(len(l.token) for l in st.levels[0]) == sum(cfg.level_sizes())
+    assert sorted(tree.depths[0][:tree.num_nodes[0]].tolist()) == sorted(
+        d for d, n in enumerate(cfg.level_sizes(), 1) for _ in range(n))
+
+
+def pin_monotone_scores():
+    """s(child) <= s(parent) + beta <= s(parent) along every emitted edge
+    (Appendix C), and the flattened tree is consistent with its own mask."""
+    cfg = tiny(seed=21, vocab=8, depth=4, width=6, branch=3, budget=12)
+    inp, tree, st = run_oracle(cfg)
+    n = int(tree.num_nodes[0])
+    for i in range(n):
+        p = int(tree.parents[0][i])
+        if p >= 0:
+            assert p < i and tree.depths[0][p] == tree.depths[0][i] - 1
+            assert tree.scores[0][i] <= tree.scores[0][p] + cfg.depth_bonus + 1e-12
+        else:
+            assert tree.depths[0][i] == 1
+    tok, par, dep, mask, nn = I.canonical_arrays(I.tree_paths(tree.tokens[0], tree.parents[0], n), cfg.budget)
+    assert np.array_equal(mask, tree.mask[0]) and np.array_equal(par, tree.parents[0])
+
+
+def pin_batch_independence():
+    """A request's tree is the same alone or inside a batch."""
+    cfg = tiny(seed=22, batch=3, vocab=7, depth=3, width=4, branch=3, budget=7)
+    inp, tree, st = run_oracle(cfg)
+    for i in range(3):
+        one = W.make_inputs(cfg, requests=[i])
+        _, t1, _ = run_oracle(one.cfg, one)
+        for f in ("tokens", "parents", "depths", "mask"):
+            assert np.array_equal(getattr(tree, f)[i], getattr(t1, f)[0])
+        assert np.allclose(tree.scores[i], t1.scores[0], equal_nan=True)
+
+
+def pin_vocab_permutation():
+    """Relabelling the vocabulary (rows of U, columns of Lb) relabels the tokens."""
+    cfg = tiny(seed=23, vocab=9, depth=3, width=4, branch=3, budget=8)
+    inp, tree, st = run_oracle(cfg)
+    perm = np.random.default_rng(24).permutation(cfg.vocab)   # new id of old id v is perm[v]
+    inv = np.argsort(perm)
+    inp2 = W.Inputs(cfg=cfg, Lb=inp.Lb[:, :, inv], H=inp.H, r0=inp.r0, A=inp.A, U=inp.U[inv])
+    _, tree2, _ = run_oracle(cfg, inp2)
+    p1 = _paths_and_scores(tree, 0)
+    p2 = _paths_and_scores(tree2, 0)
+    mapped = {tuple(int(perm[v]) for v in p): s for p, s in p1.items()}
+    assert set(mapped) == set(p2)
+    for p in p2:
+        assert abs(mapped[p] - p2[p]) < 1e-9
+
+
+def pin_prune_ties_prefer_ancestors():
+    """Lemma 1 with exact ties (beta = 0, child scores equal to their parent's):
+    top-B by (s desc, depth asc, slot asc) still equals the heap's pop order
+    and stays prefix-closed."""
+    rng = np.random.default_rng(25)
+    for trial in range(40):
+        L = int(rng.integers(2, 6))
+        levels, prev = [], 1
+        for d in range(1, L + 1):
+            n = int(rng.integers(1, 6))
+            parent = rng.integers(0, prev, size=n) if d > 1 else np.zeros(n, np.int64)
+            drop = rng.choice([0.0, 0.0, 0.5, 1.0], size=n)
+            base = levels[-1].score[parent] if d > 1 else np.zeros(n)
+            levels.append(R.Level(token=rng.permutation(50)[:n], parent=parent,
+                                  score=base - drop))
+            prev = n
+        for B in range(1, sum(len(l.token) for l in levels) + 2):
+            kept = R.prune(levels, B)
+            assert kept == I.heap_best_first(levels, B), (trial, B)
+            ks = set(kept)
+            assert all(d == 1 or (d - 1, int(levels[d - 1].parent[sl])) in ks for d, sl in kept)
+
+
+PINS = [
+    pin_log_softmax_library, pin_topk_sorted, pin_select_sorted, pin_bf16_rounding,
+    pin_head_scalar, pin_prune_is_heap, pin_prune_ties_prefer_ancestors, pin_brute_force, pin_sequential_heap,
+    pin_zeroed_correction, pin_greedy_chain, pin_whole_supertree, pin_monotone_scores,
+    pin_batch_independence, pin_vocab_permutation,
+]

@@ -1,0 +1,139 @@
+"""Every plausible mistake planted in the oracle must fail at least one pin.
+
+Each mutant replaces one oracle function (on the CPU, inside this test only)
+with a copy carrying a single bug: a transposed operand, a dropped term, a
+wrong sign or index, a reversed tie-break.
+"""
+import numpy as np
+import pytest
+
+import oracle.dartree_ref as R
+from tests import pins
+
+_orig = {name: getattr(R, name) for name in (
+    "head_features", "vocab_logits", "log_softmax", "topk_ids", "select_level",
+    "child_states", "path_score", "prune", "emit_tree", "rnd_bf16")}
+
+
+def _head_transposed(r, A, H_d, precision):
+    t = r @ A
+    return t, R._rounder(precision)(np.tanh(t + H_d[None, :]))
+
+
+def _head_no_hidden(r, A, H_d, precision):
+    t = r @ A.T
+    return t, R._rounder(precision)(np.tanh(t))
+
+
+def _head_no_round(r, A, H_d, precision):
+    t = r @ A.T
+    return t, np.tanh(t + H_d[None, :])
+
+
+def _logits_no_base(a, U, Lb_d, chunk=16384):
+    return a @ U.T
+
+
+def _logits_sign(a, U, Lb_d, chunk=16384):
+    return Lb_d[None, :] - a @ U.T
+
+
+def _lsm_no_norm(z, tau):
+    return (z - z.max(axis=-1, keepdims=True)) / tau
+
+
+def _lsm_no_tau(z, tau):
+    return _orig["log_softmax"](z, 1.0)
+
+
+def _topk_id_desc(z_row, k):
+    order = np.lexsort((-np.arange(len(z_row)), -z_row))
+    return order[:k]
+
+
+def _topk_ascending(z_row, k):
+    return np.lexsort((np.arange(len(z_row)), z_row))[:k]
+
+
+def _select_token_first(parent, token, score, n_keep):
+    return np.lexsort((parent, token, -score))[:n_keep]
+
+
+def _child_no_scale(t_parent, U_tok, e, precision):
+    return R._rounder(precision)(np.tanh(t_parent + U_tok))
+
+
+def _child_no_parent(t_parent, U_tok, e, precision):
+    return R._rounder(precision)(np.tanh(e * U_tok))
+
+
+def _score_no_beta(s_parent, logp, beta):
+    return s_parent + logp
+
+
+def _score_no_parent(s_parent, logp, beta):
+    return logp + beta
+
+
+def _prune_depth_desc(levels, budget):
+    depth = np.concatenate([np.full(len(l.token), d + 1) for d, l in enumerate(levels)])
+    slot = np.concatenate([np.arange(len(l.token)) for l in levels])
+    score = np.concatenate([l.score for l in levels])
+    order = np.lexsort((slot, -depth, -score))[:min(budget, len(score))]
+    return [(int(depth[i]), int(slot[i])) for i in order]
+
+
+def _prune_off_by_one(levels, budget):
+    return _orig["prune"](levels, budget - 1)
+
+
+def _emit_token_order(levels, kept, budget):
+    out = _orig["emit_tree"](levels, kept, budget)
+    tokens, parents, depths, scores, mask, n = out
+    # forget the mask's ancestor bits: self only
+    m2 = np.zeros_like(mask)
+    for i in range(n):
+        m2[i, i // 64] |= np.uint64(1) << np.uint64(i % 64)
+    return tokens, parents, depths, scores, m2, n
+
+
+def _rnd_truncate(x):
+    u = np.asarray(x, np.float64).astype(np.float32).view(np.uint32) & np.uint32(0xFFFF0000)
+    return u.view(np.float32).astype(np.float64)
+
+
+MUTANTS = {
+    "head_transposed_A": ("head_features", _head_transposed),
+    "head_drops_hidden": ("head_features", _head_no_hidden),
+    "head_skips_bf16_rounding": ("head_features", _head_no_round),
+    "logits_drop_base": ("vocab_logits", _logits_no_base),
+    "logits_wrong_sign": ("vocab_logits", _logits_sign),
+    "log_softmax_unnormalised": ("log_softmax", _lsm_no_norm),
+    "log_softmax_ignores_tau": ("log_softmax", _lsm_no_tau),
+    "topk_ties_id_desc": ("topk_ids", _topk_id_desc),
+    "topk_ascending": ("topk_ids", _topk_ascending),
+    "select_tiebreak_swapped": ("select_level", _select_token_first),
+    "child_no_embed_scale": ("child_states", _child_no_scale),
+    "child_ignores_parent": ("child_states", _child_no_parent),
+    "score_drops_beta": ("path_score", _score_no_beta),
+    "score_drops_parent": ("path_score", _score_no_parent),
+    "prune_prefers_descendants": ("prune", _prune_depth_desc),
+    "prune_budget_off_by_one": ("prune", _prune_off_by_one),
+    "mask_without_ancestors": ("emit_tree", _emit_token_order),
+    "bf16_truncates": ("rnd_bf16", _rnd_truncate),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, monkeypatch):
+    attr, fn = MUTANTS[name]
+    monkeypatch.setattr(R, attr, fn)
+    caught = []
+    for pin in pins.PINS:
+        try:
+            pin()
+        except AssertionError:
+            caught.append(pin.__name__)
+        except Exception as exc:  # a crash also exposes the mutant
+            caught.append(f"{pin.__name__}:{type(exc).__name__}")
+    assert caught, f"mutant {name} passed every pin"
