@@ -1,0 +1,216 @@
+/*
+ * dartree.h - C ABI of libdartree: DARTree fixed-width draft-tree construction
+ * on one AMD Instinct MI355X (gfx950).
+ *
+ * The library implements the construction of Algorithm 1 ("DARTree
+ * Construction", Sec. 3.2) and the deferred pruning of Sec. 3.3 (eq. (5),
+ * Lemma 1) of "DARTree: Speculative Diffusion Decoding with Autoregressive
+ * Draft Trees" (arXiv 2608.13524):
+ *
+ *   for d = 1..L, for every node u_<d of S_{d-1} in one batch:
+ *     t   = A r(u_<d)                              correction head, state part
+ *     a   = bf16(tanh(t + H_d))                    correction feature
+ *     z   = L_d^base + U a                         corrected logits, all V tokens
+ *     log q~_d = log_softmax(z / tau)              tau = T if T > 0 else 1
+ *     C(u_<d) = top-k ids of z, (z desc, id asc)   per-node candidate set
+ *     s(u_1:d) = (s(u_<d) + log q~_d(u_d)) + beta  eq. (5), one depth at a time
+ *     S_d = top-W children by (s desc, parent slot asc, token asc)
+ *     r(u_1:d) = bf16(tanh(t + e U[u_d])), e = fp32(sqrt(h))   state update
+ *   T = top-B of S = S_1 u ... u S_L by (s desc, depth asc, slot asc)
+ *
+ * The paper fixes only the signature of the correction head g(H_d, r(u_<d))
+ * and that r(u_1:d) is computed from r(u_<d) and u_d; the Elman residual head
+ * above (A [h][h], U [V][h] with U's rows doubling as token embeddings) is
+ * this library's choice.  With beta <= 0 the top-B set is prefix-closed and
+ * equals best-first heap selection (Lemma 1); beta > 0 is rejected.
+ *
+ * Conventions for every entry point:
+ *  - Device pointers are HIP device memory owned by the caller; the library
+ *    never allocates or frees device memory and keeps no pointer after return.
+ *  - All work is enqueued on `stream` (a hipStream_t; 0 = the null stream);
+ *    no call synchronises the host with the device.  Outputs are valid once
+ *    the stream's work completes.
+ *  - Every argument is validated on the host before anything is enqueued;
+ *    on any error nothing is enqueued and no output is written.
+ *  - One workspace must not be used by two calls that may run concurrently.
+ *  - Input values are assumed finite; non-finite inputs give undefined trees
+ *    (never out-of-bounds accesses).
+ *  - Layouts are dense row-major with the rightmost index fastest.  "act"
+ *    tensors are bfloat16 (raw 16-bit patterns) in DARTREE_BF16 mode and
+ *    float32 in DARTREE_FP32 mode.  Every pointer must be 16-byte aligned.
+ */
+#ifndef DARTREE_H
+#define DARTREE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DARTREE_ABI_VERSION 1
+
+/* Limits of this implementation (calls beyond them return
+ * DARTREE_ERR_UNSUPPORTED). */
+#define DARTREE_MAX_VOCAB (1 << 20)      /* V */
+#define DARTREE_MAX_DEPTH 64             /* L */
+#define DARTREE_MAX_WIDTH 2048           /* W */
+#define DARTREE_MAX_BRANCH 32            /* k */
+#define DARTREE_MAX_SORT 4096            /* n_{d-1}*k candidates, |S| nodes, B */
+
+typedef enum dartree_status {
+  DARTREE_OK = 0,
+  DARTREE_ERR_INVALID_ARG = 1, /* a size, value or pointer violates the contract */
+  DARTREE_ERR_UNSUPPORTED = 2, /* valid per the paper but beyond this library's limits */
+  DARTREE_ERR_WORKSPACE = 3,   /* workspace missing, misaligned or smaller than required */
+  DARTREE_ERR_HIP = 4          /* a kernel launch failed (hipGetLastError) */
+} dartree_status;
+
+typedef enum dartree_precision {
+  DARTREE_FP32 = 0, /* every tensor fp32, no intermediate rounding */
+  DARTREE_BF16 = 1  /* head weights, hidden and states bf16; logits fp32; bf16 MFMA with fp32 accumulation */
+} dartree_precision;
+
+/* Scalar arguments of Algorithm 1 (host struct). */
+typedef struct dartree_params {
+  int32_t batch;       /* b >= 1 independent requests, each built as its own tree */
+  int32_t vocab;       /* V >= 1 */
+  int32_t hidden;      /* h >= 1; a multiple of 64 in DARTREE_BF16 mode */
+  int32_t depth;       /* L = gamma, the draft block length, 1..DARTREE_MAX_DEPTH */
+  int32_t width;       /* W, layer width (nodes kept per depth), >= 1 */
+  int32_t branch;      /* k, candidate children scored per node, 1 <= k <= V */
+  int32_t budget;      /* B, verification budget (nodes of the emitted tree), >= 1 */
+  int32_t precision;   /* dartree_precision */
+  float temperature;   /* T >= 0, finite; tau = T if T > 0 else 1 */
+  float depth_bonus;   /* beta <= 0, finite (Lemma 1 needs beta <= 0) */
+} dartree_params;
+
+/* Device inputs of one round (Algorithm 1, "Require"). */
+typedef struct dartree_inputs {
+  const float* drafter_logits; /* L^base: fp32 [b][L][V] */
+  const void* drafter_hidden;  /* H: act [b][L][h] */
+  const void* prefix_state;    /* r_0: act [b][h], the root state of each request */
+  const void* head_A;          /* A: act [h][h], state transition (t_i = sum_j A[i][j] r_j) */
+  const void* head_U;          /* U: act [V][h], output projection and token embedding */
+} dartree_inputs;
+
+/* Device outputs: the flattened verification tree of each request (Sec. 2.3).
+ * Nodes are in canonical breadth-first order: depth ascending, then the
+ * parent's output index ascending, then token ascending.  Slots at and after
+ * num_nodes[i] hold token -1, parent -1, depth 0, score -inf, mask 0. */
+typedef struct dartree_tree {
+  int32_t* tokens;    /* [b][B] token id of the node */
+  int32_t* parents;   /* [b][B] output index of the parent; -1 for depth-1 nodes (children of the root) */
+  int32_t* depths;    /* [b][B] 1..L */
+  float* scores;      /* [b][B] s_beta of the node, eq. (5) */
+  uint64_t* mask;     /* [b][B][ceil(B/64)] tree-attention mask: bit (j % 64) of word
+                         j / 64 in row i is set iff node j is node i or an ancestor of it;
+                         the verified context is visible to every node and is not stored */
+  int32_t* num_nodes; /* [b] min(B, |S|) */
+} dartree_tree;
+
+/* Device destination of dartree_export_supertree.  n_d = min(W, n_{d-1} k),
+ * n_0 = 1.  Level arrays use a fixed stride W per request; per-parent arrays
+ * use a fixed stride b*W rows per depth, where depth d's rows are
+ * q * n_{d-1} + j for parent slot j of request q.  Any member may be NULL
+ * (not copied). */
+typedef struct dartree_supertree {
+  int32_t* tokens;    /* [L][b][W] token of slot i of S_d (i < n_d) */
+  int32_t* parents;   /* [L][b][W] parent's slot in S_{d-1} (0, the root, at d = 1) */
+  float* scores;      /* [L][b][W] s_beta */
+  float* lse;         /* [L][b*W] log sum_v exp(z_v / tau) of each parent row */
+  float* cand_logp;   /* [L][b*W][k] log q~ of the row's top-k candidates, best first */
+  int32_t* cand_ids;  /* [L][b*W][k] their token ids */
+} dartree_supertree;
+
+/* ABI version (DARTREE_ABI_VERSION of the built library). */
+int32_t dartree_abi_version(void);
+
+/* Static English description of a status code; never NULL. */
+const char* dartree_status_string(dartree_status status);
+
+/* Host-only check of `p` against the contract above (no HIP call). */
+dartree_status dartree_validate(const dartree_params* p);
+
+/* Bytes of device workspace needed by the calls below for `p` (host only).
+ * The workspace holds every level of the supertree, per-parent candidates
+ * and the per-depth scratch (states, features, logits [b*W][V] fp32). */
+dartree_status dartree_workspace_size(const dartree_params* p, size_t* bytes);
+
+/* One iteration of Algorithm 1's depth loop (d = 1..L): score every child of
+ * every node of S_{d-1} over the full vocabulary, keep the top-W as S_d and
+ * compute their states.  Reads S_{d-1} from `ws` (d = 1 reads
+ * in->prefix_state), so depths must be enqueued in order 1..L on one stream
+ * with the same workspace.  ws: device, 256-byte aligned, >= workspace_size. */
+dartree_status dartree_expand_depth(const dartree_params* p, const dartree_inputs* in,
+                                    int32_t d, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Deferred best-first pruning (Sec. 3.3, Algorithm 1 after the loop): top-B of
+ * the supertree held in `ws` after dartree_expand_depth(1..L), emitted as the
+ * flattened tree with parent indices and the ancestor-or-self mask. */
+dartree_status dartree_prune(const dartree_params* p, const void* ws, size_t ws_bytes,
+                             const dartree_tree* out, hipStream_t stream);
+
+/* Algorithm 1 end to end: expand_depth(1..L) then prune. */
+dartree_status dartree_build_tree(const dartree_params* p, const dartree_inputs* in,
+                                  void* ws, size_t ws_bytes, const dartree_tree* out,
+                                  hipStream_t stream);
+
+/* Copy the supertree levels and per-parent candidates out of `ws` into the
+ * caller's device buffers (layouts in dartree_supertree), for inspection. */
+dartree_status dartree_export_supertree(const dartree_params* p, const void* ws, size_t ws_bytes,
+                                        const dartree_supertree* dst, hipStream_t stream);
+
+/* ---- single steps on caller buffers --------------------------------------
+ * The kernels of one depth, exposed for callers that assemble their own loop
+ * (and for testing each step on injected inputs). */
+
+/* Corrected logits (Algorithm 1, "correct all prefixes ... in parallel"):
+ * z[m][v] = bias[m / rows_per_group][v] + sum_i x[m][i] U[v][i]
+ * for m < rows, v < vocab.  x: act [rows][hidden]; U: act [vocab][hidden];
+ * bias: fp32 rows of length vocab, row g at bias + g * bias_stride (elements);
+ * z: fp32 [rows][vocab].  precision as in dartree_params. */
+dartree_status dartree_project(int32_t precision, int32_t rows, int32_t vocab, int32_t hidden,
+                               int32_t rows_per_group, const void* x, const void* U,
+                               const float* bias, int64_t bias_stride, float* z,
+                               hipStream_t stream);
+
+/* Row-wise log-softmax normaliser and top-k of z / tau (tau = T if T > 0 else 1):
+ * lse[m] = log sum_v exp(z[m][v] / tau); cand_ids[m][0..k) are the k best ids
+ * by (z desc, id asc) and cand_logp[m][i] = (z[m][id] - max_v z[m][v]) / tau
+ * - log sum_v exp((z[m][v] - max) / tau).  z: fp32 [rows][vocab];
+ * ws/ws_bytes: device scratch of dartree_lse_topk_workspace_size bytes
+ * (may be NULL when that size is 0). */
+dartree_status dartree_lse_topk_workspace_size(int32_t rows, int32_t vocab, int32_t k, size_t* bytes);
+dartree_status dartree_lse_topk(const float* z, int32_t rows, int32_t vocab, int32_t k,
+                                float temperature, float* lse, float* cand_logp,
+                                int32_t* cand_ids, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Segmented top-W (Algorithm 1, "retain the global top-W child prefixes"):
+ * for each request q < batch, candidates (j, i) for parent j < n_parent and
+ * rank i < k score s = (parent_score[q][j] + cand_logp[q*n_parent + j][i]) + beta
+ * (parent_score may be NULL: every parent scores 0, the root); the first n_keep
+ * by (s desc, j asc, token asc) are written in that order to out_tokens,
+ * out_parents (j) and out_scores, each [batch][n_keep].
+ * n_parent * k <= DARTREE_MAX_SORT and n_keep <= n_parent * k. */
+dartree_status dartree_select_topw(int32_t batch, int32_t n_parent, int32_t k, int32_t n_keep,
+                                   float depth_bonus, const float* parent_score,
+                                   const float* cand_logp, const int32_t* cand_ids,
+                                   int32_t* out_tokens, int32_t* out_parents, float* out_scores,
+                                   hipStream_t stream);
+
+/* Deferred top-B prune of a supertree given in the dartree_supertree level
+ * layout (tokens, parents, scores: [L][b][W], level sizes from p).  Same
+ * output as dartree_prune. */
+dartree_status dartree_prune_levels(const dartree_params* p, const int32_t* tokens,
+                                    const int32_t* parents, const float* scores,
+                                    const dartree_tree* out, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DARTREE_H */

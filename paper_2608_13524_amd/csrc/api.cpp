@@ -1,0 +1,368 @@
+// C ABI of libdartree: argument validation, workspace layout and the order
+// of kernel launches for one round of Algorithm 1.  No function here touches
+// the device until every argument has been checked.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "internal.hpp"
+
+using namespace dartree;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t act_bytes(int precision) { return precision == DARTREE_BF16 ? 2 : 4; }
+
+// Level sizes n_d = min(W, n_{d-1} k), n_0 = 1, and derived extents.
+struct Shape {
+  int64_t n[DARTREE_MAX_DEPTH + 1];  // n[0] = 1, n[d] for d = 1..L
+  int64_t total;                     // |S| per request
+  int64_t max_parent;                // max_d n_{d-1}
+  int64_t max_cand;                  // max_d n_{d-1} k
+};
+
+Shape shape_of(const dartree_params& p) {
+  Shape s{};
+  s.n[0] = 1;
+  s.total = 0;
+  s.max_parent = 1;
+  s.max_cand = 0;
+  for (int d = 1; d <= p.depth; ++d) {
+    s.max_parent = std::max(s.max_parent, s.n[d - 1]);
+    s.max_cand = std::max(s.max_cand, s.n[d - 1] * p.branch);
+    s.n[d] = std::min<int64_t>(p.width, s.n[d - 1] * p.branch);
+    s.total += s.n[d];
+  }
+  return s;
+}
+
+// Workspace layout (each region 256-byte aligned), R = b * W rows:
+//   lvl_tok, lvl_par: i32 [L][b][W]     lvl_score: f32 [L][b][W]
+//   lse: f32 [L][R]   cand_logp: f32 [L][R][k]   cand_ids: i32 [L][R][k]
+//   state: act [2][R][h]   t: f32 [R][h]   a: act [R][h]   z: f32 [R][V]
+//   k3: the row-split partials of the largest depth
+struct Layout {
+  size_t lvl_tok, lvl_par, lvl_score, lse, cand_logp, cand_ids, state0, state1, t, a, z, k3, total;
+};
+
+Layout layout_of(const dartree_params& p, const Shape& s) {
+  const size_t L = p.depth, b = p.batch, W = p.width, k = p.branch, h = p.hidden, V = p.vocab;
+  const size_t R = b * W;
+  size_t k3 = 0;
+  for (int d = 1; d <= p.depth; ++d) k3 = std::max(k3, lse_topk_scratch_bytes(int64_t(b) * s.n[d - 1], V, int(k)));
+  Layout l{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) { const size_t at = o; o = align_up(o + bytes); return at; };
+  l.lvl_tok = take(L * b * W * 4);
+  l.lvl_par = take(L * b * W * 4);
+  l.lvl_score = take(L * b * W * 4);
+  l.lse = take(L * R * 4);
+  l.cand_logp = take(L * R * k * 4);
+  l.cand_ids = take(L * R * k * 4);
+  l.state0 = take(R * h * act_bytes(p.precision));
+  l.state1 = take(R * h * act_bytes(p.precision));
+  l.t = take(R * h * 4);
+  l.a = take(R * h * act_bytes(p.precision));
+  l.z = take(R * V * 4);
+  l.k3 = take(k3);
+  l.total = o;
+  return l;
+}
+
+dartree_status validate(const dartree_params* p) {
+  if (!p) return DARTREE_ERR_INVALID_ARG;
+  if (p->batch < 1 || p->vocab < 1 || p->hidden < 1 || p->depth < 1 || p->width < 1 || p->branch < 1 ||
+      p->budget < 1)
+    return DARTREE_ERR_INVALID_ARG;
+  if (p->branch > p->vocab) return DARTREE_ERR_INVALID_ARG;
+  if (p->precision != DARTREE_FP32 && p->precision != DARTREE_BF16) return DARTREE_ERR_INVALID_ARG;
+  if (!isfinite(p->temperature) || p->temperature < 0.f) return DARTREE_ERR_INVALID_ARG;
+  if (!isfinite(p->depth_bonus) || p->depth_bonus > 0.f) return DARTREE_ERR_INVALID_ARG;
+  if (p->vocab > DARTREE_MAX_VOCAB || p->depth > DARTREE_MAX_DEPTH || p->width > DARTREE_MAX_WIDTH ||
+      p->branch > DARTREE_MAX_BRANCH || p->budget > DARTREE_MAX_SORT)
+    return DARTREE_ERR_UNSUPPORTED;
+  if (p->precision == DARTREE_BF16 && p->hidden % 64 != 0) return DARTREE_ERR_UNSUPPORTED;
+  const Shape s = shape_of(*p);
+  if (s.max_cand > DARTREE_MAX_SORT || s.total > DARTREE_MAX_SORT) return DARTREE_ERR_UNSUPPORTED;
+  // row counts and element offsets must stay within 32-bit grid/row indexing
+  if (int64_t(p->batch) * p->width > (int64_t(1) << 24)) return DARTREE_ERR_UNSUPPORTED;
+  return DARTREE_OK;
+}
+
+dartree_status check_inputs(const dartree_inputs* in) {
+  if (!in || !in->drafter_logits || !in->drafter_hidden || !in->prefix_state || !in->head_A || !in->head_U)
+    return DARTREE_ERR_INVALID_ARG;
+  if (!aligned16(in->drafter_logits) || !aligned16(in->drafter_hidden) || !aligned16(in->prefix_state) ||
+      !aligned16(in->head_A) || !aligned16(in->head_U))
+    return DARTREE_ERR_INVALID_ARG;
+  return DARTREE_OK;
+}
+
+dartree_status check_tree(const dartree_tree* t) {
+  if (!t || !t->tokens || !t->parents || !t->depths || !t->scores || !t->mask || !t->num_nodes)
+    return DARTREE_ERR_INVALID_ARG;
+  if (!aligned16(t->tokens) || !aligned16(t->parents) || !aligned16(t->depths) || !aligned16(t->scores) ||
+      !aligned16(t->mask) || !aligned16(t->num_nodes))
+    return DARTREE_ERR_INVALID_ARG;
+  return DARTREE_OK;
+}
+
+dartree_status check_ws(const dartree_params& p, const void* ws, size_t ws_bytes, Layout* out) {
+  const Layout l = layout_of(p, shape_of(p));
+  if (!ws || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0 || ws_bytes < l.total) return DARTREE_ERR_WORKSPACE;
+  *out = l;
+  return DARTREE_OK;
+}
+
+template <typename T>
+T* at(void* base, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+template <typename T>
+const T* at(const void* base, size_t off) {
+  return reinterpret_cast<const T*>(static_cast<const char*>(base) + off);
+}
+
+dartree_status hip_status(hipError_t e) { return e == hipSuccess ? DARTREE_OK : DARTREE_ERR_HIP; }
+
+LevelShape level_shape(const dartree_params& p, const Shape& s) {
+  LevelShape ls{};
+  ls.depth = p.depth;
+  ls.width = p.width;
+  ls.off[0] = 0;
+  for (int d = 1; d <= p.depth; ++d) {
+    ls.n[d - 1] = int32_t(s.n[d]);
+    ls.off[d] = ls.off[d - 1] + int32_t(s.n[d]);
+  }
+  return ls;
+}
+
+// Enqueue depth d (validated arguments).
+dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, void* ws, const Layout& l,
+                      const Shape& s, hipStream_t st) {
+  const int64_t b = p.batch, V = p.vocab, h = p.hidden, L = p.depth, W = p.width, k = p.branch;
+  const int64_t np = s.n[d - 1], nc = s.n[d];
+  const int64_t R = b * np;  // parent rows of this depth
+  const size_t ab = act_bytes(p.precision);
+  const void* r_in = d == 1 ? in.prefix_state : at<char>(ws, (d - 1) % 2 ? l.state1 : l.state0);
+  void* r_out = at<char>(ws, d % 2 ? l.state1 : l.state0);
+  float* t = at<float>(ws, l.t);
+  void* a = at<char>(ws, l.a);
+  float* z = at<float>(ws, l.z);
+  float* lse = at<float>(ws, l.lse) + (d - 1) * b * W;
+  float* clp = at<float>(ws, l.cand_logp) + (d - 1) * b * W * k;
+  int32_t* cid = at<int32_t>(ws, l.cand_ids) + (d - 1) * b * W * k;
+  int32_t* tok = at<int32_t>(ws, l.lvl_tok) + (d - 1) * b * W;
+  int32_t* par = at<int32_t>(ws, l.lvl_par) + (d - 1) * b * W;
+  float* score = at<float>(ws, l.lvl_score) + (d - 1) * b * W;
+  const float* parent_score = d == 1 ? nullptr : at<float>(ws, l.lvl_score) + (d - 2) * b * W;
+  const float tau = p.temperature > 0.f ? p.temperature : 1.f;
+  const float e = float(sqrt(double(p.hidden)));
+
+  // K1: t = A r, a = act(tanh(t + H_d))
+  ProjArgs head{};
+  head.precision = p.precision;
+  head.epilogue = EPI_HEAD;
+  head.M = R;
+  head.N = h;
+  head.K = h;
+  head.rows_per_group = np;
+  head.x = r_in;
+  head.w = in.head_A;
+  head.bias_act = static_cast<const char*>(in.drafter_hidden) + size_t(d - 1) * h * ab;
+  head.bias_stride = L * h;
+  head.out = t;
+  head.act_out = a;
+  hipError_t err = launch_project(head, st);
+  if (err != hipSuccess) return DARTREE_ERR_HIP;
+
+  // K2: z = L_d^base + U a
+  ProjArgs lg{};
+  lg.precision = p.precision;
+  lg.epilogue = EPI_LOGITS;
+  lg.M = R;
+  lg.N = V;
+  lg.K = h;
+  lg.rows_per_group = np;
+  lg.x = a;
+  lg.w = in.head_U;
+  lg.bias_f32 = in.drafter_logits + size_t(d - 1) * V;
+  lg.bias_stride = L * V;
+  lg.out = z;
+  err = launch_project(lg, st);
+  if (err != hipSuccess) return DARTREE_ERR_HIP;
+
+  // K3: lse and top-k per parent row
+  err = launch_lse_topk(z, R, V, int(k), tau, lse, clp, cid, at<char>(ws, l.k3), st);
+  if (err != hipSuccess) return DARTREE_ERR_HIP;
+
+  // K4: S_d = segmented top-W; level arrays have stride W per request
+  err = launch_select_topw(int(b), int(np), int(k), int(nc), p.depth_bonus, int(W), int(W), parent_score, clp, cid,
+                           tok, par, score, st);
+  if (err != hipSuccess) return DARTREE_ERR_HIP;
+
+  // K5: states of the kept children (unused after the last depth)
+  if (d < p.depth) {
+    err = launch_state_update(p.precision, int(b), int(nc), int(np), int(h), int(W), tok, par, t, in.head_U, e, r_out,
+                             st);
+    if (err != hipSuccess) return DARTREE_ERR_HIP;
+  }
+  return DARTREE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t dartree_abi_version(void) { return DARTREE_ABI_VERSION; }
+
+const char* dartree_status_string(dartree_status status) {
+  switch (status) {
+    case DARTREE_OK: return "ok";
+    case DARTREE_ERR_INVALID_ARG: return "invalid argument";
+    case DARTREE_ERR_UNSUPPORTED: return "unsupported: beyond this library's limits";
+    case DARTREE_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case DARTREE_ERR_HIP: return "HIP kernel launch failed";
+  }
+  return "unknown status";
+}
+
+dartree_status dartree_validate(const dartree_params* p) { return validate(p); }
+
+dartree_status dartree_workspace_size(const dartree_params* p, size_t* bytes) {
+  if (!bytes) return DARTREE_ERR_INVALID_ARG;
+  const dartree_status v = validate(p);
+  if (v != DARTREE_OK) return v;
+  *bytes = layout_of(*p, shape_of(*p)).total;
+  return DARTREE_OK;
+}
+
+dartree_status dartree_expand_depth(const dartree_params* p, const dartree_inputs* in, int32_t d, void* ws,
+                                    size_t ws_bytes, hipStream_t stream) {
+  dartree_status v = validate(p);
+  if (v != DARTREE_OK) return v;
+  if ((v = check_inputs(in)) != DARTREE_OK) return v;
+  if (d < 1 || d > p->depth) return DARTREE_ERR_INVALID_ARG;
+  Layout l;
+  if ((v = check_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
+  return expand(*p, *in, d, ws, l, shape_of(*p), stream);
+}
+
+dartree_status dartree_prune(const dartree_params* p, const void* ws, size_t ws_bytes, const dartree_tree* out,
+                             hipStream_t stream) {
+  dartree_status v = validate(p);
+  if (v != DARTREE_OK) return v;
+  if ((v = check_tree(out)) != DARTREE_OK) return v;
+  Layout l;
+  if ((v = check_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
+  const Shape s = shape_of(*p);
+  return hip_status(launch_prune_emit(p->batch, level_shape(*p, s), p->budget, at<int32_t>(ws, l.lvl_tok),
+                                      at<int32_t>(ws, l.lvl_par), at<float>(ws, l.lvl_score), *out, stream));
+}
+
+dartree_status dartree_build_tree(const dartree_params* p, const dartree_inputs* in, void* ws, size_t ws_bytes,
+                                  const dartree_tree* out, hipStream_t stream) {
+  dartree_status v = validate(p);
+  if (v != DARTREE_OK) return v;
+  if ((v = check_inputs(in)) != DARTREE_OK) return v;
+  if ((v = check_tree(out)) != DARTREE_OK) return v;
+  Layout l;
+  if ((v = check_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
+  const Shape s = shape_of(*p);
+  for (int d = 1; d <= p->depth; ++d)
+    if ((v = expand(*p, *in, d, ws, l, s, stream)) != DARTREE_OK) return v;
+  return hip_status(launch_prune_emit(p->batch, level_shape(*p, s), p->budget, at<int32_t>(ws, l.lvl_tok),
+                                      at<int32_t>(ws, l.lvl_par), at<float>(ws, l.lvl_score), *out, stream));
+}
+
+dartree_status dartree_export_supertree(const dartree_params* p, const void* ws, size_t ws_bytes,
+                                        const dartree_supertree* dst, hipStream_t stream) {
+  dartree_status v = validate(p);
+  if (v != DARTREE_OK) return v;
+  if (!dst) return DARTREE_ERR_INVALID_ARG;
+  Layout l;
+  if ((v = check_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
+  const size_t L = p->depth, b = p->batch, W = p->width, k = p->branch;
+  struct Item { void* to; size_t off; size_t bytes; } items[] = {
+      {dst->tokens, l.lvl_tok, L * b * W * 4},   {dst->parents, l.lvl_par, L * b * W * 4},
+      {dst->scores, l.lvl_score, L * b * W * 4}, {dst->lse, l.lse, L * b * W * 4},
+      {dst->cand_logp, l.cand_logp, L * b * W * k * 4}, {dst->cand_ids, l.cand_ids, L * b * W * k * 4},
+  };
+  for (const Item& it : items)
+    if (it.to && hipMemcpyAsync(it.to, at<char>(ws, it.off), it.bytes, hipMemcpyDeviceToDevice, stream) != hipSuccess)
+      return DARTREE_ERR_HIP;
+  return DARTREE_OK;
+}
+
+dartree_status dartree_project(int32_t precision, int32_t rows, int32_t vocab, int32_t hidden, int32_t rows_per_group,
+                               const void* x, const void* U, const float* bias, int64_t bias_stride, float* z,
+                               hipStream_t stream) {
+  if (precision != DARTREE_FP32 && precision != DARTREE_BF16) return DARTREE_ERR_INVALID_ARG;
+  if (rows < 1 || vocab < 1 || hidden < 1 || rows_per_group < 1 || bias_stride < 0) return DARTREE_ERR_INVALID_ARG;
+  if (!x || !U || !bias || !z || !aligned16(x) || !aligned16(U) || !aligned16(z)) return DARTREE_ERR_INVALID_ARG;
+  if (precision == DARTREE_BF16 && hidden % 64 != 0) return DARTREE_ERR_UNSUPPORTED;
+  ProjArgs a{};
+  a.precision = precision;
+  a.epilogue = EPI_LOGITS;
+  a.M = rows;
+  a.N = vocab;
+  a.K = hidden;
+  a.rows_per_group = rows_per_group;
+  a.x = x;
+  a.w = U;
+  a.bias_f32 = bias;
+  a.bias_stride = bias_stride;
+  a.out = z;
+  return hip_status(launch_project(a, stream));
+}
+
+dartree_status dartree_lse_topk_workspace_size(int32_t rows, int32_t vocab, int32_t k, size_t* bytes) {
+  if (!bytes || rows < 1 || vocab < 1 || k < 1 || k > vocab) return DARTREE_ERR_INVALID_ARG;
+  if (k > DARTREE_MAX_BRANCH || vocab > DARTREE_MAX_VOCAB) return DARTREE_ERR_UNSUPPORTED;
+  *bytes = lse_topk_scratch_bytes(rows, vocab, k);
+  return DARTREE_OK;
+}
+
+dartree_status dartree_lse_topk(const float* z, int32_t rows, int32_t vocab, int32_t k, float temperature, float* lse,
+                                float* cand_logp, int32_t* cand_ids, void* ws, size_t ws_bytes, hipStream_t stream) {
+  size_t need = 0;
+  dartree_status v = dartree_lse_topk_workspace_size(rows, vocab, k, &need);
+  if (v != DARTREE_OK) return v;
+  if (!isfinite(temperature) || temperature < 0.f) return DARTREE_ERR_INVALID_ARG;
+  if (!z || !lse || !cand_logp || !cand_ids) return DARTREE_ERR_INVALID_ARG;
+  if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return DARTREE_ERR_WORKSPACE;
+  const float tau = temperature > 0.f ? temperature : 1.f;
+  return hip_status(launch_lse_topk(z, rows, vocab, k, tau, lse, cand_logp, cand_ids, ws, stream));
+}
+
+dartree_status dartree_select_topw(int32_t batch, int32_t n_parent, int32_t k, int32_t n_keep, float depth_bonus,
+                                   const float* parent_score, const float* cand_logp, const int32_t* cand_ids,
+                                   int32_t* out_tokens, int32_t* out_parents, float* out_scores, hipStream_t stream) {
+  if (batch < 1 || n_parent < 1 || k < 1 || n_keep < 1) return DARTREE_ERR_INVALID_ARG;
+  if (int64_t(n_parent) * k > DARTREE_MAX_SORT) return DARTREE_ERR_UNSUPPORTED;
+  if (n_keep > n_parent * k) return DARTREE_ERR_INVALID_ARG;
+  if (!isfinite(depth_bonus) || depth_bonus > 0.f) return DARTREE_ERR_INVALID_ARG;
+  if (!cand_logp || !cand_ids || !out_tokens || !out_parents || !out_scores) return DARTREE_ERR_INVALID_ARG;
+  return hip_status(launch_select_topw(batch, n_parent, k, n_keep, depth_bonus, n_parent, n_keep, parent_score,
+                                       cand_logp, cand_ids, out_tokens, out_parents, out_scores, stream));
+}
+
+dartree_status dartree_prune_levels(const dartree_params* p, const int32_t* tokens, const int32_t* parents,
+                                    const float* scores, const dartree_tree* out, hipStream_t stream) {
+  dartree_status v = validate(p);
+  if (v != DARTREE_OK) return v;
+  if ((v = check_tree(out)) != DARTREE_OK) return v;
+  if (!tokens || !parents || !scores) return DARTREE_ERR_INVALID_ARG;
+  const Shape s = shape_of(*p);
+  return hip_status(
+      launch_prune_emit(p->batch, level_shape(*p, s), p->budget, tokens, parents, scores, *out, stream));
+}
+
+}  // extern "C"

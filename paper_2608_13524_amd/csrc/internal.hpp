@@ -1,0 +1,93 @@
+// Internal declarations shared by the libdartree kernels and the C ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dartree.h"
+
+namespace dartree {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// bfloat16 <-> fp32 on raw 16-bit patterns (finite values; nearest-even).
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return uint16_t(u >> 16);
+}
+
+// Order-preserving map of an fp32 score to a key that sorts ascending for
+// descending scores (-0 and +0 are the same score).
+__device__ __forceinline__ uint32_t score_desc_key(float s) {
+  uint32_t u = __float_as_uint(s + 0.0f);
+  uint32_t asc = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ~asc;
+}
+__device__ __forceinline__ float score_from_desc_key(uint32_t k) {
+  uint32_t asc = ~k;
+  uint32_t u = (asc & 0x80000000u) ? (asc & 0x7FFFFFFFu) : ~asc;
+  return __uint_as_float(u);
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (host side).  They assume validated arguments.
+// ---------------------------------------------------------------------------
+
+// out[m][n] = epilogue(bias, sum_k x[m][k] * w[n][k]); row m belongs to group
+// m / rows_per_group, whose bias row starts at bias + group * bias_stride.
+enum ProjEpilogue {
+  EPI_LOGITS = 0,  // out (fp32) = acc + bias_f32
+  EPI_HEAD = 1     // out (fp32) = acc ; act_out = act(tanh(acc + bias_act))
+};
+
+struct ProjArgs {
+  int precision;
+  int epilogue;
+  int64_t M, N, K;
+  int64_t rows_per_group;
+  const void* x;         // act [M][K]
+  const void* w;         // act [N][K]
+  const float* bias_f32; // EPI_LOGITS
+  const void* bias_act;  // EPI_HEAD
+  int64_t bias_stride;   // elements between consecutive group bias rows
+  float* out;            // fp32 [M][N]
+  void* act_out;         // EPI_HEAD: act [M][N]
+};
+hipError_t launch_project(const ProjArgs& a, hipStream_t s);
+
+// Row-wise online log-sum-exp and top-k (K3).
+size_t lse_topk_scratch_bytes(int64_t rows, int64_t vocab, int k);
+hipError_t launch_lse_topk(const float* z, int64_t rows, int64_t vocab, int k, float tau,
+                           float* lse, float* cand_logp, int32_t* cand_ids, void* scratch,
+                           hipStream_t s);
+
+// Segmented top-W over n_parent * k candidates per request (K4).
+// Parent scores of request q start at parent_score + q * parent_stride (NULL:
+// all zero); outputs of request q at out + q * out_stride.
+hipError_t launch_select_topw(int batch, int n_parent, int k, int n_keep, float beta,
+                              int parent_stride, int out_stride,
+                              const float* parent_score, const float* cand_logp,
+                              const int32_t* cand_ids, int32_t* out_tok, int32_t* out_par,
+                              float* out_score, hipStream_t s);
+
+// State update of the kept children (K5); level entries of request q start at
+// q * lvl_stride.
+hipError_t launch_state_update(int precision, int batch, int n_child, int n_parent, int hidden, int lvl_stride,
+                               const int32_t* lvl_tok, const int32_t* lvl_par, const float* t,
+                               const void* U, float e, void* r_out, hipStream_t s);
+
+// Deferred top-B prune and tree emission (K6).
+struct LevelShape {
+  int32_t depth;
+  int32_t width;
+  int32_t n[DARTREE_MAX_DEPTH];     // n_d, d = 1..L at index d-1
+  int32_t off[DARTREE_MAX_DEPTH + 1];  // prefix sums of n
+};
+hipError_t launch_prune_emit(int batch, const LevelShape& shape, int budget,
+                             const int32_t* lvl_tok, const int32_t* lvl_par,
+                             const float* lvl_score, const dartree_tree& out, hipStream_t s);
+
+}  // namespace dartree

@@ -1,0 +1,312 @@
+// Log-softmax normaliser and per-row top-k of the corrected logits (Algorithm
+// 1: log q~_d over the vocabulary, then the k best candidate children of each
+// node).  One read of z:
+//   * each thread streams float4s of its row segment, keeping an online
+//     (max, sum of exp((z - max) / tau)) pair and a sorted top-K list in
+//     registers (insertion only when a value beats the current K-th);
+//   * the block merges with wavefront butterflies: (max, sum) pairs combine,
+//     and the top-k is taken in k rounds of a (value desc, id asc) arg-max
+//     across lanes, the winning lane shifting its list;
+//   * rows are split into segments when there are too few rows to fill the
+//     chip; a second kernel merges the per-segment partials in segment order.
+// Ties: ids ascend along every thread's traversal, so "strictly greater"
+// keeps the lower id first; every merge compares (value desc, id asc).
+#include <float.h>
+
+#include "internal.hpp"
+
+namespace dartree {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr float kLog2e = 1.4426950408889634f;
+
+struct Partial {
+  float m;  // running max of z
+  float s;  // sum of exp((z - m) / tau)
+};
+
+__device__ __forceinline__ bool better(float v, int i, float w, int j) {
+  return v > w || (v == w && i < j);
+}
+
+__device__ __forceinline__ Partial combine(Partial a, Partial b, float scale) {
+  // scale = log2(e) / tau.  exp2(-inf) = 0 handles an empty side.
+  const float m = fmaxf(a.m, b.m);
+  if (m == -INFINITY) return Partial{m, 0.f};
+  return Partial{m, a.s * exp2f((a.m - m) * scale) + b.s * exp2f((b.m - m) * scale)};
+}
+
+template <int K>
+__device__ __forceinline__ void insert(float v, int id, float (&tv)[K], int (&ti)[K]) {
+  if (!better(v, id, tv[K - 1], ti[K - 1])) return;
+  tv[K - 1] = v;
+  ti[K - 1] = id;
+#pragma unroll
+  for (int j = K - 1; j > 0; --j) {
+    if (better(tv[j], ti[j], tv[j - 1], ti[j - 1])) {
+      const float fv = tv[j]; tv[j] = tv[j - 1]; tv[j - 1] = fv;
+      const int fi = ti[j]; ti[j] = ti[j - 1]; ti[j - 1] = fi;
+    }
+  }
+}
+
+__device__ __forceinline__ Partial wave_combine(Partial p, float scale) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    Partial o{__shfl_xor(p.m, off), __shfl_xor(p.s, off)};
+    p = combine(p, o, scale);
+  }
+  return p;
+}
+
+// k rounds of arg-max over the heads of each lane's sorted list.  On return
+// every lane holds the wave's top-k in (out_v, out_i) (lane-uniform).
+template <int K>
+__device__ __forceinline__ void wave_topk(float (&tv)[K], int (&ti)[K], int k, float (&out_v)[K],
+                                          int (&out_i)[K]) {
+#pragma unroll
+  for (int r = 0; r < K; ++r) {
+    float v = tv[0];
+    int i = ti[0];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const float ov = __shfl_xor(v, off);
+      const int oi = __shfl_xor(i, off);
+      if (better(ov, oi, v, i)) { v = ov; i = oi; }
+    }
+    out_v[r] = r < k ? v : -INFINITY;
+    out_i[r] = r < k ? i : INT32_MAX;
+    if (r < k && ti[0] == i && tv[0] == v) {  // ids are unique: this lane supplied the winner
+#pragma unroll
+      for (int j = 0; j < K - 1; ++j) { tv[j] = tv[j + 1]; ti[j] = ti[j + 1]; }
+      tv[K - 1] = -INFINITY;
+      ti[K - 1] = INT32_MAX;
+    }
+  }
+}
+
+// Block-wide merge of per-thread (Partial, top-K); result valid in thread 0's
+// registers (and in every lane of wave 0).
+template <int K>
+__device__ void block_merge(Partial& p, float (&tv)[K], int (&ti)[K], int k, float scale,
+                            float (&res_v)[K], int (&res_i)[K]) {
+  __shared__ Partial sp[kBlock / 64];
+  __shared__ float sv[kBlock / 64][K];
+  __shared__ int si[kBlock / 64][K];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  p = wave_combine(p, scale);
+  float wv[K];
+  int wi[K];
+#pragma unroll
+  for (int r = 0; r < K; ++r) { wv[r] = -INFINITY; wi[r] = INT32_MAX; }
+  wave_topk<K>(tv, ti, k, wv, wi);
+  if (lane == 0) {
+    sp[wave] = p;
+#pragma unroll
+    for (int r = 0; r < K; ++r) { sv[wave][r] = wv[r]; si[wave][r] = wi[r]; }
+  }
+  __syncthreads();
+  if (wave == 0) {
+    Partial q{-INFINITY, 0.f};
+    for (int w = 0; w < kBlock / 64; ++w) q = combine(q, sp[w], scale);  // fixed order
+    p = q;
+    // lanes 0..3 hold the four wave lists; other lanes are empty
+#pragma unroll
+    for (int r = 0; r < K; ++r) {
+      tv[r] = lane < kBlock / 64 ? sv[lane][r] : -INFINITY;
+      ti[r] = lane < kBlock / 64 ? si[lane][r] : INT32_MAX;
+    }
+#pragma unroll
+    for (int r = 0; r < K; ++r) { res_v[r] = -INFINITY; res_i[r] = INT32_MAX; }
+    wave_topk<K>(tv, ti, k, res_v, res_i);
+  }
+}
+
+template <int K>
+__device__ __forceinline__ void finalize(int64_t row, Partial p, const float (&v)[K], const int (&id)[K],
+                                         int k, float tau, float* lse, float* cand_logp,
+                                         int32_t* cand_ids) {
+  const float log_s = logf(p.s);
+  lse[row] = p.m / tau + log_s;
+#pragma unroll
+  for (int r = 0; r < K; ++r) {
+    if (r < k) {
+      cand_logp[row * k + r] = (v[r] - p.m) / tau - log_s;
+      cand_ids[row * k + r] = id[r];
+    }
+  }
+}
+
+constexpr int kChunk = 4;  // float4 loads in flight per thread
+
+// grid: rows * nseg blocks, block = row * nseg + segment.  Writes the final
+// result when nseg == 1, otherwise the segment's partial.
+template <int K, bool VEC>
+__global__ __launch_bounds__(kBlock) void lse_topk_partial(const float* __restrict__ z, int vocab,
+                                                           int nseg, int seg_len, int k, float tau,
+                                                           float* lse, float* cand_logp,
+                                                           int32_t* cand_ids, float* part) {
+  // per-thread staging row for the (rare) chunks that reach the top-K list
+  __shared__ float stage[kBlock][4 * kChunk + 1];
+  const int64_t row = blockIdx.x / nseg;
+  const int seg = blockIdx.x % nseg;
+  const int v0 = seg * seg_len;
+  const int v1 = min(vocab, v0 + seg_len);
+  const float* zr = z + row * int64_t(vocab);
+  const float scale = kLog2e / tau;
+  const int tid = threadIdx.x;
+
+  Partial p{-INFINITY, 0.f};
+  float tv[K];
+  int ti[K];
+#pragma unroll
+  for (int r = 0; r < K; ++r) { tv[r] = -INFINITY; ti[r] = INT32_MAX; }
+
+  if constexpr (VEC) {
+    // Thread tid visits, per iteration, float4 c at base + 4 kBlock c: ids
+    // ascend along the traversal.  The first float4 of an iteration is always
+    // in range, so the running max is finite before any -inf padding is summed.
+    for (int base = v0 + 4 * tid; base < v1; base += 4 * kBlock * kChunk) {
+      f32x4 x[kChunk];
+#pragma unroll
+      for (int c = 0; c < kChunk; ++c) {
+        const int v = base + 4 * kBlock * c;
+        x[c] = v < v1 ? *reinterpret_cast<const f32x4*>(zr + v) : f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int c = 0; c < kChunk; ++c) mx = fmaxf(mx, fmaxf(fmaxf(x[c][0], x[c][1]), fmaxf(x[c][2], x[c][3])));
+      if (mx > p.m) {
+        p.s *= exp2f((p.m - mx) * scale);
+        p.m = mx;
+      }
+      float acc = 0.f;
+#pragma unroll
+      for (int c = 0; c < kChunk; ++c)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc += exp2f((x[c][i] - p.m) * scale);
+      p.s += acc;
+      if (mx > tv[K - 1]) {
+#pragma unroll
+        for (int c = 0; c < kChunk; ++c)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) stage[tid][4 * c + i] = x[c][i];
+#pragma unroll 1
+        for (int j = 0; j < 4 * kChunk; ++j) {
+          const float xv = stage[tid][j];
+          if (xv > tv[K - 1]) insert<K>(xv, base + 4 * kBlock * (j >> 2) + (j & 3), tv, ti);
+        }
+      }
+    }
+  } else {
+#pragma unroll 1
+    for (int v = v0 + tid; v < v1; v += kBlock) {
+      const float x = zr[v];
+      if (x > p.m) {
+        p.s *= exp2f((p.m - x) * scale);
+        p.m = x;
+      }
+      p.s += exp2f((x - p.m) * scale);
+      if (x > tv[K - 1]) insert<K>(x, v, tv, ti);
+    }
+  }
+
+  float rv[K];
+  int ri[K];
+  block_merge<K>(p, tv, ti, k, scale, rv, ri);
+  if (tid != 0) return;
+  if (nseg == 1) {
+    finalize<K>(row, p, rv, ri, k, tau, lse, cand_logp, cand_ids);
+    return;
+  }
+  // partial record: m, s, then k values, then k ids (as int bits)
+  float* rec = part + (row * nseg + seg) * int64_t(2 + 2 * k);
+  rec[0] = p.m;
+  rec[1] = p.s;
+#pragma unroll
+  for (int r = 0; r < K; ++r) {
+    if (r < k) {
+      rec[2 + r] = rv[r];
+      rec[2 + k + r] = __int_as_float(ri[r]);
+    }
+  }
+}
+
+// One wave per row: merge the row's segment partials in segment order.
+template <int K>
+__global__ __launch_bounds__(64) void lse_topk_merge(int nseg, int k, float tau, const float* part,
+                                                     float* lse, float* cand_logp, int32_t* cand_ids) {
+  const int64_t row = blockIdx.x;
+  const int lane = threadIdx.x;
+  const float scale = kLog2e / tau;
+  Partial p{-INFINITY, 0.f};
+  float tv[K];
+  int ti[K];
+#pragma unroll
+  for (int r = 0; r < K; ++r) { tv[r] = -INFINITY; ti[r] = INT32_MAX; }
+  for (int sgi = lane; sgi < nseg; sgi += 64) {
+    const float* rec = part + (row * nseg + sgi) * int64_t(2 + 2 * k);
+    p = combine(p, Partial{rec[0], rec[1]}, scale);
+#pragma unroll 1
+    for (int r = 0; r < k; ++r) insert<K>(rec[2 + r], __float_as_int(rec[2 + k + r]), tv, ti);
+  }
+  p = wave_combine(p, scale);
+  float rv[K];
+  int ri[K];
+#pragma unroll
+  for (int r = 0; r < K; ++r) { rv[r] = -INFINITY; ri[r] = INT32_MAX; }
+  wave_topk<K>(tv, ti, k, rv, ri);
+  if (lane == 0) finalize<K>(row, p, rv, ri, k, tau, lse, cand_logp, cand_ids);
+}
+
+// Segments per row: enough blocks to fill 256 CUs a few times over, but no
+// segment shorter than 2048 elements.
+int num_segments(int64_t rows, int64_t vocab) {
+  const int64_t want = (2048 + rows - 1) / rows;
+  const int64_t most = (vocab + 2047) / 2048;
+  return int(std::max<int64_t>(1, std::min(want, most)));
+}
+
+template <int K>
+hipError_t launch_k(const float* z, int64_t rows, int64_t vocab, int k, float tau, float* lse,
+                    float* cand_logp, int32_t* cand_ids, float* part, hipStream_t s) {
+  const int nseg = num_segments(rows, vocab);
+  const bool vec = (vocab % 4) == 0 && (reinterpret_cast<uintptr_t>(z) % 16) == 0;
+  int seg_len = int((vocab + nseg - 1) / nseg);
+  if (vec) seg_len = (seg_len + 3) & ~3;
+  const dim3 grid(unsigned(rows * nseg));
+  if (vec)
+    hipLaunchKernelGGL((lse_topk_partial<K, true>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
+                       tau, lse, cand_logp, cand_ids, part);
+  else
+    hipLaunchKernelGGL((lse_topk_partial<K, false>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
+                       tau, lse, cand_logp, cand_ids, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || nseg == 1) return e;
+  hipLaunchKernelGGL((lse_topk_merge<K>), dim3(unsigned(rows)), dim3(64), 0, s, nseg, k, tau, part, lse,
+                     cand_logp, cand_ids);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t lse_topk_scratch_bytes(int64_t rows, int64_t vocab, int k) {
+  const int nseg = num_segments(rows, vocab);
+  if (nseg == 1) return 0;
+  return size_t(rows) * nseg * (2 + 2 * size_t(k)) * sizeof(float);
+}
+
+hipError_t launch_lse_topk(const float* z, int64_t rows, int64_t vocab, int k, float tau, float* lse,
+                           float* cand_logp, int32_t* cand_ids, void* scratch, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  float* part = static_cast<float*>(scratch);
+  if (k <= 1) return launch_k<1>(z, rows, vocab, k, tau, lse, cand_logp, cand_ids, part, s);
+  if (k <= 2) return launch_k<2>(z, rows, vocab, k, tau, lse, cand_logp, cand_ids, part, s);
+  if (k <= 4) return launch_k<4>(z, rows, vocab, k, tau, lse, cand_logp, cand_ids, part, s);
+  if (k <= 8) return launch_k<8>(z, rows, vocab, k, tau, lse, cand_logp, cand_ids, part, s);
+  if (k <= 16) return launch_k<16>(z, rows, vocab, k, tau, lse, cand_logp, cand_ids, part, s);
+  return launch_k<32>(z, rows, vocab, k, tau, lse, cand_logp, cand_ids, part, s);
+}
+
+}  // namespace dartree

@@ -1,0 +1,307 @@
+"""ctypes binding of libdartree (the C ABI in include/dartree.h).
+
+Argument marshalling only: every step of tree construction runs in the HIP
+kernels of ``libdartree.so``.  PyTorch supplies device memory and the stream.
+If the library has not been built, :func:`lib` raises; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libdartree.so")
+
+FP32 = 0
+BF16 = 1
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
+
+MAX_VOCAB = 1 << 20
+MAX_DEPTH = 64
+MAX_WIDTH = 2048
+MAX_BRANCH = 32
+MAX_SORT = 4096
+
+SYMBOLS = [
+    "dartree_abi_version", "dartree_status_string", "dartree_validate",
+    "dartree_workspace_size", "dartree_expand_depth", "dartree_prune",
+    "dartree_build_tree", "dartree_export_supertree", "dartree_project",
+    "dartree_lse_topk_workspace_size", "dartree_lse_topk", "dartree_select_topw",
+    "dartree_prune_levels",
+]
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("vocab", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("depth", ctypes.c_int32), ("width", ctypes.c_int32), ("branch", ctypes.c_int32),
+                ("budget", ctypes.c_int32), ("precision", ctypes.c_int32),
+                ("temperature", ctypes.c_float), ("depth_bonus", ctypes.c_float)]
+
+    @staticmethod
+    def of(cfg) -> "Params":
+        return Params(cfg.batch, cfg.vocab, cfg.hidden, cfg.depth, cfg.width, cfg.branch,
+                      cfg.budget, cfg.precision, float(cfg.temperature), float(cfg.depth_bonus))
+
+    def level_sizes(self) -> list[int]:
+        n, out = 1, []
+        for _ in range(self.depth):
+            n = min(self.width, n * self.branch)
+            out.append(n)
+        return out
+
+
+class InputsC(ctypes.Structure):
+    _fields_ = [("drafter_logits", ctypes.c_void_p), ("drafter_hidden", ctypes.c_void_p),
+                ("prefix_state", ctypes.c_void_p), ("head_A", ctypes.c_void_p),
+                ("head_U", ctypes.c_void_p)]
+
+
+class TreeC(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.c_void_p), ("parents", ctypes.c_void_p), ("depths", ctypes.c_void_p),
+                ("scores", ctypes.c_void_p), ("mask", ctypes.c_void_p), ("num_nodes", ctypes.c_void_p)]
+
+
+class SupertreeC(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.c_void_p), ("parents", ctypes.c_void_p), ("scores", ctypes.c_void_p),
+                ("lse", ctypes.c_void_p), ("cand_logp", ctypes.c_void_p), ("cand_ids", ctypes.c_void_p)]
+
+
+class DartreeError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded HIP library.  Raises if it is missing: build it first with
+    ``python -m paper_2608_13524_amd.build``."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: the HIP library must be built "
+                           "(python -m paper_2608_13524_amd.build); there is no fallback path")
+    L = ctypes.CDLL(LIB_PATH)
+    P, vp, i32, i64, f32, sz = (ctypes.POINTER(Params), ctypes.c_void_p, ctypes.c_int32,
+                                ctypes.c_int64, ctypes.c_float, ctypes.c_size_t)
+    L.dartree_abi_version.restype = i32
+    L.dartree_abi_version.argtypes = []
+    L.dartree_status_string.restype = ctypes.c_char_p
+    L.dartree_status_string.argtypes = [ctypes.c_int]
+    L.dartree_validate.argtypes = [P]
+    L.dartree_workspace_size.argtypes = [P, ctypes.POINTER(sz)]
+    L.dartree_expand_depth.argtypes = [P, ctypes.POINTER(InputsC), i32, vp, sz, vp]
+    L.dartree_prune.argtypes = [P, vp, sz, ctypes.POINTER(TreeC), vp]
+    L.dartree_build_tree.argtypes = [P, ctypes.POINTER(InputsC), vp, sz, ctypes.POINTER(TreeC), vp]
+    L.dartree_export_supertree.argtypes = [P, vp, sz, ctypes.POINTER(SupertreeC), vp]
+    L.dartree_project.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, i64, vp, vp]
+    L.dartree_lse_topk_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(sz)]
+    L.dartree_lse_topk.argtypes = [vp, i32, i32, i32, f32, vp, vp, vp, vp, sz, vp]
+    L.dartree_select_topw.argtypes = [i32, i32, i32, i32, f32, vp, vp, vp, vp, vp, vp, vp]
+    L.dartree_prune_levels.argtypes = [P, vp, vp, vp, ctypes.POINTER(TreeC), vp]
+    for name in SYMBOLS:
+        if name not in ("dartree_abi_version", "dartree_status_string"):
+            getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return lib().dartree_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != OK:
+        raise DartreeError(status, where)
+
+
+def _ptr(t) -> Optional[int]:
+    """Device address of a tensor (None for None)."""
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+# ---------------------------------------------------------------------------
+# Host-only calls
+# ---------------------------------------------------------------------------
+
+def abi_version() -> int:
+    return lib().dartree_abi_version()
+
+
+def validate(p: Params) -> int:
+    return lib().dartree_validate(None if p is None else ctypes.byref(p))
+
+
+def workspace_size(p: Params) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().dartree_workspace_size(ctypes.byref(p), ctypes.byref(n)), "dartree_workspace_size")
+    return n.value
+
+
+def lse_topk_workspace_size(rows: int, vocab: int, k: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().dartree_lse_topk_workspace_size(rows, vocab, k, ctypes.byref(n)),
+           "dartree_lse_topk_workspace_size")
+    return n.value
+
+
+# ---------------------------------------------------------------------------
+# Device buffers (torch allocations: plumbing only)
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class DeviceInputs:
+    Lb: object
+    H: object
+    r0: object
+    A: object
+    U: object
+
+    def c(self) -> InputsC:
+        return InputsC(_ptr(self.Lb), _ptr(self.H), _ptr(self.r0), _ptr(self.A), _ptr(self.U))
+
+    @staticmethod
+    def from_host(inputs, device="cuda") -> "DeviceInputs":
+        """Copy host inputs (numpy; bf16 given as uint16 bit patterns) to the device."""
+        import numpy as np
+        import torch
+
+        def dev(x):
+            x = np.ascontiguousarray(x)
+            if x.dtype == np.uint16:
+                x = x.view(np.int16)
+            return torch.from_numpy(x).to(device)
+
+        return DeviceInputs(dev(inputs.Lb), dev(inputs.H), dev(inputs.r0), dev(inputs.A), dev(inputs.U))
+
+
+@dataclasses.dataclass
+class DeviceTree:
+    tokens: object
+    parents: object
+    depths: object
+    scores: object
+    mask: object
+    num_nodes: object
+
+    def c(self) -> TreeC:
+        return TreeC(_ptr(self.tokens), _ptr(self.parents), _ptr(self.depths), _ptr(self.scores),
+                     _ptr(self.mask), _ptr(self.num_nodes))
+
+    @staticmethod
+    def alloc(batch: int, budget: int, device="cuda") -> "DeviceTree":
+        import torch
+        words = (budget + 63) // 64
+        i32 = dict(dtype=torch.int32, device=device)
+        return DeviceTree(torch.empty(batch, budget, **i32), torch.empty(batch, budget, **i32),
+                          torch.empty(batch, budget, **i32),
+                          torch.empty(batch, budget, dtype=torch.float32, device=device),
+                          torch.empty(batch, budget, words, dtype=torch.int64, device=device),
+                          torch.empty(batch, **i32))
+
+    def host(self) -> dict:
+        """Numpy copies (mask as uint64)."""
+        import numpy as np
+        out = {f.name: getattr(self, f.name).cpu().numpy() for f in dataclasses.fields(self)}
+        out["mask"] = out["mask"].view(np.uint64)
+        return out
+
+
+@dataclasses.dataclass
+class DeviceSupertree:
+    tokens: object
+    parents: object
+    scores: object
+    lse: object
+    cand_logp: object
+    cand_ids: object
+
+    def c(self) -> SupertreeC:
+        return SupertreeC(*(_ptr(getattr(self, f.name)) for f in dataclasses.fields(self)))
+
+    @staticmethod
+    def alloc(p: Params, device="cuda") -> "DeviceSupertree":
+        import torch
+        L, b, W, k = p.depth, p.batch, p.width, p.branch
+        i32 = dict(dtype=torch.int32, device=device)
+        f32 = dict(dtype=torch.float32, device=device)
+        return DeviceSupertree(torch.empty(L, b, W, **i32), torch.empty(L, b, W, **i32),
+                               torch.empty(L, b, W, **f32), torch.empty(L, b * W, **f32),
+                               torch.empty(L, b * W, k, **f32), torch.empty(L, b * W, k, **i32))
+
+    def host(self) -> dict:
+        return {f.name: getattr(self, f.name).cpu().numpy() for f in dataclasses.fields(self)}
+
+
+def alloc_workspace(p: Params, device="cuda"):
+    import torch
+    # torch's caching allocator returns blocks aligned to at least 512 bytes
+    return torch.empty(max(workspace_size(p), 1), dtype=torch.uint8, device=device)
+
+
+# ---------------------------------------------------------------------------
+# Device calls (enqueued on `stream`, default: torch's current stream)
+# ---------------------------------------------------------------------------
+
+def build_tree(p: Params, inputs: DeviceInputs, ws, out: DeviceTree, stream=None) -> None:
+    ic, tc = inputs.c(), out.c()
+    _check(lib().dartree_build_tree(ctypes.byref(p), ctypes.byref(ic), _ptr(ws), ws.numel(),
+                                    ctypes.byref(tc), _stream(stream)), "dartree_build_tree")
+
+
+def expand_depth(p: Params, inputs: DeviceInputs, d: int, ws, stream=None) -> None:
+    ic = inputs.c()
+    _check(lib().dartree_expand_depth(ctypes.byref(p), ctypes.byref(ic), d, _ptr(ws), ws.numel(),
+                                      _stream(stream)), "dartree_expand_depth")
+
+
+def prune(p: Params, ws, out: DeviceTree, stream=None) -> None:
+    tc = out.c()
+    _check(lib().dartree_prune(ctypes.byref(p), _ptr(ws), ws.numel(), ctypes.byref(tc), _stream(stream)),
+           "dartree_prune")
+
+
+def export_supertree(p: Params, ws, dst: DeviceSupertree, stream=None) -> None:
+    sc = dst.c()
+    _check(lib().dartree_export_supertree(ctypes.byref(p), _ptr(ws), ws.numel(), ctypes.byref(sc),
+                                          _stream(stream)), "dartree_export_supertree")
+
+
+def project(precision: int, x, U, bias, bias_stride: int, z, rows_per_group: int, stream=None) -> None:
+    rows, hidden = x.shape
+    vocab = U.shape[0]
+    _check(lib().dartree_project(precision, rows, vocab, hidden, rows_per_group, _ptr(x), _ptr(U), _ptr(bias),
+                                 bias_stride, _ptr(z), _stream(stream)), "dartree_project")
+
+
+def lse_topk(z, k: int, temperature: float, lse, cand_logp, cand_ids, ws=None, stream=None) -> None:
+    rows, vocab = z.shape
+    _check(lib().dartree_lse_topk(_ptr(z), rows, vocab, k, temperature, _ptr(lse), _ptr(cand_logp),
+                                  _ptr(cand_ids), _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)),
+           "dartree_lse_topk")
+
+
+def select_topw(batch: int, n_parent: int, k: int, n_keep: int, depth_bonus: float, parent_score,
+                cand_logp, cand_ids, out_tokens, out_parents, out_scores, stream=None) -> None:
+    _check(lib().dartree_select_topw(batch, n_parent, k, n_keep, depth_bonus, _ptr(parent_score),
+                                     _ptr(cand_logp), _ptr(cand_ids), _ptr(out_tokens), _ptr(out_parents),
+                                     _ptr(out_scores), _stream(stream)), "dartree_select_topw")
+
+
+def prune_levels(p: Params, tokens, parents, scores, out: DeviceTree, stream=None) -> None:
+    tc = out.c()
+    _check(lib().dartree_prune_levels(ctypes.byref(p), _ptr(tokens), _ptr(parents), _ptr(scores),
+                                      ctypes.byref(tc), _stream(stream)), "dartree_prune_levels")

@@ -1,0 +1,46 @@
+"""Helpers for the GPU tests: run the HIP path on host inputs and copy back."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from paper_2608_13524_amd import dartree as D
+
+
+def device():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    return torch.device("cuda:0")
+
+
+def say(msg: str) -> None:
+    """Name the case before a GPU step (visible even if the process dies)."""
+    print(f"[gpu] {msg}", file=sys.stderr, flush=True)
+
+
+def run_build(cfg, inputs, export=True):
+    """dartree_build_tree on cuda:0; returns (tree dict, supertree dict, params)."""
+    dev = device()
+    p = D.Params.of(cfg)
+    di = D.DeviceInputs.from_host(inputs, dev)
+    ws = D.alloc_workspace(p, dev)
+    out = D.DeviceTree.alloc(cfg.batch, cfg.budget, dev)
+    say(f"build_tree {cfg.name} b={cfg.batch} V={cfg.vocab} h={cfg.hidden} L={cfg.depth} "
+        f"W={cfg.width} k={cfg.branch} B={cfg.budget} T={cfg.temperature}")
+    D.build_tree(p, di, ws, out)
+    sup = None
+    if export:
+        st = D.DeviceSupertree.alloc(p, dev)
+        D.export_supertree(p, ws, st)
+        torch.cuda.synchronize()
+        sup = st.host()
+    torch.cuda.synchronize()
+    return out.host(), sup, p
+
+
+def to_dev(a: np.ndarray):
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).to(device())

@@ -1,0 +1,159 @@
+"""Replay comparator: run the oracle along the GPU's choices and check them.
+
+Exact parity is not well defined where two candidates' scores differ by less
+than the arithmetic noise (fp32 accumulation on the GPU, fp64 in the oracle).
+So, at every selection the GPU made (each parent's top-k, each depth's
+top-W, the final top-B), the oracle recomputes the values in fp64 along the
+GPU's tree and requires:
+
+  every chosen item's oracle value >= the best unchosen item's value - EPS
+
+(EPS = 1e-3, in log-probability units for top-k and score units otherwise).
+A differing set within that window is a near-tie event: the oracle adopts
+the GPU's set and continues.  A larger gap fails.  Afterwards the emitted
+arrays (tokens, parents, depths, mask, node counts) must equal the oracle's
+flattening of the followed supertree bit for bit, and every score must agree
+within SCORE_TOL (2e-2 absolute).  With no near-tie events this is plain
+equality with the free-running oracle.
+"""
+from __future__ import annotations
+
+import dataclasses
+
+import numpy as np
+
+import oracle.dartree_ref as R
+
+EPS = 1e-3
+SCORE_TOL = 2e-2
+
+
+@dataclasses.dataclass
+class Report:
+    topk_events: int = 0
+    topw_events: int = 0
+    topb_events: int = 0
+    max_logp_err: float = 0.0
+    max_lse_err: float = 0.0
+    max_score_err: float = 0.0
+    checked_rows: int = 0
+
+    @property
+    def events(self) -> int:
+        return self.topk_events + self.topw_events + self.topb_events
+
+
+class ParityError(AssertionError):
+    pass
+
+
+def _valid_choice(chosen_vals: np.ndarray, unchosen_best: float, what: str):
+    if chosen_vals.size and unchosen_best > -np.inf and chosen_vals.min() < unchosen_best - EPS:
+        raise ParityError(f"{what}: chosen value {chosen_vals.min():.6f} below unchosen "
+                          f"{unchosen_best:.6f} by more than {EPS}")
+
+
+def follow(dec, sup: dict, tree: dict, batch_index: list, requests: list, rep: Report | None = None) -> Report:
+    """Check GPU results against the oracle.
+
+    dec          oracle.prepare(...) of inputs holding the requests in ``requests``
+                 (row i of dec is request requests[i])
+    sup, tree    host copies of the GPU's exported supertree and emitted tree
+    batch_index  position of each checked request in the GPU's batch
+    """
+    rep = rep or Report()
+    p = dec.p
+    sizes = p.level_sizes()
+    W, k = p.width, min(p.branch, p.vocab)
+
+    followed = []
+    for i, b in enumerate(requests):
+        q = batch_index[i]
+
+        def choose_topk(req, d, j, z_row, lp_row, kk, q=q):
+            row = q * sizes[d - 2] + j if d > 1 else q  # parent row of this depth
+            ids = sup["cand_ids"][d - 1, row, :kk].astype(np.int64)
+            glp = sup["cand_logp"][d - 1, row, :kk].astype(np.float64)
+            if len(set(ids.tolist())) != kk or ids.min() < 0 or ids.max() >= len(z_row):
+                raise ParityError(f"depth {d} row {row}: malformed candidate ids {ids}")
+            mine = set(ids.tolist())
+            ref = R.topk_ids(z_row, min(kk + 1, len(z_row)))
+            best_un = next((lp_row[v] for v in ref if v not in mine), -np.inf)
+            _valid_choice(lp_row[ids], best_un, f"top-k depth {d} row {row}")
+            if mine != set(ref[:kk].tolist()):
+                rep.topk_events += 1
+            rep.max_logp_err = max(rep.max_logp_err, float(np.abs(glp - lp_row[ids]).max()))
+            m = z_row.max()
+            lse = m / p.tau + np.log(np.exp((z_row - m) / p.tau).sum())
+            rep.max_lse_err = max(rep.max_lse_err, abs(float(sup["lse"][d - 1, row]) - lse))
+            rep.checked_rows += 1
+            return ids
+
+        def choose(req, d, par, tok, sc, n_keep, _unused, q=q):
+            gtok = sup["tokens"][d - 1, q, :n_keep].astype(np.int64)
+            gpar = sup["parents"][d - 1, q, :n_keep].astype(np.int64)
+            index = {(int(a), int(t)): c for c, (a, t) in enumerate(zip(par, tok))}
+            try:
+                keep = np.array([index[(int(a), int(t))] for a, t in zip(gpar, gtok)], np.int64)
+            except KeyError as e:
+                raise ParityError(f"depth {d}: GPU kept a child that is not a candidate: {e}")
+            if len(set(keep.tolist())) != n_keep:
+                raise ParityError(f"depth {d}: duplicate children in the GPU level")
+            un = np.ones(len(sc), bool)
+            un[keep] = False
+            _valid_choice(sc[keep], sc[un].max() if un.any() else -np.inf, f"top-W depth {d}")
+            if set(keep.tolist()) != set(R.select_level(par, tok, sc, n_keep).tolist()):
+                rep.topw_events += 1
+            gs = sup["scores"][d - 1, q, :n_keep].astype(np.float64)
+            err = float(np.abs(gs - sc[keep]).max())
+            rep.max_score_err = max(rep.max_score_err, err)
+            if err > SCORE_TOL:
+                raise ParityError(f"depth {d}: score error {err}")
+            return keep
+
+        st = R.build_supertree(dec, requests=[i], choose=choose, choose_topk=choose_topk)
+        followed.append(st.levels[0])
+
+        # top-B: the GPU's kept set, read back from its emitted tree
+        levels = st.levels[0]
+        n = int(tree["num_nodes"][q])
+        slot_of = {}
+        for d, lvl in enumerate(levels, start=1):
+            for sl in range(len(lvl.token)):
+                slot_of[(d, int(lvl.parent[sl]) if d > 1 else 0, int(lvl.token[sl]))] = sl
+        out_slot = []
+        kept = []
+        for o in range(n):
+            d = int(tree["depths"][q, o])
+            po = int(tree["parents"][q, o])
+            ps = 0 if po < 0 else out_slot[po][1]
+            key = (d, ps, int(tree["tokens"][q, o]))
+            if key not in slot_of or (po >= 0 and out_slot[po][0] != d - 1) or (po < 0 and d != 1):
+                raise ParityError(f"emitted node {o} {key} is not in the supertree")
+            out_slot.append((d, slot_of[key]))
+            kept.append((d, slot_of[key]))
+        if len(set(kept)) != n or n != min(p.budget, sum(sizes)):
+            raise ParityError(f"emitted tree has {n} nodes / duplicates")
+        all_nodes = [(d, sl) for d, lvl in enumerate(levels, start=1) for sl in range(len(lvl.token))]
+        score = {(d, sl): levels[d - 1].score[sl] for d, sl in all_nodes}
+        ks = set(kept)
+        _valid_choice(np.array([score[x] for x in kept]),
+                      max((score[x] for x in all_nodes if x not in ks), default=-np.inf), "top-B")
+        if ks != set(R.prune(levels, p.budget)):
+            rep.topb_events += 1
+        tok, par, dep, sco, mask, nn = R.emit_tree(levels, kept, p.budget)
+        for name, want in (("tokens", tok), ("parents", par), ("depths", dep)):
+            if not np.array_equal(tree[name][q], want):
+                raise ParityError(f"request {b}: {name} differ\nGPU    {tree[name][q][:n]}\noracle {want[:n]}")
+        if not np.array_equal(tree["mask"][q], mask):
+            raise ParityError(f"request {b}: mask differs")
+        if nn != n:
+            raise ParityError(f"request {b}: num_nodes {n} vs {nn}")
+        fin = np.isfinite(sco)
+        if not np.array_equal(fin, np.isfinite(tree["scores"][q])):
+            raise ParityError(f"request {b}: padding of scores differs")
+        err = float(np.abs(tree["scores"][q][fin] - sco[fin]).max()) if fin.any() else 0.0
+        rep.max_score_err = max(rep.max_score_err, err)
+        if err > SCORE_TOL:
+            raise ParityError(f"request {b}: emitted score error {err}")
+    return rep

@@ -1,0 +1,134 @@
+"""The C ABI without a GPU: the library loads, exports every declared entry
+point, and rejects bad arguments on the host before touching the device."""
+import ctypes
+import math
+import re
+import os
+
+import pytest
+
+from paper_2608_13524_amd import dartree as D
+from paper_2608_13524_amd import workloads as W
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "dartree.h")
+FAKE = 0x10000  # 16-byte aligned address that is never dereferenced
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(dartree_\w+)\s*\(", text, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    syms = declared_symbols()
+    assert len(syms) == 13, syms
+    lib = D.lib()
+    for s in syms:
+        assert hasattr(lib, s), s
+    assert sorted(D.SYMBOLS) == syms
+
+
+def test_abi_version_and_status_strings():
+    assert D.abi_version() == 1
+    for s in range(5):
+        assert D.status_string(s)
+    assert D.status_string(99) == "unknown status"
+
+
+def _p(**kw):
+    cfg = W.CONFIGS["qwen3-4b"]
+    p = D.Params.of(cfg)
+    for k, v in kw.items():
+        setattr(p, k, v)
+    return p
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("batch", 0, D.ERR_INVALID_ARG), ("vocab", 0, D.ERR_INVALID_ARG), ("hidden", 0, D.ERR_INVALID_ARG),
+    ("depth", 0, D.ERR_INVALID_ARG), ("width", 0, D.ERR_INVALID_ARG), ("branch", 0, D.ERR_INVALID_ARG),
+    ("budget", 0, D.ERR_INVALID_ARG), ("precision", 7, D.ERR_INVALID_ARG),
+    ("temperature", -0.5, D.ERR_INVALID_ARG), ("temperature", math.nan, D.ERR_INVALID_ARG),
+    ("temperature", math.inf, D.ERR_INVALID_ARG), ("depth_bonus", 0.1, D.ERR_INVALID_ARG),
+    ("depth_bonus", math.nan, D.ERR_INVALID_ARG), ("branch", 151937, D.ERR_INVALID_ARG),
+    ("vocab", (1 << 20) + 1, D.ERR_UNSUPPORTED), ("depth", 65, D.ERR_UNSUPPORTED),
+    ("width", 2049, D.ERR_UNSUPPORTED), ("branch", 33, D.ERR_UNSUPPORTED),
+    ("budget", 4097, D.ERR_UNSUPPORTED), ("hidden", 2560 + 32, D.ERR_UNSUPPORTED),
+    ("width", 1024, D.ERR_UNSUPPORTED),   # 1024 parents x 8 candidates > 4096
+])
+def test_validate_rejects(field, value, code):
+    assert D.validate(_p(**{field: value})) == code
+
+
+def test_validate_accepts_all_workloads_and_edges():
+    for name in W.CONFIG_ORDER:
+        assert D.validate(D.Params.of(W.CONFIGS[name])) == D.OK, name
+    assert D.validate(_p(depth_bonus=0.0, temperature=0.0)) == D.OK
+    assert D.validate(_p(depth_bonus=-0.0)) == D.OK
+    assert D.validate(_p(width=1, branch=1, budget=1)) == D.OK
+    fp = D.Params.of(W.CONFIGS["tiny"])
+    fp.hidden = 7                      # any hidden size in fp32 mode
+    assert D.validate(fp) == D.OK
+    assert D.validate(None) == D.ERR_INVALID_ARG
+
+
+def test_workspace_size():
+    p = D.Params.of(W.CONFIGS["stress-x16"])
+    n = D.workspace_size(p)
+    R, V, h = 16 * 64, 151936, 5120
+    assert n >= R * V * 4 + 2 * R * h * 2 + R * h * 4   # logits, states, features
+    assert n % 256 == 0
+    assert D.workspace_size(D.Params.of(W.CONFIGS["qwen3-4b"])) < n
+    with pytest.raises(D.DartreeError) as e:
+        D.workspace_size(_p(batch=0))
+    assert e.value.status == D.ERR_INVALID_ARG
+
+
+def _inputs():
+    return D.InputsC(FAKE, FAKE, FAKE, FAKE, FAKE)
+
+
+def _tree():
+    return D.TreeC(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+
+
+def test_entry_points_reject_before_any_launch():
+    lib = D.lib()
+    p = _p()
+    need = D.workspace_size(p)
+    byref = ctypes.byref
+    # null / misaligned pointers
+    bad_in = D.InputsC(FAKE, FAKE, None, FAKE, FAKE)
+    assert lib.dartree_build_tree(byref(p), byref(bad_in), FAKE, need, byref(_tree()), None) == D.ERR_INVALID_ARG
+    mis = D.InputsC(FAKE + 4, FAKE, FAKE, FAKE, FAKE)
+    assert lib.dartree_build_tree(byref(p), byref(mis), FAKE, need, byref(_tree()), None) == D.ERR_INVALID_ARG
+    bad_tree = D.TreeC(FAKE, FAKE, FAKE, FAKE, None, FAKE)
+    assert lib.dartree_build_tree(byref(p), byref(_inputs()), FAKE, need, byref(bad_tree), None) == D.ERR_INVALID_ARG
+    # workspace: too small, misaligned, missing
+    assert lib.dartree_build_tree(byref(p), byref(_inputs()), FAKE, need - 1, byref(_tree()), None) == D.ERR_WORKSPACE
+    assert lib.dartree_build_tree(byref(p), byref(_inputs()), FAKE + 16, need, byref(_tree()), None) == D.ERR_WORKSPACE
+    assert lib.dartree_build_tree(byref(p), byref(_inputs()), None, need, byref(_tree()), None) == D.ERR_WORKSPACE
+    # depth index out of range
+    assert lib.dartree_expand_depth(byref(p), byref(_inputs()), 0, FAKE, need, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_expand_depth(byref(p), byref(_inputs()), 17, FAKE, need, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_prune(byref(p), FAKE, need - 256, byref(_tree()), None) == D.ERR_WORKSPACE
+    assert lib.dartree_export_supertree(byref(p), FAKE, need, None, None) == D.ERR_INVALID_ARG
+    # single-step calls
+    assert lib.dartree_project(1, 8, 100, 65, 8, FAKE, FAKE, FAKE, 100, FAKE, None) == D.ERR_UNSUPPORTED
+    assert lib.dartree_project(1, 0, 100, 64, 8, FAKE, FAKE, FAKE, 100, FAKE, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_project(1, 8, 100, 64, 8, FAKE + 2, FAKE, FAKE, 100, FAKE, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_lse_topk(FAKE, 4, 100, 101, 1.0, FAKE, FAKE, FAKE, None, 0, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_lse_topk(FAKE, 4, 100, 4, -1.0, FAKE, FAKE, FAKE, None, 0, None) == D.ERR_INVALID_ARG
+    big = D.lse_topk_workspace_size(1, 151936, 8)
+    assert big > 0
+    assert lib.dartree_lse_topk(FAKE, 1, 151936, 8, 1.0, FAKE, FAKE, FAKE, None, 0, None) == D.ERR_WORKSPACE
+    assert lib.dartree_select_topw(1, 8, 8, 65, -0.2, None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_select_topw(1, 8, 8, 8, 0.5, None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_select_topw(1, 1024, 8, 8, -0.2, None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == D.ERR_UNSUPPORTED
+    assert lib.dartree_prune_levels(byref(p), None, FAKE, FAKE, byref(_tree()), None) == D.ERR_INVALID_ARG
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(D, "_lib", None)
+    monkeypatch.setattr(D, "LIB_PATH", str(tmp_path / "absent.so"))
+    with pytest.raises(RuntimeError, match="no fallback"):
+        D.lib()

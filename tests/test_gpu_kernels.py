@@ -1,0 +1,218 @@
+"""Each kernel of one depth on injected inputs, through the C ABI, against the
+oracle's routines on the same values.
+
+Selections (top-k, top-W, top-B and the emitted tree) are integer work on the
+same fp32 values on both sides and must agree bit for bit, ties included.
+Products and normalisers are checked against fp64 with error bounds."""
+import numpy as np
+import pytest
+import torch
+
+import oracle.dartree_ref as R
+from paper_2608_13524_amd import dartree as D
+from paper_2608_13524_amd import workloads as W
+from tests.gpu_util import device, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+# ---------------------------------------------------------------------------
+# log-softmax normaliser + per-row top-k
+# ---------------------------------------------------------------------------
+
+LSE_CASES = [
+    # rows, vocab, k, T, distribution
+    (1, 151936, 8, 0.0, "normal"),      # split over many segments + merge
+    (8, 151936, 8, 1.0, "normal"),
+    (64, 151936, 8, 0.7, "normal"),
+    (1024, 4096, 8, 1.0, "normal"),     # one segment per row
+    (3, 1001, 4, 0.7, "normal"),        # vocab not a multiple of 4: scalar path
+    (5, 1024, 32, 1.0, "ties"),         # coarse values: many exact ties
+    (7, 151936, 16, 0.0, "ties"),
+    (2, 40, 1, 0.0, "ties"),
+    (4, 9, 9, 2.0, "normal"),           # k = V
+]
+
+
+@pytest.mark.parametrize("rows,vocab,k,T,dist", LSE_CASES)
+def test_lse_topk(rows, vocab, k, T, dist):
+    rng = np.random.default_rng(rows * 7919 + vocab + k)
+    z = rng.normal(0, 2, size=(rows, vocab)).astype(np.float32)
+    if dist == "ties":
+        z = (np.round(z * 4) / 4).astype(np.float32)
+    dev = device()
+    zd = to_dev(z)
+    lse = torch.empty(rows, dtype=torch.float32, device=dev)
+    lp = torch.empty(rows, k, dtype=torch.float32, device=dev)
+    ids = torch.empty(rows, k, dtype=torch.int32, device=dev)
+    need = D.lse_topk_workspace_size(rows, vocab, k)
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    say(f"lse_topk rows={rows} vocab={vocab} k={k} T={T} {dist}")
+    D.lse_topk(zd, k, T, lse, lp, ids, ws)
+    torch.cuda.synchronize()
+    lse, lp, ids = lse.cpu().numpy(), lp.cpu().numpy(), ids.cpu().numpy()
+    tau = T if T > 0 else 1.0
+    z64 = z.astype(np.float64)
+    ref_lp = R.log_softmax(z64, tau)
+    m = z64.max(axis=1)
+    ref_lse = m / tau + np.log(np.exp((z64 - m[:, None]) / tau).sum(axis=1))
+    for r in range(rows):
+        want = R.topk_ids(z64[r], k)
+        assert np.array_equal(ids[r], want), (r, ids[r], want)
+    assert np.allclose(lse, ref_lse, rtol=2e-6, atol=2e-5)
+    got = np.take_along_axis(ref_lp, ids.astype(np.int64), axis=1)
+    assert np.abs(lp - got).max() < 2e-5
+    assert (lp <= 0).all()
+
+
+# ---------------------------------------------------------------------------
+# corrected-logit products
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("rows,vocab,hidden,group", [
+    (1, 4099, 2560, 1), (8, 4099, 2560, 8), (13, 5000, 512, 5), (16, 151936, 2560, 8),
+    (33, 3001, 1024, 11), (64, 4099, 4096, 16), (100, 4099, 512, 25), (128, 4103, 1024, 64),
+    (200, 3000, 256, 50),
+])
+def test_project_bf16_within_error_bound(rows, vocab, hidden, group):
+    rng = np.random.default_rng(rows + vocab + hidden)
+    x = W.fp32_to_bf16_bits(np.tanh(rng.normal(0, 1.4, size=(rows, hidden))).astype(np.float32))
+    U = W.fp32_to_bf16_bits(rng.normal(0, 0.02, size=(vocab, hidden)).astype(np.float32))
+    groups = (rows + group - 1) // group
+    bias = rng.normal(0, 2, size=(groups, vocab + 3)).astype(np.float32)  # stride vocab + 3
+    dev = device()
+    z = torch.empty(rows, vocab, dtype=torch.float32, device=dev)
+    say(f"project bf16 rows={rows} vocab={vocab} hidden={hidden} group={group}")
+    D.project(D.BF16, to_dev(x), to_dev(U), to_dev(bias), vocab + 3, z, group)
+    torch.cuda.synchronize()
+    z = z.cpu().numpy().astype(np.float64)
+    xf = W.bf16_bits_to_fp32(x).astype(np.float64)
+    Uf = W.bf16_bits_to_fp32(U).astype(np.float64)
+    g = np.arange(rows) // group
+    ref = bias[g, :vocab].astype(np.float64) + xf @ Uf.T
+    # fp32 accumulation of `hidden` exact products, then one fp32 add of the bias
+    bound = 1.01 * hidden * 2.0 ** -24 * (np.abs(xf) @ np.abs(Uf).T) + 2.0 ** -23 * np.abs(ref)
+    err = np.abs(z - ref)
+    assert (err <= bound + 1e-7).all(), float((err - bound).max())
+
+
+def test_project_fp32():
+    rng = np.random.default_rng(5)
+    rows, vocab, hidden = 7, 1030, 64
+    x = rng.normal(0, 1, size=(rows, hidden)).astype(np.float32)
+    U = rng.normal(0, 0.05, size=(vocab, hidden)).astype(np.float32)
+    bias = rng.normal(0, 3, size=(1, vocab)).astype(np.float32)
+    z = torch.empty(rows, vocab, dtype=torch.float32, device=device())
+    say("project fp32")
+    D.project(D.FP32, to_dev(x), to_dev(U), to_dev(bias), 0, z, rows)
+    torch.cuda.synchronize()
+    ref = bias.astype(np.float64) + x.astype(np.float64) @ U.astype(np.float64).T
+    assert np.abs(z.cpu().numpy() - ref).max() < 1e-4
+
+
+# ---------------------------------------------------------------------------
+# segmented top-W
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("batch,n_parent,k,n_keep,beta,ties", [
+    (1, 1, 8, 8, -0.2, False), (1, 8, 8, 8, -0.2, False), (3, 32, 8, 32, -0.2, True),
+    (16, 64, 8, 64, 0.0, True), (2, 5, 3, 7, -1.0, True), (4, 512, 8, 100, -0.2, False),
+    (1, 128, 32, 2048, -0.2, True),
+])
+def test_select_topw_bit_exact(batch, n_parent, k, n_keep, beta, ties):
+    rng = np.random.default_rng(batch * 100 + n_parent + k)
+    sp = rng.normal(-5, 2, size=(batch, n_parent)).astype(np.float32)
+    lp = -np.abs(rng.normal(0, 3, size=(batch * n_parent, k))).astype(np.float32)
+    if ties:
+        sp = (np.round(sp * 2) / 2).astype(np.float32)
+        lp = (np.round(lp * 2) / 2).astype(np.float32)
+    ids = np.stack([rng.choice(151936, size=k, replace=False) for _ in range(batch * n_parent)]).astype(np.int32)
+    dev = device()
+    tok = torch.empty(batch, n_keep, dtype=torch.int32, device=dev)
+    par = torch.empty(batch, n_keep, dtype=torch.int32, device=dev)
+    sc = torch.empty(batch, n_keep, dtype=torch.float32, device=dev)
+    say(f"select_topw batch={batch} n_parent={n_parent} k={k} n_keep={n_keep}")
+    D.select_topw(batch, n_parent, k, n_keep, beta, to_dev(sp), to_dev(lp), to_dev(ids), tok, par, sc)
+    torch.cuda.synchronize()
+    tok, par, sc = tok.cpu().numpy(), par.cpu().numpy(), sc.cpu().numpy()
+    for q in range(batch):
+        parent = np.repeat(np.arange(n_parent), k)
+        token = ids[q * n_parent:(q + 1) * n_parent].reshape(-1).astype(np.int64)
+        # the same two fp32 additions as the kernel
+        s32 = (sp[q][parent] + lp[q * n_parent:(q + 1) * n_parent].reshape(-1)) + np.float32(beta)
+        keep = R.select_level(parent, token, s32.astype(np.float64), n_keep)
+        assert np.array_equal(tok[q], token[keep])
+        assert np.array_equal(par[q], parent[keep])
+        assert np.array_equal(sc[q], s32[keep])
+
+
+def test_select_topw_root_scores_null():
+    dev = device()
+    lp = np.array([[-0.1, -2.0, -0.5]], np.float32)
+    ids = np.array([[5, 9, 2]], np.int32)
+    tok = torch.empty(1, 3, dtype=torch.int32, device=dev)
+    par = torch.empty(1, 3, dtype=torch.int32, device=dev)
+    sc = torch.empty(1, 3, dtype=torch.float32, device=dev)
+    say("select_topw root")
+    D.select_topw(1, 1, 3, 3, -0.2, None, to_dev(lp), to_dev(ids), tok, par, sc)
+    torch.cuda.synchronize()
+    assert tok.cpu().tolist() == [[5, 2, 9]]
+    assert par.cpu().tolist() == [[0, 0, 0]]
+    assert np.array_equal(sc.cpu().numpy(), (lp[0][[0, 2, 1]] + np.float32(0)) + np.float32(-0.2))
+
+
+# ---------------------------------------------------------------------------
+# deferred top-B prune + emission
+# ---------------------------------------------------------------------------
+
+def _random_supertree(rng, batch, L, Wd, k, ties):
+    sizes, n = [], 1
+    for _ in range(L):
+        n = min(Wd, n * k)
+        sizes.append(n)
+    tok = np.full((L, batch, Wd), -7, np.int32)
+    par = np.full((L, batch, Wd), -7, np.int32)
+    sco = np.full((L, batch, Wd), np.nan, np.float32)
+    levels = []
+    for q in range(batch):
+        lv, prev = [], np.zeros(1, np.float32)
+        for d in range(L):
+            nd = sizes[d]
+            pp = rng.integers(0, len(prev), size=nd) if d > 0 else np.zeros(nd, np.int64)
+            # distinct tokens among siblings: draw without replacement per level
+            tt = rng.choice(50000, size=nd, replace=False)
+            drop = (np.round(rng.exponential(1.0, nd) * 2) / 2 if ties else rng.exponential(1.0, nd))
+            s = (prev[pp] - drop.astype(np.float32)).astype(np.float32)
+            tok[d, q, :nd], par[d, q, :nd], sco[d, q, :nd] = tt, pp, s
+            lv.append(R.Level(token=tt.astype(np.int64), parent=pp.astype(np.int64), score=s.astype(np.float64)))
+            prev = s
+        levels.append(lv)
+    return sizes, tok, par, sco, levels
+
+
+@pytest.mark.parametrize("batch,L,Wd,k,B,ties", [
+    (1, 4, 4, 4, 16, False), (1, 16, 8, 8, 64, True), (1, 16, 32, 8, 256, True),
+    (4, 16, 16, 8, 128, False), (16, 16, 64, 8, 512, True), (2, 5, 3, 2, 100, False),
+    (3, 6, 5, 3, 1, True), (1, 64, 64, 2, 4096, False), (2, 7, 9, 4, 20, True),
+])
+def test_prune_levels_bit_exact(batch, L, Wd, k, B, ties):
+    rng = np.random.default_rng(batch * 1000 + L * 10 + Wd + B)
+    sizes, tok, par, sco, levels = _random_supertree(rng, batch, L, Wd, k, ties)
+    cfg = W.Config("prune", batch=batch, vocab=50000, hidden=64, depth=L, width=Wd, branch=k, budget=B,
+                   temperature=0.0, precision=W.FP32, seed=0)
+    p = D.Params.of(cfg)
+    dev = device()
+    out = D.DeviceTree.alloc(batch, B, dev)
+    say(f"prune_levels batch={batch} L={L} W={Wd} k={k} B={B}")
+    D.prune_levels(p, to_dev(tok), to_dev(par), to_dev(sco), out)
+    torch.cuda.synchronize()
+    got = out.host()
+    for q in range(batch):
+        kept = R.prune(levels[q], B)
+        t, pa, de, s, m, n = R.emit_tree(levels[q], kept, B)
+        assert got["num_nodes"][q] == n
+        assert np.array_equal(got["tokens"][q], t)
+        assert np.array_equal(got["parents"][q], pa)
+        assert np.array_equal(got["depths"][q], de)
+        assert np.array_equal(got["mask"][q], m)
+        assert np.array_equal(got["scores"][q].astype(np.float64), s)

@@ -1,0 +1,133 @@
+"""End-to-end parity: the whole round through dartree_build_tree against the
+oracle, by the replay comparator (tests/replay.py).
+
+Small cases span several tiles and ragged tails of every kernel and run the
+oracle on every request; the five full-size workloads run the launch
+configuration the benchmark times and check sampled requests (requests are
+independent, so a sampled request is checked completely)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle.dartree_ref as R
+from paper_2608_13524_amd import dartree as D
+from paper_2608_13524_amd import workloads as W
+from tests import replay
+from tests.gpu_util import device, run_build, say
+
+pytestmark = pytest.mark.gpu
+
+
+def small(**kw):
+    base = dict(name="small", batch=3, vocab=5003, hidden=256, depth=5, width=6, branch=4, budget=20,
+                temperature=0.0, precision=W.BF16, seed=31, sigma_w=0.06, n_boost=8)
+    base.update(kw)
+    return W.Config(**base)
+
+
+SMALL = {
+    "bf16-ragged": small(),
+    "bf16-T0.7": small(temperature=0.7, seed=32),
+    "bf16-beta0": small(depth_bonus=0.0, seed=33),
+    "bf16-tiled-rows": small(batch=8, width=16, branch=8, budget=60, vocab=3001, seed=34),  # 128 parent rows
+    "bf16-wide-rows": small(batch=2, width=40, branch=8, budget=100, vocab=2053, hidden=128, seed=35),
+    "bf16-chain-W1": small(width=1, budget=8, seed=36),
+    "bf16-k1": small(branch=1, budget=8, seed=37),
+    "bf16-prune-all": small(budget=4096, seed=38),
+    "bf16-B1": small(budget=1, seed=39),
+    "fp32-small": small(precision=W.FP32, hidden=48, sigma_w=0.1, seed=40),
+    "fp32-tiny-vocab": small(precision=W.FP32, vocab=7, hidden=5, branch=3, width=5, budget=12, seed=41),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_small_parity(name):
+    cfg = SMALL[name]
+    inputs = W.make_inputs(cfg)
+    tree, sup, _ = run_build(cfg, inputs)
+    dec = R.prepare(inputs)
+    rep = replay.follow(dec, sup, tree, batch_index=list(range(cfg.batch)), requests=list(range(cfg.batch)))
+    print(name, rep)
+    if rep.events == 0:  # then the GPU equals the free-running oracle outright
+        want, _ = R.build_tree(dec)
+        assert np.array_equal(tree["tokens"], want.tokens) and np.array_equal(tree["mask"], want.mask)
+
+
+def test_zeroed_correction_matches_marginals():
+    """U = 0: every node of a depth sees the drafter marginals, scores are
+    sums of marginal log-probabilities (DDTree's surrogate) plus beta*d."""
+    cfg = small(seed=42, vocab=4001)
+    inputs = W.make_inputs(cfg)
+    inputs.U[:] = 0
+    tree, sup, _ = run_build(cfg, inputs)
+    Lb = inputs.Lb.astype(np.float64)
+    for q in range(cfg.batch):
+        for o in range(int(tree["num_nodes"][q])):
+            path, j = [], o
+            while j >= 0:
+                path.append(int(tree["tokens"][q, j]))
+                j = int(tree["parents"][q, j])
+            path.reverse()
+            s = sum(R.log_softmax(Lb[q, i][None, :], 1.0)[0, v] + cfg.depth_bonus for i, v in enumerate(path))
+            assert abs(s - tree["scores"][q, o]) < 1e-3
+
+
+def test_batch_and_repeat_determinism():
+    """Same inputs twice: identical bits.  A request alone or in a batch: identical tree."""
+    cfg = small(seed=43, batch=4)
+    inputs = W.make_inputs(cfg)
+    t1, s1, _ = run_build(cfg, inputs)
+    t2, s2, _ = run_build(cfg, inputs)
+    for k in t1:
+        assert np.array_equal(t1[k], t2[k]), k
+    for k in s1:
+        assert np.array_equal(s1[k], s2[k], equal_nan=True), k
+    one = W.make_inputs(cfg, requests=[2])
+    t3, _, _ = run_build(one.cfg, one, export=False)
+    for k in ("tokens", "parents", "depths", "scores", "mask"):
+        assert np.array_equal(t1[k][2], t3[k][0]), k
+
+
+def test_expand_then_prune_equals_build():
+    cfg = small(seed=44)
+    inputs = W.make_inputs(cfg)
+    t1, _, _ = run_build(cfg, inputs, export=False)
+    dev = device()
+    p = D.Params.of(cfg)
+    di = D.DeviceInputs.from_host(inputs, dev)
+    ws = D.alloc_workspace(p, dev)
+    out = D.DeviceTree.alloc(cfg.batch, cfg.budget, dev)
+    say("expand_depth x L + prune")
+    for d in range(1, cfg.depth + 1):
+        D.expand_depth(p, di, d, ws)
+    D.prune(p, ws, out)
+    torch.cuda.synchronize()
+    t2 = out.host()
+    for k in t1:
+        assert np.array_equal(t1[k], t2[k]), k
+
+
+# Full-size workloads: which requests the oracle re-derives.
+FULL_SAMPLE = {"tiny": [0], "qwen3-4b": [0], "qwen3-4b-wide": [0], "qwen3-8b-x4": [0, 3],
+               "stress-x16": [0, 15]}
+
+
+@pytest.mark.parametrize("name", W.CONFIG_ORDER)
+def test_full_size_parity(name):
+    cfg = W.CONFIGS[name]
+    weights = W.make_weights(cfg)
+    inputs = W.make_inputs(cfg, weights=weights)
+    tree, sup, _ = run_build(cfg, inputs)
+    # structural checks on every request
+    for q in range(cfg.batch):
+        n = int(tree["num_nodes"][q])
+        assert n == min(cfg.budget, cfg.supertree_size())
+        assert (tree["parents"][q, :n] < np.arange(n)).all()
+        assert (tree["tokens"][q, n:] == -1).all() and (tree["depths"][q, n:] == 0).all()
+    reqs = FULL_SAMPLE[name]
+    sub = W.make_inputs(cfg, requests=reqs, weights=weights)
+    del inputs
+    dec = R.prepare(sub)
+    rep = replay.follow(dec, sup, tree, batch_index=reqs, requests=reqs)
+    print(name, rep)
+    assert rep.max_score_err < replay.SCORE_TOL
