@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Draft-tree build latency of one DARTree round on one MI355X.
+
+A step is one full round of Algorithm 1 plus the deferred prune
+(dartree_build_tree) over one batch of synthetic drafter outputs already
+resident in HBM.  Default workload: the Qwen3-4B-shaped one (vocab 151936,
+hidden 2560, L=16, W=8, k=8, B=64, T=0, batch 1).
+
+    python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu-baseline]
+
+Prints one JSON line: latency per round (value, us), nodes scored per second,
+per-kernel average durations, the roofline fraction of the dominant kernel,
+and the CPU oracle timed on a bounded sample on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2608_13524_amd import dartree as D  # noqa: E402
+from paper_2608_13524_amd import workloads as W  # noqa: E402
+
+METRIC = "draft-tree build latency µs/round; nodes scored/s; % of MFMA/HBM peak"
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFS = 2500.0  # dense bf16 MFMA, TFLOP/s
+FP32_VECTOR_PEAK_TFS = 157.3
+RIDGE = MFMA_BF16_PEAK_TFS * 1e12 / (HBM_PEAK_GBS * 1e9)
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_work(cfg, kind: str, d: int):
+    """Algorithmic (bytes, flops) of one launch at depth d.
+
+    logits : per vocabulary row, U row (2h B) + the bias row read once per
+             request (4b B) + one fp32 logit written per parent row (4R B);
+             plus the R feature rows (2hR B).  flops 2 R h V.
+    lse_topk: one fp32 read of z (4 R V B).
+    head   : A (2h^2 B) + R state rows in, t (4hR) and a (2hR) out, H rows.
+    """
+    sizes = [1] + cfg.level_sizes()
+    R = cfg.batch * sizes[d - 1]
+    h, V, b = cfg.hidden, cfg.vocab, cfg.batch
+    act = 2 if cfg.precision == W.BF16 else 4
+    if kind == "logits":
+        return V * (act * h + 4 * b + 4 * R) + act * h * R, 2.0 * R * h * V
+    if kind == "lse_topk":
+        return 4 * R * V, 0.0
+    if kind == "head":
+        return act * h * h + act * h * R + 4 * h * R + act * h * R + act * h * b, 2.0 * R * h * h
+    return 0, 0.0
+
+
+def cpu_baseline(cfg, inputs, budget_s: float = 20.0) -> dict:
+    """The oracle (fp64 NumPy) on the host cores, on the first D depths of
+    request 0 with D chosen to take ~budget_s; scaled to us per full round."""
+    import threadpoolctl
+
+    import oracle.dartree_ref as R
+    sub = W.Inputs(cfg=cfg.replace(batch=1), Lb=inputs.Lb[:1], H=inputs.H[:1], r0=inputs.r0[:1],
+                   A=inputs.A, U=inputs.U)
+    dec = R.prepare(sub)
+    rows = [1] + cfg.level_sizes()[:-1]          # parent rows per depth, one request
+    info = threadpoolctl.threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+
+    def run(depth: int) -> float:
+        p = R.Params.of(cfg.replace(batch=1, depth=depth))
+        d2 = R.Decoded(p, dec.Lb[:, :depth], dec.H[:, :depth], dec.r0, dec.A, dec.U)
+        t0 = time.perf_counter()
+        R.build_tree(d2)
+        return time.perf_counter() - t0
+
+    t1 = run(1)
+    per_row = t1 / rows[0]
+    depth = 1
+    while depth < cfg.depth and per_row * sum(rows[:depth + 1]) < budget_s:
+        depth += 1
+    t = run(depth) if depth > 1 else t1
+    reps = 1
+    while depth == cfg.depth and reps * t < budget_s / 2:   # whole rounds: repeat, report the mean
+        t = (t * reps + run(depth)) / (reps + 1)
+        reps += 1
+    scale = sum(rows) / sum(rows[:depth]) * cfg.batch
+    return {"value": t * scale * 1e6, "unit": "us/round", "cores": int(threads), "kind": "oracle",
+            "sample": f"request 0, depths 1..{depth} of {cfg.depth} (mean of {reps} run(s), {t:.2f} s each), "
+                      f"scaled by parent rows to the full round of {cfg.batch} request(s)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="qwen3-4b", choices=W.CONFIG_ORDER)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: requests are independent trees and this build has no "
+              "multi-GPU path (sharding is described in DESIGN.md).", file=sys.stderr)
+        return 2
+
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
+    dev = torch.device("cuda:0")
+    cfg = W.CONFIGS[args.config]
+    log(f"workload {cfg.name}: generating inputs")
+    inputs = W.make_inputs(cfg)
+    p = D.Params.of(cfg)
+    di = D.DeviceInputs.from_host(inputs, dev)
+    ws = D.alloc_workspace(p, dev)
+    out = D.DeviceTree.alloc(cfg.batch, cfg.budget, dev)
+    stream = torch.cuda.current_stream()
+
+    log(f"warmup {args.warmup}")
+    for _ in range(args.warmup):
+        D.build_tree(p, di, ws, out)
+    torch.cuda.synchronize()
+
+    # timed region: exactly K rounds, one event pair per round
+    K = args.steps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(K):
+        D.build_tree(p, di, ws, out)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_step_ms = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(K)])
+    total_ms = ev[0].elapsed_time(ev[K])
+    us_round = total_ms * 1e3 / K
+    log(f"timed {K} rounds: {us_round:.1f} us/round (wall {wall * 1e3 / K:.1f} ms/round)")
+
+    # kernel durations: the same K rounds through the instrumented launch
+    # sequence, an event pair around every launch
+    nk = len(D.KERNEL_NAMES)
+    n_ev = 2 * (nk * cfg.depth + 1)
+    kev = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(K)]
+    for e in kev[0]:
+        e.record(stream)                     # creates the underlying hipEvent_t
+    for evs in kev[1:]:
+        for e in evs:
+            e.record(stream)
+    torch.cuda.synchronize()
+    for i in range(K):
+        D.build_tree_timed(p, di, ws, out, [e.cuda_event for e in kev[i]])
+    torch.cuda.synchronize()
+    dur = {name: [] for name in D.KERNEL_NAMES + ["prune"]}
+    work = {name: [0.0, 0.0] for name in D.KERNEL_NAMES + ["prune"]}
+    for i in range(K):
+        for d in range(1, cfg.depth + 1):
+            for c, name in enumerate(D.KERNEL_NAMES):
+                if name == "state" and d == cfg.depth:
+                    continue
+                j = (d - 1) * nk + c
+                dur[name].append(kev[i][2 * j].elapsed_time(kev[i][2 * j + 1]) * 1e3)
+                if i == 0:
+                    b_, f_ = kernel_work(cfg, name, d)
+                    work[name][0] += b_
+                    work[name][1] += f_
+        j = cfg.depth * nk
+        dur["prune"].append(kev[i][2 * j].elapsed_time(kev[i][2 * j + 1]) * 1e3)
+    kernels = {}
+    for name, v in dur.items():
+        per_round = sum(v) / K
+        kernels[name] = {"us_per_round": per_round, "launches_per_round": len(v) // K,
+                         "avg_us_per_launch": per_round / max(len(v) // K, 1)}
+        log(f"  {name:9s} {per_round:9.1f} us/round  ({len(v) // K} launches)")
+    instrumented_us = sum(k["us_per_round"] for k in kernels.values())
+
+    dom = max(kernels, key=lambda n: kernels[n]["us_per_round"])
+    bytes_round, flops_round = work[dom]
+    t_round = kernels[dom]["us_per_round"] * 1e-6
+    intensity = flops_round / bytes_round if bytes_round else 0.0
+    launches = kernels[dom]["launches_per_round"]
+    if cfg.precision == W.BF16 and dom == "logits" and intensity > RIDGE:
+        roof = {"bound": "mfma", "achieved": flops_round / t_round / 1e12, "peak": MFMA_BF16_PEAK_TFS,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": bytes_round / t_round / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = dom
+    roof["algorithmic_bytes_per_launch"] = bytes_round / launches
+    roof["algorithmic_flops_per_launch"] = flops_round / launches
+    roof["avg_launch_us"] = kernels[dom]["avg_us_per_launch"]
+    # second roofline of the per-row softmax/top-k pass (HBM)
+    lb, _ = work["lse_topk"]
+    lse_t = kernels["lse_topk"]["us_per_round"] * 1e-6
+    lse_roof = {"bound": "hbm", "achieved": lb / lse_t / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": lb / lse_t / 1e9 / HBM_PEAK_GBS,
+                "note": "z is written by the projection just before; below ~256 MB it can be served "
+                        "from the Infinity Cache rather than HBM"}
+    proj_flops = work["logits"][1] / (kernels["logits"]["us_per_round"] * 1e-6) / 1e12
+
+    sizes = [1] + cfg.level_sizes()
+    nodes = cfg.batch * sum(sizes[d - 1] * cfg.branch for d in range(1, cfg.depth + 1))
+    vocab_entries = cfg.batch * sum(sizes[d - 1] for d in range(1, cfg.depth + 1)) * cfg.vocab
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle on host cores)")
+        cpu = cpu_baseline(cfg, inputs)
+        log(f"  oracle {cpu['value'] / 1e6:.2f} s/round on {cpu['cores']} threads ({cpu['sample']})")
+
+    line = {
+        "metric": METRIC, "value": us_round, "unit": "us/round", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": total_ms / K, "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if cfg.precision == W.BF16 else "f32", "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": cfg.batch, "vocab": cfg.vocab, "hidden": cfg.hidden,
+                   "depth": cfg.depth, "width": cfg.width, "branch": cfg.branch, "budget": cfg.budget,
+                   "temperature": cfg.temperature, "depth_bonus": cfg.depth_bonus},
+        "us_per_round_p10": float(np.percentile(per_step_ms, 10) * 1e3),
+        "us_per_round_p50": float(np.percentile(per_step_ms, 50) * 1e3),
+        "us_per_round_p90": float(np.percentile(per_step_ms, 90) * 1e3),
+        "nodes_scored_per_s": nodes / (us_round * 1e-6),
+        "vocab_entries_scored_per_s": vocab_entries / (us_round * 1e-6),
+        "projection_tflops": proj_flops,
+        "projection_mfma_frac": proj_flops / MFMA_BF16_PEAK_TFS,
+        "kernels": kernels, "instrumented_us_per_round": instrumented_us,
+        "roofline": roof, "lse_topk_roofline": lse_roof, "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -159,10 +159,36 @@ dartree_status dartree_build_tree(const dartree_params* p, const dartree_inputs*
                                   void* ws, size_t ws_bytes, const dartree_tree* out,
                                   hipStream_t stream);
 
+/* Kernels of one round, in launch order, as indexed by dartree_build_tree_timed. */
+#define DARTREE_KERNEL_HEAD 0   /* t = A r, a = bf16(tanh(t + H_d)) */
+#define DARTREE_KERNEL_LOGITS 1 /* z = L_d^base + U a */
+#define DARTREE_KERNEL_LSE 2    /* log-softmax normaliser and per-row top-k */
+#define DARTREE_KERNEL_TOPW 3   /* segmented top-W */
+#define DARTREE_KERNEL_STATE 4  /* state update (not launched at d = L) */
+#define DARTREE_KERNELS_PER_DEPTH 5
+
+/* dartree_build_tree that also records `events` (created by the caller, for
+ * instance with hipEventCreate) on `stream` around each launch: for depth d
+ * and kernel kind c, events[2 i] before and events[2 i + 1] after, with
+ * i = (d - 1) * DARTREE_KERNELS_PER_DEPTH + c; the prune is i = L *
+ * DARTREE_KERNELS_PER_DEPTH.  `events` holds 2 (5 L + 1) entries; NULL
+ * entries are not recorded.  For measuring kernel durations inside a round. */
+dartree_status dartree_build_tree_timed(const dartree_params* p, const dartree_inputs* in, void* ws,
+                                        size_t ws_bytes, const dartree_tree* out, hipEvent_t* events,
+                                        hipStream_t stream);
+
 /* Copy the supertree levels and per-parent candidates out of `ws` into the
  * caller's device buffers (layouts in dartree_supertree), for inspection. */
 dartree_status dartree_export_supertree(const dartree_params* p, const void* ws, size_t ws_bytes,
                                         const dartree_supertree* dst, hipStream_t stream);
+
+/* Copy the states r(u) of the nodes of S_d (act [b][n_d][h], row q*n_d + i
+ * for slot i of request q) out of `ws` into `dst` (device).  Valid for
+ * 1 <= d < L once dartree_expand_depth(d) has run and until
+ * dartree_expand_depth(d + 2) is enqueued (states are double-buffered; the
+ * last depth computes none). */
+dartree_status dartree_export_states(const dartree_params* p, const void* ws, size_t ws_bytes, int32_t d,
+                                     void* dst, hipStream_t stream);
 
 /* ---- single steps on caller buffers --------------------------------------
  * The kernels of one depth, exposed for callers that assemble their own loop

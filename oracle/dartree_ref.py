@@ -220,13 +220,16 @@ def _default_choose(req: int, d: int, parent, token, score, n_keep: int, level_r
 
 
 def build_supertree(dec: Decoded, requests=None, choose: Optional[Chooser] = None,
-                    choose_topk: Optional[Callable] = None, keep_logp: bool = False) -> Supertree:
+                    choose_topk: Optional[Callable] = None, keep_logp: bool = False,
+                    adopt_states: Optional[Callable] = None) -> Supertree:
     """Alg. 1's depth loop for every request (slow: full fp64 vocabulary products).
 
     ``choose`` / ``choose_topk`` let a caller replace the two selections (used
     to follow another implementation's choices); by default the oracle makes
     its own.  ``choose_topk(req, d, j, z_row, logp_row, k)`` returns the ids of
-    parent j's candidate set.
+    parent j's candidate set.  ``adopt_states(req, d, r)`` may replace the
+    states of S_d computed here (to follow another implementation's rounding
+    of the recurrent state).
     """
     p = dec.p
     choose = choose or _default_choose
@@ -259,6 +262,8 @@ def build_supertree(dec: Decoded, requests=None, choose: Optional[Chooser] = Non
                         cand_ids=cids, cand_logp=clp, logp=lp if keep_logp else None)
             levels.append(lvl)
             r = child_states(t[lvl.parent], dec.U[lvl.token], e, p.precision)
+            if adopt_states is not None and d < p.depth:
+                r = adopt_states(b, d, r)
             s = lvl.score
         out.append(levels)
     return Supertree(p, out)

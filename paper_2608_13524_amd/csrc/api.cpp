@@ -144,9 +144,19 @@ LevelShape level_shape(const dartree_params& p, const Shape& s) {
   return ls;
 }
 
+// Optional event pair around one launch (see dartree_build_tree_timed).
+struct Timer {
+  hipEvent_t* ev = nullptr;
+  hipStream_t st = nullptr;
+  void mark(int index, int which) const {
+    if (ev && ev[2 * index + which]) (void)hipEventRecord(ev[2 * index + which], st);
+  }
+};
+
 // Enqueue depth d (validated arguments).
 dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, void* ws, const Layout& l,
-                      const Shape& s, hipStream_t st) {
+                      const Shape& s, hipStream_t st, const Timer& tm = Timer()) {
+  const int tb = (d - 1) * DARTREE_KERNELS_PER_DEPTH;
   const int64_t b = p.batch, V = p.vocab, h = p.hidden, L = p.depth, W = p.width, k = p.branch;
   const int64_t np = s.n[d - 1], nc = s.n[d];
   const int64_t R = b * np;  // parent rows of this depth
@@ -180,7 +190,9 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   head.bias_stride = L * h;
   head.out = t;
   head.act_out = a;
+  tm.mark(tb + DARTREE_KERNEL_HEAD, 0);
   hipError_t err = launch_project(head, st);
+  tm.mark(tb + DARTREE_KERNEL_HEAD, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
 
   // K2: z = L_d^base + U a
@@ -196,22 +208,30 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   lg.bias_f32 = in.drafter_logits + size_t(d - 1) * V;
   lg.bias_stride = L * V;
   lg.out = z;
+  tm.mark(tb + DARTREE_KERNEL_LOGITS, 0);
   err = launch_project(lg, st);
+  tm.mark(tb + DARTREE_KERNEL_LOGITS, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
 
   // K3: lse and top-k per parent row
+  tm.mark(tb + DARTREE_KERNEL_LSE, 0);
   err = launch_lse_topk(z, R, V, int(k), tau, lse, clp, cid, at<char>(ws, l.k3), st);
+  tm.mark(tb + DARTREE_KERNEL_LSE, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
 
   // K4: S_d = segmented top-W; level arrays have stride W per request
+  tm.mark(tb + DARTREE_KERNEL_TOPW, 0);
   err = launch_select_topw(int(b), int(np), int(k), int(nc), p.depth_bonus, int(W), int(W), parent_score, clp, cid,
                            tok, par, score, st);
+  tm.mark(tb + DARTREE_KERNEL_TOPW, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
 
   // K5: states of the kept children (unused after the last depth)
   if (d < p.depth) {
+    tm.mark(tb + DARTREE_KERNEL_STATE, 0);
     err = launch_state_update(p.precision, int(b), int(nc), int(np), int(h), int(W), tok, par, t, in.head_U, e, r_out,
                              st);
+    tm.mark(tb + DARTREE_KERNEL_STATE, 1);
     if (err != hipSuccess) return DARTREE_ERR_HIP;
   }
   return DARTREE_OK;
@@ -267,8 +287,8 @@ dartree_status dartree_prune(const dartree_params* p, const void* ws, size_t ws_
                                       at<int32_t>(ws, l.lvl_par), at<float>(ws, l.lvl_score), *out, stream));
 }
 
-dartree_status dartree_build_tree(const dartree_params* p, const dartree_inputs* in, void* ws, size_t ws_bytes,
-                                  const dartree_tree* out, hipStream_t stream) {
+dartree_status dartree_build_tree_timed(const dartree_params* p, const dartree_inputs* in, void* ws, size_t ws_bytes,
+                                        const dartree_tree* out, hipEvent_t* events, hipStream_t stream) {
   dartree_status v = validate(p);
   if (v != DARTREE_OK) return v;
   if ((v = check_inputs(in)) != DARTREE_OK) return v;
@@ -276,10 +296,22 @@ dartree_status dartree_build_tree(const dartree_params* p, const dartree_inputs*
   Layout l;
   if ((v = check_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
   const Shape s = shape_of(*p);
+  Timer tm;
+  tm.ev = events;
+  tm.st = stream;
   for (int d = 1; d <= p->depth; ++d)
-    if ((v = expand(*p, *in, d, ws, l, s, stream)) != DARTREE_OK) return v;
-  return hip_status(launch_prune_emit(p->batch, level_shape(*p, s), p->budget, at<int32_t>(ws, l.lvl_tok),
-                                      at<int32_t>(ws, l.lvl_par), at<float>(ws, l.lvl_score), *out, stream));
+    if ((v = expand(*p, *in, d, ws, l, s, stream, tm)) != DARTREE_OK) return v;
+  const int ti = p->depth * DARTREE_KERNELS_PER_DEPTH;
+  tm.mark(ti, 0);
+  v = hip_status(launch_prune_emit(p->batch, level_shape(*p, s), p->budget, at<int32_t>(ws, l.lvl_tok),
+                                   at<int32_t>(ws, l.lvl_par), at<float>(ws, l.lvl_score), *out, stream));
+  tm.mark(ti, 1);
+  return v;
+}
+
+dartree_status dartree_build_tree(const dartree_params* p, const dartree_inputs* in, void* ws, size_t ws_bytes,
+                                  const dartree_tree* out, hipStream_t stream) {
+  return dartree_build_tree_timed(p, in, ws, ws_bytes, out, nullptr, stream);
 }
 
 dartree_status dartree_export_supertree(const dartree_params* p, const void* ws, size_t ws_bytes,
@@ -299,6 +331,19 @@ dartree_status dartree_export_supertree(const dartree_params* p, const void* ws,
     if (it.to && hipMemcpyAsync(it.to, at<char>(ws, it.off), it.bytes, hipMemcpyDeviceToDevice, stream) != hipSuccess)
       return DARTREE_ERR_HIP;
   return DARTREE_OK;
+}
+
+dartree_status dartree_export_states(const dartree_params* p, const void* ws, size_t ws_bytes, int32_t d, void* dst,
+                                     hipStream_t stream) {
+  dartree_status v = validate(p);
+  if (v != DARTREE_OK) return v;
+  if (!dst || d < 1 || d >= p->depth) return DARTREE_ERR_INVALID_ARG;
+  Layout l;
+  if ((v = check_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
+  const Shape s = shape_of(*p);
+  const size_t bytes = size_t(p->batch) * s.n[d] * p->hidden * act_bytes(p->precision);
+  const void* src = at<char>(ws, d % 2 ? l.state1 : l.state0);
+  return hip_status(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, stream));
 }
 
 dartree_status dartree_project(int32_t precision, int32_t rows, int32_t vocab, int32_t hidden, int32_t rows_per_group,

@@ -28,7 +28,7 @@ MAX_SORT = 4096
 SYMBOLS = [
     "dartree_abi_version", "dartree_status_string", "dartree_validate",
     "dartree_workspace_size", "dartree_expand_depth", "dartree_prune",
-    "dartree_build_tree", "dartree_export_supertree", "dartree_project",
+    "dartree_build_tree", "dartree_build_tree_timed", "dartree_export_supertree", "dartree_export_states", "dartree_project",
     "dartree_lse_topk_workspace_size", "dartree_lse_topk", "dartree_select_topw",
     "dartree_prune_levels",
 ]
@@ -99,7 +99,10 @@ def lib() -> ctypes.CDLL:
     L.dartree_expand_depth.argtypes = [P, ctypes.POINTER(InputsC), i32, vp, sz, vp]
     L.dartree_prune.argtypes = [P, vp, sz, ctypes.POINTER(TreeC), vp]
     L.dartree_build_tree.argtypes = [P, ctypes.POINTER(InputsC), vp, sz, ctypes.POINTER(TreeC), vp]
+    L.dartree_build_tree_timed.argtypes = [P, ctypes.POINTER(InputsC), vp, sz, ctypes.POINTER(TreeC),
+                                           ctypes.POINTER(vp), vp]
     L.dartree_export_supertree.argtypes = [P, vp, sz, ctypes.POINTER(SupertreeC), vp]
+    L.dartree_export_states.argtypes = [P, vp, sz, i32, vp, vp]
     L.dartree_project.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, i64, vp, vp]
     L.dartree_lse_topk_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(sz)]
     L.dartree_lse_topk.argtypes = [vp, i32, i32, i32, f32, vp, vp, vp, vp, sz, vp]
@@ -262,6 +265,20 @@ def build_tree(p: Params, inputs: DeviceInputs, ws, out: DeviceTree, stream=None
                                     ctypes.byref(tc), _stream(stream)), "dartree_build_tree")
 
 
+KERNEL_NAMES = ["head", "logits", "lse_topk", "topw", "state"]   # per depth, launch order
+
+
+def build_tree_timed(p: Params, inputs: DeviceInputs, ws, out: DeviceTree, events, stream=None) -> None:
+    """build_tree recording ``events`` (2 * (5 L + 1) raw hipEvent_t handles or
+    None) around each launch; see dartree_build_tree_timed."""
+    ic, tc = inputs.c(), out.c()
+    n = 2 * (len(KERNEL_NAMES) * p.depth + 1)
+    assert len(events) == n
+    arr = (ctypes.c_void_p * n)(*events)
+    _check(lib().dartree_build_tree_timed(ctypes.byref(p), ctypes.byref(ic), _ptr(ws), ws.numel(),
+                                          ctypes.byref(tc), arr, _stream(stream)), "dartree_build_tree_timed")
+
+
 def expand_depth(p: Params, inputs: DeviceInputs, d: int, ws, stream=None) -> None:
     ic = inputs.c()
     _check(lib().dartree_expand_depth(ctypes.byref(p), ctypes.byref(ic), d, _ptr(ws), ws.numel(),
@@ -278,6 +295,12 @@ def export_supertree(p: Params, ws, dst: DeviceSupertree, stream=None) -> None:
     sc = dst.c()
     _check(lib().dartree_export_supertree(ctypes.byref(p), _ptr(ws), ws.numel(), ctypes.byref(sc),
                                           _stream(stream)), "dartree_export_supertree")
+
+
+def export_states(p: Params, ws, d: int, dst, stream=None) -> None:
+    """States of S_d into dst (act [b * n_d][h]); see the header for validity."""
+    _check(lib().dartree_export_states(ctypes.byref(p), _ptr(ws), ws.numel(), d, _ptr(dst), _stream(stream)),
+           "dartree_export_states")
 
 
 def project(precision: int, x, U, bias, bias_stride: int, z, rows_per_group: int, stream=None) -> None:

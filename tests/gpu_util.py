@@ -44,3 +44,28 @@ def to_dev(a: np.ndarray):
     if a.dtype == np.uint16:
         a = a.view(np.int16)
     return torch.from_numpy(a).to(device())
+
+
+def run_stepwise(cfg, inputs):
+    """expand_depth(1..L) with the states of every depth exported, then prune.
+    Returns (tree dict, supertree dict, {d: host states of S_d})."""
+    dev = device()
+    p = D.Params.of(cfg)
+    di = D.DeviceInputs.from_host(inputs, dev)
+    ws = D.alloc_workspace(p, dev)
+    out = D.DeviceTree.alloc(cfg.batch, cfg.budget, dev)
+    sizes = p.level_sizes()
+    act = torch.int16 if cfg.precision == D.BF16 else torch.float32
+    states = {}
+    say(f"stepwise {cfg.name} b={cfg.batch} V={cfg.vocab} h={cfg.hidden} L={cfg.depth} W={cfg.width}")
+    for d in range(1, cfg.depth + 1):
+        D.expand_depth(p, di, d, ws)
+        if d < cfg.depth:
+            buf = torch.empty(cfg.batch * sizes[d - 1], cfg.hidden, dtype=act, device=dev)
+            D.export_states(p, ws, d, buf)
+            states[d] = buf.cpu().numpy()
+    D.prune(p, ws, out)
+    st = D.DeviceSupertree.alloc(p, dev)
+    D.export_supertree(p, ws, st)
+    torch.cuda.synchronize()
+    return out.host(), st.host(), states

@@ -15,6 +15,18 @@ arrays (tokens, parents, depths, mask, node counts) must equal the oracle's
 flattening of the followed supertree bit for bit, and every score must agree
 within SCORE_TOL (2e-2 absolute).  With no near-tie events this is plain
 equality with the free-running oracle.
+
+Recurrent state.  States are rounded to bf16 after every depth (they are
+operands of bf16 products).  Two correct implementations that accumulate in
+a different order round a few state elements to neighbouring bf16 values; a
+1-ulp change in r moves every element of t = A r, which flips more roundings
+at the next depth, so free-running states drift apart until they differ by
+about one ulp per element (corrected logits then differ by ~1e-3 at
+h = 4096-5120).  The strict check therefore follows the GPU's states too
+(``gpu_states``): each depth is recomputed in fp64 from the GPU's parent
+states, and the GPU's state update is checked element by element against the
+oracle's (equal, or the neighbouring bf16 value).  Without ``gpu_states`` the
+comparator runs free (used with a wider window as a whole-round check).
 """
 from __future__ import annotations
 
@@ -26,6 +38,7 @@ import oracle.dartree_ref as R
 
 EPS = 1e-3
 SCORE_TOL = 2e-2
+STATE_ABS_TOL = 1e-5   # fp32 error of t + e U[v] before the state is rounded
 
 
 @dataclasses.dataclass
@@ -37,6 +50,8 @@ class Report:
     max_lse_err: float = 0.0
     max_score_err: float = 0.0
     checked_rows: int = 0
+    state_elems: int = 0
+    state_mismatch: int = 0
 
     @property
     def events(self) -> int:
@@ -47,19 +62,43 @@ class ParityError(AssertionError):
     pass
 
 
-def _valid_choice(chosen_vals: np.ndarray, unchosen_best: float, what: str):
-    if chosen_vals.size and unchosen_best > -np.inf and chosen_vals.min() < unchosen_best - EPS:
+def _valid_choice(chosen_vals: np.ndarray, unchosen_best: float, what: str, eps: float = EPS):
+    if chosen_vals.size and unchosen_best > -np.inf and chosen_vals.min() < unchosen_best - eps:
         raise ParityError(f"{what}: chosen value {chosen_vals.min():.6f} below unchosen "
-                          f"{unchosen_best:.6f} by more than {EPS}")
+                          f"{unchosen_best:.6f} by more than {eps}")
 
 
-def follow(dec, sup: dict, tree: dict, batch_index: list, requests: list, rep: Report | None = None) -> Report:
+def decode_states(bits_or_f32: np.ndarray, precision: int) -> np.ndarray:
+    if precision == R.BF16:
+        return (np.asarray(bits_or_f32).view(np.uint16).astype(np.uint32) << np.uint32(16)).view(
+            np.float32).astype(np.float64)
+    return np.asarray(bits_or_f32, np.float32).astype(np.float64)
+
+
+def free_running_tol(p) -> float:
+    """Window for the free-running comparison of a bf16 round.
+
+    Free-running states differ by up to one bf16 step (2^-7 relative) per
+    element; a 1-step change of the feature a moves z_v by sum_i U_vi da_i,
+    whose rms is at most sigma_U 2^-7 sqrt(h) (|a_i| <= 1, independent signs).
+    Scores add one such difference per depth (plus the same order from the
+    normaliser), so after L depths the rms is at most
+    2 sqrt(L) sigma_U 2^-7 sqrt(h); sigma_U is taken from the weights."""
+    if p.precision != R.BF16:
+        return EPS
+    return 2.0 * np.sqrt(p.depth) * 2.0 ** -7 * np.sqrt(p.hidden)
+
+
+def follow(dec, sup: dict, tree: dict, batch_index: list, requests: list, gpu_states: dict | None = None,
+           eps: float = EPS, score_tol: float = SCORE_TOL, rep: Report | None = None) -> Report:
     """Check GPU results against the oracle.
 
     dec          oracle.prepare(...) of inputs holding the requests in ``requests``
                  (row i of dec is request requests[i])
     sup, tree    host copies of the GPU's exported supertree and emitted tree
     batch_index  position of each checked request in the GPU's batch
+    gpu_states   {d: states of S_d as exported, [b * n_d][h]} for d = 1..L-1
+                 (decoded with decode_states), or None to run free
     """
     rep = rep or Report()
     p = dec.p
@@ -79,7 +118,7 @@ def follow(dec, sup: dict, tree: dict, batch_index: list, requests: list, rep: R
             mine = set(ids.tolist())
             ref = R.topk_ids(z_row, min(kk + 1, len(z_row)))
             best_un = next((lp_row[v] for v in ref if v not in mine), -np.inf)
-            _valid_choice(lp_row[ids], best_un, f"top-k depth {d} row {row}")
+            _valid_choice(lp_row[ids], best_un, f"top-k depth {d} row {row}", eps)
             if mine != set(ref[:kk].tolist()):
                 rep.topk_events += 1
             rep.max_logp_err = max(rep.max_logp_err, float(np.abs(glp - lp_row[ids]).max()))
@@ -101,17 +140,36 @@ def follow(dec, sup: dict, tree: dict, batch_index: list, requests: list, rep: R
                 raise ParityError(f"depth {d}: duplicate children in the GPU level")
             un = np.ones(len(sc), bool)
             un[keep] = False
-            _valid_choice(sc[keep], sc[un].max() if un.any() else -np.inf, f"top-W depth {d}")
+            _valid_choice(sc[keep], sc[un].max() if un.any() else -np.inf, f"top-W depth {d}", eps)
             if set(keep.tolist()) != set(R.select_level(par, tok, sc, n_keep).tolist()):
                 rep.topw_events += 1
             gs = sup["scores"][d - 1, q, :n_keep].astype(np.float64)
             err = float(np.abs(gs - sc[keep]).max())
             rep.max_score_err = max(rep.max_score_err, err)
-            if err > SCORE_TOL:
+            if err > score_tol:
                 raise ParityError(f"depth {d}: score error {err}")
             return keep
 
-        st = R.build_supertree(dec, requests=[i], choose=choose, choose_topk=choose_topk)
+        def adopt(req, d, r, q=q):
+            n = sizes[d - 1]
+            g = gpu_states[d][q * n:(q + 1) * n]
+            # one bf16 rounding step (2^-7 relative) plus the fp32 noise of the
+            # value before rounding; in fp32 mode the fp32 noise alone
+            err = np.abs(r - g)
+            if p.precision == R.BF16:
+                diff = err > 0
+                far = err > 2.0 ** -7 * np.maximum(np.abs(r), np.abs(g)) + STATE_ABS_TOL
+            else:
+                diff = err > 1e-6
+                far = err > STATE_ABS_TOL
+            if far.any():
+                raise ParityError(f"depth {d}: {int(far.sum())} state elements differ by more than one rounding step")
+            rep.state_elems += r.size
+            rep.state_mismatch += int(diff.sum())
+            return g
+
+        st = R.build_supertree(dec, requests=[i], choose=choose, choose_topk=choose_topk,
+                               adopt_states=adopt if gpu_states is not None else None)
         followed.append(st.levels[0])
 
         # top-B: the GPU's kept set, read back from its emitted tree
@@ -138,7 +196,7 @@ def follow(dec, sup: dict, tree: dict, batch_index: list, requests: list, rep: R
         score = {(d, sl): levels[d - 1].score[sl] for d, sl in all_nodes}
         ks = set(kept)
         _valid_choice(np.array([score[x] for x in kept]),
-                      max((score[x] for x in all_nodes if x not in ks), default=-np.inf), "top-B")
+                      max((score[x] for x in all_nodes if x not in ks), default=-np.inf), "top-B", eps)
         if ks != set(R.prune(levels, p.budget)):
             rep.topb_events += 1
         tok, par, dep, sco, mask, nn = R.emit_tree(levels, kept, p.budget)
@@ -154,6 +212,6 @@ def follow(dec, sup: dict, tree: dict, batch_index: list, requests: list, rep: R
             raise ParityError(f"request {b}: padding of scores differs")
         err = float(np.abs(tree["scores"][q][fin] - sco[fin]).max()) if fin.any() else 0.0
         rep.max_score_err = max(rep.max_score_err, err)
-        if err > SCORE_TOL:
+        if err > score_tol:
             raise ParityError(f"request {b}: emitted score error {err}")
     return rep

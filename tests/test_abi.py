@@ -21,7 +21,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     syms = declared_symbols()
-    assert len(syms) == 13, syms
+    assert len(syms) == 15, syms
     lib = D.lib()
     for s in syms:
         assert hasattr(lib, s), s
@@ -112,6 +112,9 @@ def test_entry_points_reject_before_any_launch():
     assert lib.dartree_expand_depth(byref(p), byref(_inputs()), 17, FAKE, need, None) == D.ERR_INVALID_ARG
     assert lib.dartree_prune(byref(p), FAKE, need - 256, byref(_tree()), None) == D.ERR_WORKSPACE
     assert lib.dartree_export_supertree(byref(p), FAKE, need, None, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_export_states(byref(p), FAKE, need, 16, FAKE, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_export_states(byref(p), FAKE, need, 0, FAKE, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_export_states(byref(p), FAKE, need - 1, 3, FAKE, None) == D.ERR_WORKSPACE
     # single-step calls
     assert lib.dartree_project(1, 8, 100, 65, 8, FAKE, FAKE, FAKE, 100, FAKE, None) == D.ERR_UNSUPPORTED
     assert lib.dartree_project(1, 0, 100, 64, 8, FAKE, FAKE, FAKE, 100, FAKE, None) == D.ERR_INVALID_ARG

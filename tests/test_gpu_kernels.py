@@ -158,7 +158,7 @@ def test_select_topw_root_scores_null():
     torch.cuda.synchronize()
     assert tok.cpu().tolist() == [[5, 2, 9]]
     assert par.cpu().tolist() == [[0, 0, 0]]
-    assert np.array_equal(sc.cpu().numpy(), (lp[0][[0, 2, 1]] + np.float32(0)) + np.float32(-0.2))
+    assert np.array_equal(sc.cpu().numpy()[0], (lp[0][[0, 2, 1]] + np.float32(0)) + np.float32(-0.2))
 
 
 # ---------------------------------------------------------------------------
