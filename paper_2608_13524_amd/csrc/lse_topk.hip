@@ -51,6 +51,22 @@ __device__ __forceinline__ void insert(float v, int id, float (&tv)[K], int (&ti
   }
 }
 
+// Insertion along one thread's traversal, where ids only grow: a value equal
+// to an entry already kept has a larger id and ranks after it, so comparing
+// values alone gives the (value desc, id asc) order.
+template <int K>
+__device__ __forceinline__ void insert_ascending(float v, int id, float (&tv)[K], int (&ti)[K]) {
+  tv[K - 1] = v;
+  ti[K - 1] = id;
+#pragma unroll
+  for (int j = K - 1; j > 0; --j) {
+    if (tv[j] > tv[j - 1]) {
+      const float fv = tv[j]; tv[j] = tv[j - 1]; tv[j - 1] = fv;
+      const int fi = ti[j]; ti[j] = ti[j - 1]; ti[j - 1] = fi;
+    }
+  }
+}
+
 __device__ __forceinline__ Partial wave_combine(Partial p, float scale) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -188,14 +204,21 @@ __global__ __launch_bounds__(kBlock) void lse_topk_partial(const float* __restri
         for (int i = 0; i < 4; ++i) acc += exp2f((x[c][i] - p.m) * scale);
       p.s += acc;
       if (mx > tv[K - 1]) {
+        // only this lane's values above its current K-th are visited, in id order
+        const float thr = tv[K - 1];
+        uint32_t mask = 0;
 #pragma unroll
         for (int c = 0; c < kChunk; ++c)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) stage[tid][4 * c + i] = x[c][i];
-#pragma unroll 1
-        for (int j = 0; j < 4 * kChunk; ++j) {
+          for (int i = 0; i < 4; ++i) {
+            stage[tid][4 * c + i] = x[c][i];
+            mask |= uint32_t(x[c][i] > thr) << (4 * c + i);
+          }
+        while (mask) {
+          const int j = __builtin_ctz(mask);
+          mask &= mask - 1;
           const float xv = stage[tid][j];
-          if (xv > tv[K - 1]) insert<K>(xv, base + 4 * kBlock * (j >> 2) + (j & 3), tv, ti);
+          if (xv > tv[K - 1]) insert_ascending<K>(xv, base + 4 * kBlock * (j >> 2) + (j & 3), tv, ti);
         }
       }
     }
@@ -208,7 +231,7 @@ __global__ __launch_bounds__(kBlock) void lse_topk_partial(const float* __restri
         p.m = x;
       }
       p.s += exp2f((x - p.m) * scale);
-      if (x > tv[K - 1]) insert<K>(x, v, tv, ti);
+      if (x > tv[K - 1]) insert_ascending<K>(x, v, tv, ti);
     }
   }
 

@@ -6,10 +6,10 @@
 // [N][K] row-major (K contiguous), so one family of kernels serves both.
 //
 // bf16 path, gfx950 MFMA v_mfma_f32_16x16x32_bf16 (fp32 accumulation):
-//  * proj_bf16_skinny: few rows (M <= 64).  The product is a stream over the
-//    weight matrix (U is 0.78-1.56 GB per depth), so every weight element is
-//    loaded once, straight from HBM into MFMA operand registers; the 4 waves
-//    of a block split K and are summed through LDS.
+//  * proj_bf16_stream: few rows (M <= 64).  The product is a stream over the
+//    weight matrix (U is 0.78-1.56 GB per depth, far beyond the caches), so
+//    every weight element is read once from HBM with coalesced non-temporal
+//    loads and staged through LDS into MFMA operand layout.
 //  * proj_bf16_tiled: many rows.  128x128 output tiles, 64-deep K steps staged
 //    through double-buffered, padded LDS tiles shared by 4 waves (64x64 each).
 // fp32 path: plain FMA loop (small problems only).
@@ -58,17 +58,64 @@ __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
 }
 
 // ---------------------------------------------------------------------------
-// Few rows: weight streaming.  MFMA operand A = 16 weight rows (output n),
-// operand B = 16 node rows (output m); lane l supplies row (l & 15) and the
-// 8 consecutive k at (l >> 4) * 8 of each 32-deep step.  The result lane l
-// holds D[n = 4 (l >> 4) + i][m = l & 15], i = 0..3.
+// Few rows: weight streaming through LDS-staged tiles.
+//
+// MFMA operand A = 16 weight rows (output n), operand B = 16 node rows
+// (output m); lane l supplies row (l & 15) and the 8 consecutive k at
+// (l >> 4) * 8 of each 32-deep step, so a direct operand load would touch 16
+// rows x 64 B per instruction (half cache lines).  Instead each wave moves a
+// 16*NT-row x 64-k chunk (128 B per row) with fully coalesced non-temporal
+// loads (lane l: row l / 8, 16-byte piece l % 8) into its private LDS slot,
+// XOR-swizzled by row so that both these writes and the operand reads are
+// bank-conflict free, and reads the operands back from LDS.  Chunks are
+// prefetched D ahead in registers.  The result lane l holds
+// D[n = 4 (l >> 4) + i][m = l & 15], i = 0..3.
+//
+// A block owns 16*NT weight rows; its KW waves split K into contiguous ranges
+// of 64-k chunks and are summed through LDS in wave order.  The node rows
+// (the B operand, at most 64 x h) are small and stay in the caches.
 // ---------------------------------------------------------------------------
-constexpr int kSkinnyWaves = 4;
+__device__ __forceinline__ u32x4 ld_stream(const uint16_t* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+__device__ __forceinline__ u32x4 ld_cached(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ int lds_swizzle(int row) { return (row ^ (row >> 3)) & 7; }
 
-template <int MT, int NT, int EPI>
-__global__ __launch_bounds__(256) void proj_bf16_skinny(KArgs a) {
+template <int EPI>
+__device__ __forceinline__ void emit4(const KArgs& a, int m, int n, f32x4 v, bool vec) {
+  const int64_t g = m / a.rows_per_group;
+  const int64_t o = int64_t(m) * a.N + n;
+  if (vec && n + 3 < a.N) {
+    if constexpr (EPI == EPI_LOGITS) {
+      const f32x4 b = *reinterpret_cast<const f32x4*>(a.bias_f32 + g * a.bias_stride + n);
+      *reinterpret_cast<f32x4*>(a.out + o) = v + b;
+    } else {
+      typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+      const u16x4 hb = *reinterpret_cast<const u16x4*>(static_cast<const uint16_t*>(a.bias_act) + g * a.bias_stride + n);
+      *reinterpret_cast<f32x4*>(a.out + o) = v;
+      u16x4 r;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r[i] = f32_to_bf16(tanhf(v[i] + bf16_to_f32(hb[i])));
+      *reinterpret_cast<u16x4*>(static_cast<uint16_t*>(a.act_out) + o) = r;
+    }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (n + i < a.N) emit<EPI, true>(a, m, n + i, v[i]);
+}
+
+template <int MT, int NT, int KW, int D, int EPI>
+__global__ __launch_bounds__(64 * KW) void proj_bf16_stream(KArgs a, int vec) {
+  // staging slots during the stream, then the cross-wave partial sums
+  constexpr int kSlotBytes = KW * 16 * NT * 64 * 2;
+  constexpr int kRedBytes = KW * NT * MT * 64 * 16;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[kSlotBytes > kRedBytes ? kSlotBytes : kRedBytes];
+  auto slot = reinterpret_cast<uint16_t(*)[16 * NT * 64]>(smem);
+  auto red = reinterpret_cast<f32x4(*)[NT * MT][64]>(smem);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
+  const int lr = lane >> 3, lc = lane & 7;
   const int n0 = blockIdx.x * (16 * NT);
   const int M = a.M, N = a.N, K = a.K;
   const uint16_t* X = static_cast<const uint16_t*>(a.x);
@@ -76,17 +123,31 @@ __global__ __launch_bounds__(256) void proj_bf16_skinny(KArgs a) {
 
   // Rows past M or N are clamped to the last row: their sums are computed and
   // never stored.
+  const uint16_t* wg[2 * NT];
+  int woff[2 * NT];
+#pragma unroll
+  for (int i = 0; i < 2 * NT; ++i) {
+    const int row = 8 * i + lr;
+    wg[i] = Wt + int64_t(min(n0 + row, N - 1)) * K + lc * 8;
+    woff[i] = row * 64 + (lc ^ lds_swizzle(row)) * 8;
+  }
+  int roff[2][NT];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int row = nt * 16 + r16;
+      roff[j][nt] = row * 64 + ((4 * j + kg) ^ lds_swizzle(row)) * 8;
+    }
   const uint16_t* xp[MT];
-  const uint16_t* wp[NT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) xp[mt] = X + int64_t(min(mt * 16 + r16, M - 1)) * K + kg * 8;
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) wp[nt] = Wt + int64_t(min(n0 + nt * 16 + r16, N - 1)) * K + kg * 8;
 
-  const int steps = K >> 5;
-  const int per = (steps + kSkinnyWaves - 1) / kSkinnyWaves;
-  const int s0 = wave * per;
-  const int s1 = min(steps, s0 + per);
+  const int chunks = K >> 6;
+  const int per = (chunks + KW - 1) / KW;
+  const int c0 = min(chunks, wave * per);
+  const int n = min(chunks, c0 + per) - c0;
+  uint16_t* sl = slot[wave];
 
   f32x4 acc[NT][MT];
 #pragma unroll
@@ -94,40 +155,56 @@ __global__ __launch_bounds__(256) void proj_bf16_skinny(KArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-#pragma unroll 4
-  for (int s = s0; s < s1; ++s) {
-    const int k = s << 5;
-    bf16x8 xv[MT], wv[NT];
+  u32x4 R[D][2 * NT], XR[D][2][MT];
+  auto fetch = [&](int d, int k) {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) wv[nt] = load_bf16x8(wp[nt] + k);
+    for (int i = 0; i < 2 * NT; ++i) R[d][i] = ld_stream(wg[i] + k);
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) xv[mt] = load_bf16x8(xp[mt] + k);
+    for (int mt = 0; mt < MT; ++mt) {
+      XR[d][0][mt] = ld_cached(xp[mt] + k);
+      XR[d][1][mt] = ld_cached(xp[mt] + k + 32);
+    }
+  };
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+  for (int d = 0; d < D; ++d)
+    if (d < n) fetch(d, (c0 + d) * 64);
+  for (int c = 0; c < n; c += D) {
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = mfma16(wv[nt], xv[mt], acc[nt][mt]);
+    for (int d = 0; d < D; ++d) {
+      if (c + d < n) {
+#pragma unroll
+        for (int i = 0; i < 2 * NT; ++i) *reinterpret_cast<u32x4*>(sl + woff[i]) = R[d][i];
+        u32x4 xv[2][MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) { xv[0][mt] = XR[d][0][mt]; xv[1][mt] = XR[d][1][mt]; }
+        if (c + d + D < n) fetch(d, (c0 + c + d + D) * 64);
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            const bf16x8 av = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(sl + roff[j][nt]));
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+              acc[nt][mt] = mfma16(av, __builtin_bit_cast(bf16x8, xv[j][mt]), acc[nt][mt]);
+          }
+      }
+    }
   }
 
-  __shared__ f32x4 red[kSkinnyWaves][NT * MT][64];
+  __syncthreads();  // every wave is done with its slot before the sums reuse the memory
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) red[wave][nt * MT + mt][lane] = acc[nt][mt];
   __syncthreads();
 
-  for (int p = wave; p < NT * MT; p += kSkinnyWaves) {
+  for (int p = wave; p < NT * MT; p += KW) {
     const int nt = p / MT, mt = p % MT;
     f32x4 v = red[0][p][lane];
 #pragma unroll
-    for (int w = 1; w < kSkinnyWaves; ++w) v += red[w][p][lane];
+    for (int w = 1; w < KW; ++w) v += red[w][p][lane];
     const int m = mt * 16 + r16;
-    if (m < M) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int n = n0 + nt * 16 + kg * 4 + i;
-        if (n < N) emit<EPI, true>(a, m, n, v[i]);
-      }
-    }
+    if (m < M) emit4<EPI>(a, m, n0 + nt * 16 + kg * 4, v, vec != 0);
   }
 }
 
@@ -237,20 +314,36 @@ __global__ __launch_bounds__(256) void proj_f32(KArgs a, int nblk_n) {
   emit<EPI, false>(a, m, n, acc);
 }
 
-template <int MT, int NT>
-hipError_t launch_skinny(const KArgs& k, int epi, hipStream_t s) {
+// vec: every group of 4 outputs and its bias are 16-byte aligned
+bool epilogue_vec_ok(const KArgs& k, int epi) {
+  if (k.N % 4 != 0 || k.bias_stride % 4 != 0) return false;
+  const uintptr_t bias = epi == EPI_LOGITS ? reinterpret_cast<uintptr_t>(k.bias_f32)
+                                           : reinterpret_cast<uintptr_t>(k.bias_act);
+  const size_t bias_align = epi == EPI_LOGITS ? 16 : 8;
+  return bias % bias_align == 0 && reinterpret_cast<uintptr_t>(k.out) % 16 == 0 &&
+         (epi == EPI_LOGITS || reinterpret_cast<uintptr_t>(k.act_out) % 8 == 0);
+}
+
+template <int MT, int NT, int KW, int D>
+hipError_t launch_stream(const KArgs& k, int epi, hipStream_t s) {
   const dim3 grid((k.N + 16 * NT - 1) / (16 * NT));
-  if (epi == EPI_LOGITS) hipLaunchKernelGGL((proj_bf16_skinny<MT, NT, EPI_LOGITS>), grid, dim3(256), 0, s, k);
-  else hipLaunchKernelGGL((proj_bf16_skinny<MT, NT, EPI_HEAD>), grid, dim3(256), 0, s, k);
+  const int vec = epilogue_vec_ok(k, epi);
+  if (epi == EPI_LOGITS)
+    hipLaunchKernelGGL((proj_bf16_stream<MT, NT, KW, D, EPI_LOGITS>), grid, dim3(64 * KW), 0, s, k, vec);
+  else
+    hipLaunchKernelGGL((proj_bf16_stream<MT, NT, KW, D, EPI_HEAD>), grid, dim3(64 * KW), 0, s, k, vec);
   return hipGetLastError();
 }
 
 template <int MT>
-hipError_t launch_skinny_nt(const KArgs& k, int epi, hipStream_t s) {
-  // Widest weight strip per block that still gives >= 1024 blocks.
-  if ((k.N + 63) / 64 >= 1024) return launch_skinny<MT, 4>(k, epi, s);
-  if ((k.N + 31) / 32 >= 1024) return launch_skinny<MT, 2>(k, epi, s);
-  return launch_skinny<MT, 1>(k, epi, s);
+hipError_t launch_stream_nt(const KArgs& k, int epi, hipStream_t s) {
+  // Long weight matrices (the vocabulary): 32-row blocks, 8 waves over K.
+  // Short ones (A, h rows): 16-row blocks, 16 waves over K (8 when the node
+  // rows need more registers), so that even h = 2560 rows give enough waves
+  // to keep HBM busy.
+  if (k.N >= 32 * 2048) return launch_stream<MT, 2, 8, 2>(k, epi, s);
+  if constexpr (MT <= 2) return launch_stream<MT, 1, 16, 2>(k, epi, s);
+  return launch_stream<MT, 1, 8, 2>(k, epi, s);
 }
 
 }  // namespace
@@ -277,10 +370,10 @@ hipError_t launch_project(const ProjArgs& p, hipStream_t s) {
     else hipLaunchKernelGGL((proj_f32<EPI_HEAD>), grid, dim3(256), 0, s, k, nblk_n);
     return hipGetLastError();
   }
-  if (k.M <= 16) return launch_skinny_nt<1>(k, p.epilogue, s);
-  if (k.M <= 32) return launch_skinny_nt<2>(k, p.epilogue, s);
-  if (k.M <= 48) return launch_skinny_nt<3>(k, p.epilogue, s);
-  if (k.M <= 64) return launch_skinny_nt<4>(k, p.epilogue, s);
+  if (k.M <= 16) return launch_stream_nt<1>(k, p.epilogue, s);
+  if (k.M <= 32) return launch_stream_nt<2>(k, p.epilogue, s);
+  if (k.M <= 48) return launch_stream_nt<3>(k, p.epilogue, s);
+  if (k.M <= 64) return launch_stream_nt<4>(k, p.epilogue, s);
   const dim3 grid((k.M + TBM - 1) / TBM, (k.N + TBN - 1) / TBN);
   if (p.epilogue == EPI_LOGITS) hipLaunchKernelGGL((proj_bf16_tiled<EPI_LOGITS>), grid, dim3(256), 0, s, k);
   else hipLaunchKernelGGL((proj_bf16_tiled<EPI_HEAD>), grid, dim3(256), 0, s, k);
