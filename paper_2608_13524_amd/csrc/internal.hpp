@@ -58,7 +58,8 @@ struct ProjArgs {
 };
 hipError_t launch_project(const ProjArgs& a, hipStream_t s);
 
-// Row-wise online log-sum-exp and top-k (K3).
+// Row-wise online log-sum-exp and top-k (K3); scratch holds the per-segment
+// records when rows are split (lse_topk_scratch_bytes > 0).
 size_t lse_topk_scratch_bytes(int64_t rows, int64_t vocab, int k);
 hipError_t launch_lse_topk(const float* z, int64_t rows, int64_t vocab, int k, float tau,
                            float* lse, float* cand_logp, int32_t* cand_ids, void* scratch,

@@ -156,13 +156,35 @@ __device__ __forceinline__ void finalize(int64_t row, Partial p, const float (&v
 
 constexpr int kChunk = 4;  // float4 loads in flight per thread
 
-// grid: rows * nseg blocks, block = row * nseg + segment.  Writes the final
-// result when nseg == 1, otherwise the segment's partial.
+// Partial record of one row segment: m, s, two pad words, K values, K ids.
+template <int K>
+constexpr int record_floats() { return (4 + 2 * K + 3) & ~3; }
+
+// Fold the nseg records of one row into each thread's (Partial, top-K):
+// threads take single candidates, which keeps this tail small in registers.
+template <int K>
+__device__ void fold_records(const float* recs, int nseg, int k, float scale, Partial& p, float (&tv)[K],
+                             int (&ti)[K]) {
+  constexpr int RF = record_floats<K>();
+  p = Partial{-INFINITY, 0.f};
+  for (int sg = threadIdx.x; sg < nseg; sg += blockDim.x) p = combine(p, Partial{recs[sg * RF], recs[sg * RF + 1]}, scale);
+#pragma unroll
+  for (int r = 0; r < K; ++r) { tv[r] = -INFINITY; ti[r] = INT32_MAX; }
+#pragma unroll 1
+  for (int c = threadIdx.x; c < nseg * k; c += blockDim.x) {
+    const int sg = c / k, r = c - sg * k;
+    insert<K>(recs[sg * RF + 4 + r], __float_as_int(recs[sg * RF + 4 + K + r]), tv, ti);
+  }
+}
+
+// grid: rows * nseg blocks, block = row * nseg + segment.  One segment per
+// row writes the result directly; otherwise every block writes its segment's
+// record for lse_topk_merge.
 template <int K, bool VEC>
-__global__ __launch_bounds__(kBlock) void lse_topk_partial(const float* __restrict__ z, int vocab,
-                                                           int nseg, int seg_len, int k, float tau,
-                                                           float* lse, float* cand_logp,
-                                                           int32_t* cand_ids, float* part) {
+__global__ __launch_bounds__(kBlock) void lse_topk_rows(const float* __restrict__ z, int vocab,
+                                                        int nseg, int seg_len, int k, float tau,
+                                                        float* lse, float* cand_logp,
+                                                        int32_t* cand_ids, float* part) {
   // per-thread staging row for the (rare) chunks that reach the top-K list
   __shared__ float stage[kBlock][4 * kChunk + 1];
   const int64_t row = blockIdx.x / nseg;
@@ -243,44 +265,32 @@ __global__ __launch_bounds__(kBlock) void lse_topk_partial(const float* __restri
     finalize<K>(row, p, rv, ri, k, tau, lse, cand_logp, cand_ids);
     return;
   }
-  // partial record: m, s, then k values, then k ids (as int bits)
-  float* rec = part + (row * nseg + seg) * int64_t(2 + 2 * k);
+  constexpr int RF = record_floats<K>();
+  float* rec = part + (row * nseg + seg) * RF;
   rec[0] = p.m;
   rec[1] = p.s;
 #pragma unroll
   for (int r = 0; r < K; ++r) {
-    if (r < k) {
-      rec[2 + r] = rv[r];
-      rec[2 + k + r] = __int_as_float(ri[r]);
-    }
+    rec[4 + r] = rv[r];
+    rec[4 + K + r] = __int_as_float(ri[r]);
   }
 }
 
-// One wave per row: merge the row's segment partials in segment order.
+// grid: rows.  Merge the row's segment records, every thread folding single
+// candidates (no thread waits on a chain of dependent loads).
 template <int K>
-__global__ __launch_bounds__(64) void lse_topk_merge(int nseg, int k, float tau, const float* part,
-                                                     float* lse, float* cand_logp, int32_t* cand_ids) {
+__global__ __launch_bounds__(kBlock) void lse_topk_merge(int nseg, int k, float tau, const float* part, float* lse,
+                                                         float* cand_logp, int32_t* cand_ids) {
   const int64_t row = blockIdx.x;
-  const int lane = threadIdx.x;
   const float scale = kLog2e / tau;
-  Partial p{-INFINITY, 0.f};
+  Partial p;
   float tv[K];
   int ti[K];
-#pragma unroll
-  for (int r = 0; r < K; ++r) { tv[r] = -INFINITY; ti[r] = INT32_MAX; }
-  for (int sgi = lane; sgi < nseg; sgi += 64) {
-    const float* rec = part + (row * nseg + sgi) * int64_t(2 + 2 * k);
-    p = combine(p, Partial{rec[0], rec[1]}, scale);
-#pragma unroll 1
-    for (int r = 0; r < k; ++r) insert<K>(rec[2 + r], __float_as_int(rec[2 + k + r]), tv, ti);
-  }
-  p = wave_combine(p, scale);
+  fold_records<K>(part + row * nseg * record_floats<K>(), nseg, k, scale, p, tv, ti);
   float rv[K];
   int ri[K];
-#pragma unroll
-  for (int r = 0; r < K; ++r) { rv[r] = -INFINITY; ri[r] = INT32_MAX; }
-  wave_topk<K>(tv, ti, k, rv, ri);
-  if (lane == 0) finalize<K>(row, p, rv, ri, k, tau, lse, cand_logp, cand_ids);
+  block_merge<K>(p, tv, ti, k, scale, rv, ri);
+  if (threadIdx.x == 0) finalize<K>(row, p, rv, ri, k, tau, lse, cand_logp, cand_ids);
 }
 
 // Segments per row: enough blocks to fill 256 CUs a few times over, but no
@@ -300,14 +310,14 @@ hipError_t launch_k(const float* z, int64_t rows, int64_t vocab, int k, float ta
   if (vec) seg_len = (seg_len + 3) & ~3;
   const dim3 grid(unsigned(rows * nseg));
   if (vec)
-    hipLaunchKernelGGL((lse_topk_partial<K, true>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
-                       tau, lse, cand_logp, cand_ids, part);
+    hipLaunchKernelGGL((lse_topk_rows<K, true>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k, tau,
+                       lse, cand_logp, cand_ids, part);
   else
-    hipLaunchKernelGGL((lse_topk_partial<K, false>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
-                       tau, lse, cand_logp, cand_ids, part);
+    hipLaunchKernelGGL((lse_topk_rows<K, false>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k, tau,
+                       lse, cand_logp, cand_ids, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || nseg == 1) return e;
-  hipLaunchKernelGGL((lse_topk_merge<K>), dim3(unsigned(rows)), dim3(64), 0, s, nseg, k, tau, part, lse,
+  hipLaunchKernelGGL((lse_topk_merge<K>), dim3(unsigned(rows)), dim3(kBlock), 0, s, nseg, k, tau, part, lse,
                      cand_logp, cand_ids);
   return hipGetLastError();
 }
@@ -317,7 +327,9 @@ hipError_t launch_k(const float* z, int64_t rows, int64_t vocab, int k, float ta
 size_t lse_topk_scratch_bytes(int64_t rows, int64_t vocab, int k) {
   const int nseg = num_segments(rows, vocab);
   if (nseg == 1) return 0;
-  return size_t(rows) * nseg * (2 + 2 * size_t(k)) * sizeof(float);
+  const int K = k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : k <= 8 ? 8 : k <= 16 ? 16 : 32;
+  const size_t rf = size_t((4 + 2 * K + 3) & ~3);
+  return size_t(rows) * nseg * rf * sizeof(float);
 }
 
 hipError_t launch_lse_topk(const float* z, int64_t rows, int64_t vocab, int k, float tau, float* lse,

@@ -216,3 +216,22 @@ def test_prune_levels_bit_exact(batch, L, Wd, k, B, ties):
         assert np.array_equal(got["depths"][q], de)
         assert np.array_equal(got["mask"][q], m)
         assert np.array_equal(got["scores"][q].astype(np.float64), s)
+
+
+def test_lse_topk_workspace_reuse():
+    """Consecutive calls on one workspace (row tickets must come back to zero),
+    with a different number of rows each time."""
+    dev = device()
+    vocab, k = 151936, 8
+    need = max(D.lse_topk_workspace_size(r, vocab, k) for r in (8, 3, 8))
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    for rep, rows in enumerate((8, 3, 8)):
+        z = np.random.default_rng(100 + rep).normal(0, 2, size=(rows, vocab)).astype(np.float32)
+        lse = torch.empty(rows, dtype=torch.float32, device=dev)
+        lp = torch.empty(rows, k, dtype=torch.float32, device=dev)
+        ids = torch.empty(rows, k, dtype=torch.int32, device=dev)
+        say(f"lse_topk reuse rows={rows}")
+        D.lse_topk(to_dev(z), k, 0.0, lse, lp, ids, ws)
+        torch.cuda.synchronize()
+        for r in range(rows):
+            assert np.array_equal(ids.cpu().numpy()[r], R.topk_ids(z[r].astype(np.float64), k))
