@@ -73,6 +73,8 @@ def test_lse_topk(rows, vocab, k, T, dist):
     (1, 4099, 2560, 1), (8, 4099, 2560, 8), (13, 5000, 512, 5), (16, 151936, 2560, 8),
     (33, 3001, 1024, 11), (64, 4099, 4096, 16), (100, 4099, 512, 25), (128, 4103, 1024, 64),
     (200, 3000, 256, 50),
+    # >= 512 rows against >= 16384 columns: the 256x256-tile kernel, ragged in both
+    (512, 16400, 256, 64), (600, 16390, 128, 75), (1024, 20000, 512, 64),
 ])
 def test_project_bf16_within_error_bound(rows, vocab, hidden, group):
     rng = np.random.default_rng(rows + vocab + hidden)
