@@ -34,7 +34,7 @@ __device__ __forceinline__ Partial combine(Partial a, Partial b, float scale) {
   // scale = log2(e) / tau.  exp2(-inf) = 0 handles an empty side.
   const float m = fmaxf(a.m, b.m);
   if (m == -INFINITY) return Partial{m, 0.f};
-  return Partial{m, a.s * exp2f((a.m - m) * scale) + b.s * exp2f((b.m - m) * scale)};
+  return Partial{m, a.s * __builtin_amdgcn_exp2f((a.m - m) * scale) + b.s * __builtin_amdgcn_exp2f((b.m - m) * scale)};
 }
 
 template <int K>
@@ -67,91 +67,149 @@ __device__ __forceinline__ void insert_ascending(float v, int id, float (&tv)[K]
   }
 }
 
-__device__ __forceinline__ Partial wave_combine(Partial p, float scale) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    Partial o{__shfl_xor(p.m, off), __shfl_xor(p.s, off)};
-    p = combine(p, o, scale);
-  }
-  return p;
+// Ranking key of a candidate: a larger key ranks first, i.e. (value desc, id
+// asc).  High word: the value's bits in unsigned order (-0 taken as +0, so
+// equal values tie); low word: ~id.  The empty entry (-inf, INT32_MAX) has the
+// smallest key any entry can have.
+__device__ __forceinline__ uint64_t rank_key(float v, int id) {
+  uint32_t b = __float_as_uint(v + 0.0f);
+  b = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+  return (uint64_t(b) << 32) | uint32_t(~uint32_t(id));
+}
+__device__ __forceinline__ float key_value(uint64_t key) {
+  const uint32_t b = uint32_t(key >> 32);
+  return __uint_as_float((b & 0x80000000u) ? (b & 0x7FFFFFFFu) : ~b);
+}
+__device__ __forceinline__ int key_id(uint64_t key) { return int(~uint32_t(key)); }
+
+// Wavefront reductions on DPP lane moves (no LDS round trip): two quad
+// permutes and two row rotations leave every lane of a 16-lane row with the
+// row's result; row broadcasts 15 and 31 carry it to lane 63, which is read
+// back as a wave-uniform value.  Lanes whose row is masked off receive the
+// identity.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp(uint32_t identity, uint32_t x) {
+  return uint32_t(__builtin_amdgcn_update_dpp(int(identity), int(x), CTRL, ROW_MASK, 0xF, false));
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint64_t max_step(uint64_t x) {
+  const uint64_t o = (uint64_t(dpp<CTRL, ROW_MASK>(0u, uint32_t(x >> 32))) << 32) | dpp<CTRL, ROW_MASK>(0u, uint32_t(x));
+  return o > x ? o : x;
+}
+__device__ __forceinline__ uint64_t wave_max_key(uint64_t x) {
+  x = max_step<0xB1, 0xF>(x);   // quad_perm [1,0,3,2]
+  x = max_step<0x4E, 0xF>(x);   // quad_perm [2,3,0,1]
+  x = max_step<0x124, 0xF>(x);  // row_ror:4
+  x = max_step<0x128, 0xF>(x);  // row_ror:8
+  x = max_step<0x142, 0xA>(x);  // row_bcast:15 into rows 1 and 3
+  x = max_step<0x143, 0xC>(x);  // row_bcast:31 into rows 2 and 3
+  const uint32_t hi = __builtin_amdgcn_readlane(uint32_t(x >> 32), 63);
+  const uint32_t lo = __builtin_amdgcn_readlane(uint32_t(x), 63);
+  return (uint64_t(hi) << 32) | lo;
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float fmax_step(float x) {
+  return fmaxf(x, __uint_as_float(dpp<CTRL, ROW_MASK>(__float_as_uint(-INFINITY), __float_as_uint(x))));
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float add_step(float x) {
+  return x + __uint_as_float(dpp<CTRL, ROW_MASK>(0u, __float_as_uint(x)));
+}
+__device__ __forceinline__ float wave_max(float x) {
+  x = fmax_step<0xB1, 0xF>(x);
+  x = fmax_step<0x4E, 0xF>(x);
+  x = fmax_step<0x124, 0xF>(x);
+  x = fmax_step<0x128, 0xF>(x);
+  x = fmax_step<0x142, 0xA>(x);
+  x = fmax_step<0x143, 0xC>(x);
+  return __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(x), 63));
+}
+__device__ __forceinline__ float wave_sum(float x) {
+  x = add_step<0xB1, 0xF>(x);
+  x = add_step<0x4E, 0xF>(x);
+  x = add_step<0x124, 0xF>(x);
+  x = add_step<0x128, 0xF>(x);
+  x = add_step<0x142, 0xA>(x);
+  x = add_step<0x143, 0xC>(x);
+  return __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(x), 63));
 }
 
-// k rounds of arg-max over the heads of each lane's sorted list.  On return
-// every lane holds the wave's top-k in (out_v, out_i) (lane-uniform).
+// (max, sum) of the wave: the sums are rescaled to the wave max, then added.
+__device__ __forceinline__ Partial wave_partial(Partial p, float scale) {
+  const float m = wave_max(p.m);
+  if (m == -INFINITY) return Partial{m, 0.f};
+  return Partial{m, wave_sum(p.s * __builtin_amdgcn_exp2f((p.m - m) * scale))};
+}
+
+// k rounds of a wave arg-max over the heads of the lanes' sorted key lists;
+// the lane that supplied the winner shifts its list.  Keys are unique except
+// the empty one, and shifting an empty list changes nothing.
 template <int K>
-__device__ __forceinline__ void wave_topk(float (&tv)[K], int (&ti)[K], int k, float (&out_v)[K],
-                                          int (&out_i)[K]) {
+__device__ __forceinline__ void wave_topk(uint64_t (&key)[K], int k, uint64_t (&out)[K]) {
 #pragma unroll
   for (int r = 0; r < K; ++r) {
-    float v = tv[0];
-    int i = ti[0];
+    if (r < k) {  // wave-uniform
+      const uint64_t best = wave_max_key(key[0]);
+      out[r] = best;
+      if (key[0] == best) {
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      const float ov = __shfl_xor(v, off);
-      const int oi = __shfl_xor(i, off);
-      if (better(ov, oi, v, i)) { v = ov; i = oi; }
-    }
-    out_v[r] = r < k ? v : -INFINITY;
-    out_i[r] = r < k ? i : INT32_MAX;
-    if (r < k && ti[0] == i && tv[0] == v) {  // ids are unique: this lane supplied the winner
-#pragma unroll
-      for (int j = 0; j < K - 1; ++j) { tv[j] = tv[j + 1]; ti[j] = ti[j + 1]; }
-      tv[K - 1] = -INFINITY;
-      ti[K - 1] = INT32_MAX;
+        for (int j = 0; j < K - 1; ++j) key[j] = key[j + 1];
+        key[K - 1] = rank_key(-INFINITY, INT32_MAX);
+      }
     }
   }
 }
 
-// Block-wide merge of per-thread (Partial, top-K); result valid in thread 0's
-// registers (and in every lane of wave 0).
+// Block-wide merge of the threads' (Partial, top-K).  Every wave reduces its
+// own lists; the 4k wave winners are then ranked by counting (ties of equal
+// keys by position), so each thread holding a block winner learns its output
+// slot without another round of reductions.  Returns the block's Partial in
+// every thread, and in threads with *slot in [0, k) the key of rank *slot.
 template <int K>
-__device__ void block_merge(Partial& p, float (&tv)[K], int (&ti)[K], int k, float scale,
-                            float (&res_v)[K], int (&res_i)[K]) {
-  __shared__ Partial sp[kBlock / 64];
-  __shared__ float sv[kBlock / 64][K];
-  __shared__ int si[kBlock / 64][K];
+__device__ __forceinline__ uint64_t block_merge(Partial& p, const float (&tv)[K], const int (&ti)[K], int k,
+                                                float scale, int* slot) {
+  constexpr int kWaves = kBlock / 64;
+  __shared__ Partial sp[kWaves];
+  __shared__ uint64_t sk[kWaves * K];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  p = wave_combine(p, scale);
-  float wv[K];
-  int wi[K];
+  const Partial wp = wave_partial(p, scale);
+  uint64_t key[K], out[K];
 #pragma unroll
-  for (int r = 0; r < K; ++r) { wv[r] = -INFINITY; wi[r] = INT32_MAX; }
-  wave_topk<K>(tv, ti, k, wv, wi);
+  for (int r = 0; r < K; ++r) key[r] = rank_key(tv[r], ti[r]);
+  wave_topk<K>(key, k, out);
   if (lane == 0) {
-    sp[wave] = p;
+    sp[wave] = wp;
 #pragma unroll
-    for (int r = 0; r < K; ++r) { sv[wave][r] = wv[r]; si[wave][r] = wi[r]; }
+    for (int r = 0; r < K; ++r)
+      if (r < k) sk[wave * k + r] = out[r];
   }
   __syncthreads();
-  if (wave == 0) {
-    Partial q{-INFINITY, 0.f};
-    for (int w = 0; w < kBlock / 64; ++w) q = combine(q, sp[w], scale);  // fixed order
-    p = q;
-    // lanes 0..3 hold the four wave lists; other lanes are empty
+  Partial q{-INFINITY, 0.f};
 #pragma unroll
-    for (int r = 0; r < K; ++r) {
-      tv[r] = lane < kBlock / 64 ? sv[lane][r] : -INFINITY;
-      ti[r] = lane < kBlock / 64 ? si[lane][r] : INT32_MAX;
-    }
-#pragma unroll
-    for (int r = 0; r < K; ++r) { res_v[r] = -INFINITY; res_i[r] = INT32_MAX; }
-    wave_topk<K>(tv, ti, k, res_v, res_i);
+  for (int w = 0; w < kWaves; ++w) q = combine(q, sp[w], scale);  // fixed order
+  p = q;
+  const int n = kWaves * k, t = threadIdx.x;
+  *slot = -1;
+  if (t >= n) return 0;
+  const uint64_t e = sk[t];
+  int rank = 0;
+  for (int j = 0; j < n; ++j) {
+    const uint64_t o = sk[j];
+    rank += int(o > e) + int(o == e && j < t);
   }
+  *slot = rank;
+  return e;
 }
 
-template <int K>
-__device__ __forceinline__ void finalize(int64_t row, Partial p, const float (&v)[K], const int (&id)[K],
-                                         int k, float tau, float* lse, float* cand_logp,
-                                         int32_t* cand_ids) {
+// Outputs of the row from the merged result: lse once, and one candidate per
+// thread holding a rank below k.
+__device__ __forceinline__ void emit_row(int64_t row, Partial p, uint64_t key, int slot, int k, float tau,
+                                         float* lse, float* cand_logp, int32_t* cand_ids) {
+  if (slot < 0 || slot >= k) return;
   const float log_s = logf(p.s);
-  lse[row] = p.m / tau + log_s;
-#pragma unroll
-  for (int r = 0; r < K; ++r) {
-    if (r < k) {
-      cand_logp[row * k + r] = (v[r] - p.m) / tau - log_s;
-      cand_ids[row * k + r] = id[r];
-    }
-  }
+  if (slot == 0) lse[row] = p.m / tau + log_s;
+  cand_logp[row * k + slot] = (key_value(key) - p.m) / tau - log_s;
+  cand_ids[row * k + slot] = key_id(key);
 }
 
 constexpr int kChunk = 4;  // float4 loads in flight per thread
@@ -216,14 +274,14 @@ __global__ __launch_bounds__(kBlock) void lse_topk_rows(const float* __restrict_
 #pragma unroll
       for (int c = 0; c < kChunk; ++c) mx = fmaxf(mx, fmaxf(fmaxf(x[c][0], x[c][1]), fmaxf(x[c][2], x[c][3])));
       if (mx > p.m) {
-        p.s *= exp2f((p.m - mx) * scale);
+        p.s *= __builtin_amdgcn_exp2f((p.m - mx) * scale);
         p.m = mx;
       }
       float acc = 0.f;
 #pragma unroll
       for (int c = 0; c < kChunk; ++c)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc += exp2f((x[c][i] - p.m) * scale);
+        for (int i = 0; i < 4; ++i) acc += __builtin_amdgcn_exp2f((x[c][i] - p.m) * scale);
       p.s += acc;
       if (mx > tv[K - 1]) {
         // only this lane's values above its current K-th are visited, in id order
@@ -249,31 +307,29 @@ __global__ __launch_bounds__(kBlock) void lse_topk_rows(const float* __restrict_
     for (int v = v0 + tid; v < v1; v += kBlock) {
       const float x = zr[v];
       if (x > p.m) {
-        p.s *= exp2f((p.m - x) * scale);
+        p.s *= __builtin_amdgcn_exp2f((p.m - x) * scale);
         p.m = x;
       }
-      p.s += exp2f((x - p.m) * scale);
+      p.s += __builtin_amdgcn_exp2f((x - p.m) * scale);
       if (x > tv[K - 1]) insert_ascending<K>(x, v, tv, ti);
     }
   }
 
-  float rv[K];
-  int ri[K];
-  block_merge<K>(p, tv, ti, k, scale, rv, ri);
-  if (tid != 0) return;
+  int slot;
+  const uint64_t key = block_merge<K>(p, tv, ti, k, scale, &slot);
   if (nseg == 1) {
-    finalize<K>(row, p, rv, ri, k, tau, lse, cand_logp, cand_ids);
+    emit_row(row, p, key, slot, k, tau, lse, cand_logp, cand_ids);
     return;
   }
+  if (slot < 0 || slot >= k) return;
   constexpr int RF = record_floats<K>();
   float* rec = part + (row * nseg + seg) * RF;
-  rec[0] = p.m;
-  rec[1] = p.s;
-#pragma unroll
-  for (int r = 0; r < K; ++r) {
-    rec[4 + r] = rv[r];
-    rec[4 + K + r] = __int_as_float(ri[r]);
+  if (slot == 0) {
+    rec[0] = p.m;
+    rec[1] = p.s;
   }
+  rec[4 + slot] = key_value(key);
+  rec[4 + K + slot] = __int_as_float(key_id(key));
 }
 
 // grid: rows.  Merge the row's segment records, every thread folding single
@@ -287,10 +343,9 @@ __global__ __launch_bounds__(kBlock) void lse_topk_merge(int nseg, int k, float 
   float tv[K];
   int ti[K];
   fold_records<K>(part + row * nseg * record_floats<K>(), nseg, k, scale, p, tv, ti);
-  float rv[K];
-  int ri[K];
-  block_merge<K>(p, tv, ti, k, scale, rv, ri);
-  if (threadIdx.x == 0) finalize<K>(row, p, rv, ri, k, tau, lse, cand_logp, cand_ids);
+  int slot;
+  const uint64_t key = block_merge<K>(p, tv, ti, k, scale, &slot);
+  emit_row(row, p, key, slot, k, tau, lse, cand_logp, cand_ids);
 }
 
 // Segments per row: enough blocks to fill 256 CUs a few times over, but no
