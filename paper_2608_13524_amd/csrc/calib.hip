@@ -1,0 +1,135 @@
+// Calibration kernels: a streaming read, a copy and a matrix-core-only loop,
+// the achievable ceilings for the HBM-bound and MFMA-bound kernels.
+#include "dartree_calib.h"
+#include "internal.hpp"
+
+namespace dartree {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 8;  // 16-byte loads in flight per thread
+
+// Grid-stride read: per step a workgroup reads kUnroll * 256 consecutive
+// 16-byte words, each thread kUnroll of them at a stride of 256 words.
+__global__ __launch_bounds__(kThreads) void calib_read(const f32x4* __restrict__ src, int64_t n, float* sink) {
+  const int64_t stride = int64_t(gridDim.x) * kThreads * kUnroll;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int64_t i = int64_t(blockIdx.x) * kThreads * kUnroll + threadIdx.x; i < n; i += stride) {
+    f32x4 x[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t j = i + int64_t(u) * kThreads;
+      x[u] = j < n ? __builtin_nontemporal_load(src + j) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) acc += x[u];
+  }
+  __shared__ float red[kThreads];
+  red[threadIdx.x] = acc[0] + acc[1] + acc[2] + acc[3];
+  __syncthreads();
+  for (int s = kThreads / 2; s > 0; s >>= 1) {
+    if (threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) sink[blockIdx.x] = red[0];
+}
+
+__global__ __launch_bounds__(kThreads) void calib_copy(f32x4* __restrict__ dst, const f32x4* __restrict__ src,
+                                                       int64_t n) {
+  const int64_t stride = int64_t(gridDim.x) * kThreads * kUnroll;
+  for (int64_t i = int64_t(blockIdx.x) * kThreads * kUnroll + threadIdx.x; i < n; i += stride) {
+    f32x4 x[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t j = i + int64_t(u) * kThreads;
+      if (j < n) x[u] = src[j];
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t j = i + int64_t(u) * kThreads;
+      if (j < n) dst[j] = x[u];
+    }
+  }
+}
+
+// Register-only bf16 MFMA loop: an 8 x 8 grid of independent accumulators
+// per wave (64 products per round), one wave per SIMD.
+__device__ __forceinline__ bf16x8 calib_operand(int lane, int shift, int mul, float unit) {
+  bf16x8 v;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v[j] = __bf16(float((lane * mul + j + shift) & 7) * unit);
+  return v;
+}
+
+__global__ __launch_bounds__(kThreads) void calib_mfma(int iters, float* sink) {
+  const int lane = threadIdx.x & 63;
+  bf16x8 a[8], b[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = calib_operand(lane, i, 1, 0.125f);
+    b[i] = calib_operand(lane, i, 3, 0.0625f);
+  }
+  f32x4 c[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) c[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int it = 0; it < iters; ++it)
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) c[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], c[i][j], 0, 0, 0);
+  float v = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v += (c[i][j][0] + c[i][j][1]) + (c[i][j][2] + c[i][j][3]);
+  __shared__ float red[kThreads / 64];
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  if (lane == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = red[0] + red[1] + red[2] + red[3];
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Enough workgroups for several per CU on 256 CUs, within the sink.
+unsigned stream_grid(int64_t n16) {
+  const int64_t want = (n16 + kThreads * kUnroll - 1) / (kThreads * kUnroll);
+  return unsigned(std::max<int64_t>(1, std::min<int64_t>(want, 2048)));
+}
+
+}  // namespace
+}  // namespace dartree
+
+using namespace dartree;
+
+extern "C" {
+
+dartree_status dartree_calib_read(const void* src, size_t bytes, float* sink, hipStream_t stream) {
+  if (!src || !sink || bytes == 0 || bytes % 16 != 0 || !aligned16(src)) return DARTREE_ERR_INVALID_ARG;
+  const int64_t n = int64_t(bytes / 16);
+  hipLaunchKernelGGL(calib_read, dim3(stream_grid(n)), dim3(kThreads), 0, stream, static_cast<const f32x4*>(src), n,
+                     sink);
+  return hipGetLastError() == hipSuccess ? DARTREE_OK : DARTREE_ERR_HIP;
+}
+
+dartree_status dartree_calib_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
+  if (!src || !dst || bytes == 0 || bytes % 16 != 0 || !aligned16(src) || !aligned16(dst))
+    return DARTREE_ERR_INVALID_ARG;
+  const char* s = static_cast<const char*>(src);
+  const char* d = static_cast<const char*>(dst);
+  if (s < d + bytes && d < s + bytes) return DARTREE_ERR_INVALID_ARG;
+  const int64_t n = int64_t(bytes / 16);
+  hipLaunchKernelGGL(calib_copy, dim3(stream_grid(n)), dim3(kThreads), 0, stream, static_cast<f32x4*>(dst),
+                     static_cast<const f32x4*>(src), n);
+  return hipGetLastError() == hipSuccess ? DARTREE_OK : DARTREE_ERR_HIP;
+}
+
+dartree_status dartree_calib_mfma(int32_t blocks, int32_t iters, float* sink, hipStream_t stream) {
+  if (!sink || blocks < 1 || blocks > DARTREE_CALIB_SINK_FLOATS || iters < 1) return DARTREE_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(calib_mfma, dim3(unsigned(blocks)), dim3(kThreads), 0, stream, int(iters), sink);
+  return hipGetLastError() == hipSuccess ? DARTREE_OK : DARTREE_ERR_HIP;
+}
+
+}  // extern "C"

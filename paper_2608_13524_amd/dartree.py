@@ -31,7 +31,9 @@ SYMBOLS = [
     "dartree_build_tree", "dartree_build_tree_timed", "dartree_export_supertree", "dartree_export_states", "dartree_project",
     "dartree_lse_topk_workspace_size", "dartree_lse_topk", "dartree_select_topw",
     "dartree_prune_levels",
+    "dartree_calib_read", "dartree_calib_copy", "dartree_calib_mfma",
 ]
+CALIB_SINK_FLOATS = 4096
 
 
 class Params(ctypes.Structure):
@@ -108,6 +110,9 @@ def lib() -> ctypes.CDLL:
     L.dartree_lse_topk.argtypes = [vp, i32, i32, i32, f32, vp, vp, vp, vp, sz, vp]
     L.dartree_select_topw.argtypes = [i32, i32, i32, i32, f32, vp, vp, vp, vp, vp, vp, vp]
     L.dartree_prune_levels.argtypes = [P, vp, vp, vp, ctypes.POINTER(TreeC), vp]
+    L.dartree_calib_read.argtypes = [vp, sz, vp, vp]
+    L.dartree_calib_copy.argtypes = [vp, vp, sz, vp]
+    L.dartree_calib_mfma.argtypes = [i32, i32, vp, vp]
     for name in SYMBOLS:
         if name not in ("dartree_abi_version", "dartree_status_string"):
             getattr(L, name).restype = ctypes.c_int
@@ -328,3 +333,23 @@ def prune_levels(p: Params, tokens, parents, scores, out: DeviceTree, stream=Non
     tc = out.c()
     _check(lib().dartree_prune_levels(ctypes.byref(p), _ptr(tokens), _ptr(parents), _ptr(scores),
                                       ctypes.byref(tc), _stream(stream)), "dartree_prune_levels")
+
+
+# ---------------------------------------------------------------------------
+# Calibration kernels (achievable ceilings; they compute nothing of the method)
+def calib_read(src, sink, stream=None) -> None:
+    """Stream src (any contiguous device tensor, size a multiple of 16 bytes) once."""
+    nbytes = src.numel() * src.element_size()
+    _check(lib().dartree_calib_read(_ptr(src), nbytes, _ptr(sink), _stream(stream)), "dartree_calib_read")
+
+
+def calib_copy(dst, src, stream=None) -> None:
+    nbytes = src.numel() * src.element_size()
+    assert dst.numel() * dst.element_size() >= nbytes
+    _check(lib().dartree_calib_copy(_ptr(dst), _ptr(src), nbytes, _stream(stream)), "dartree_calib_copy")
+
+
+def calib_mfma(blocks: int, iters: int, sink, stream=None) -> float:
+    """Launch the MFMA-only loop; returns its flop count."""
+    _check(lib().dartree_calib_mfma(blocks, iters, _ptr(sink), _stream(stream)), "dartree_calib_mfma")
+    return float(blocks) * 4 * iters * 64 * (2 * 16 * 16 * 32)

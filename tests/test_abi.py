@@ -10,18 +10,19 @@ import pytest
 from paper_2608_13524_amd import dartree as D
 from paper_2608_13524_amd import workloads as W
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "dartree.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+HEADERS = sorted(os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h"))
 FAKE = 0x10000  # 16-byte aligned address that is never dereferenced
 
 
 def declared_symbols():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(dartree_\w+)\s*\(", text, re.M)))
 
 
 def test_library_exports_every_declared_symbol():
     syms = declared_symbols()
-    assert len(syms) == 15, syms
+    assert len(syms) == 18, syms
     lib = D.lib()
     for s in syms:
         assert hasattr(lib, s), s
@@ -135,3 +136,20 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(D, "LIB_PATH", str(tmp_path / "absent.so"))
     with pytest.raises(RuntimeError, match="no fallback"):
         D.lib()
+
+
+def test_calibration_kernels_reject_bad_arguments():
+    lib = D.lib()
+    sink = ctypes.c_void_p(FAKE)
+    assert lib.dartree_calib_read(None, 1024, sink, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_read(ctypes.c_void_p(FAKE), 1000, sink, None) == D.ERR_INVALID_ARG   # not 16 B units
+    assert lib.dartree_calib_read(ctypes.c_void_p(FAKE + 4), 1024, sink, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_read(ctypes.c_void_p(FAKE), 0, sink, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_read(ctypes.c_void_p(FAKE), 1024, None, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_copy(ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE + 512), 1024, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_copy(ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE + 4096), 1000, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_copy(None, ctypes.c_void_p(FAKE), 1024, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_mfma(0, 10, sink, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_mfma(D.CALIB_SINK_FLOATS + 1, 10, sink, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_mfma(4, 0, sink, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_mfma(4, 10, None, None) == D.ERR_INVALID_ARG

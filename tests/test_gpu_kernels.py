@@ -237,3 +237,38 @@ def test_lse_topk_workspace_reuse():
         torch.cuda.synchronize()
         for r in range(rows):
             assert np.array_equal(ids.cpu().numpy()[r], R.topk_ids(z[r].astype(np.float64), k))
+
+
+def test_calibration_kernels():
+    """The calibration kernels do the work they state: the copy is exact, the
+    streaming read sums every element, the MFMA loop gives the closed-form sum."""
+    dev = device()
+    g = torch.Generator().manual_seed(7)
+    n = (1 << 20) + 4 * 37                        # ragged against the grid
+    src = torch.randint(-8, 8, (n,), generator=g).float().to(dev)
+    dst = torch.zeros_like(src)
+    sink = torch.zeros(D.CALIB_SINK_FLOATS, device=dev)
+    say("calib copy/read/mfma")
+    D.calib_copy(dst, src)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src)
+    D.calib_read(src, sink)
+    torch.cuda.synchronize()
+    assert float(sink.double().sum()) == float(src.double().sum())   # small integers: exact in fp32
+    sink.zero_()
+    D.calib_mfma(3, 5, sink)
+    torch.cuda.synchronize()
+    # accumulator (i, j) adds the tile a_i b_j^T every round: 4 waves, 5 rounds
+    lane = torch.arange(64)
+
+    def operand(shift, mul, unit):                 # lane l holds row l % 16, k-group l // 16
+        vals = torch.stack([((lane * mul + e + shift) & 7).float() * unit for e in range(8)], 1)
+        M = torch.zeros(16, 32)
+        for l in range(64):
+            M[l % 16, 8 * (l // 16):8 * (l // 16) + 8] = vals[l]
+        return M
+
+    tile = sum(float((operand(i, 1, 0.125) @ operand(j, 3, 0.0625).T).sum()) for i in range(8) for j in range(8))
+    want = 4 * 5 * tile
+    got = sink[:3].cpu()
+    assert torch.allclose(got, torch.full((3,), want), rtol=1e-6), (got, want)

@@ -158,3 +158,34 @@ def test_full_size_parity(name):
     tol = max(tol, replay.EPS)
     free = replay.follow(dec, sup, tree, batch_index=reqs, requests=reqs, eps=tol, score_tol=max(tol, replay.SCORE_TOL))
     _log_report(name, f"free-running(window {tol:.3g})", free)
+
+
+def test_graph_replay_matches_eager():
+    """One round captured in a HIP graph: every replay, with eager rounds on
+    other inputs in between, gives the eager result bit for bit."""
+    cfg = small(seed=45, batch=2)
+    inputs = W.make_inputs(cfg)
+    other = W.make_inputs(cfg.replace(seed=46))
+    dev = device()
+    p = D.Params.of(cfg)
+    di = D.DeviceInputs.from_host(inputs, dev)
+    do = D.DeviceInputs.from_host(other, dev)
+    ws = D.alloc_workspace(p, dev)
+    out = D.DeviceTree.alloc(cfg.batch, cfg.budget, dev)
+    say("graph capture of build_tree")
+    D.build_tree(p, di, ws, out)
+    torch.cuda.synchronize()
+    want = out.host()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        D.build_tree(p, di, ws, out)
+    for rep in range(4):
+        D.build_tree(p, do, ws, out)               # eager work on other inputs in between
+        torch.cuda.synchronize()
+        for f in dataclasses.fields(out):
+            getattr(out, f.name).fill_(-7)
+        g.replay()
+        torch.cuda.synchronize()
+        got = out.host()
+        for k in want:
+            assert np.array_equal(got[k], want[k]), (rep, k)
