@@ -207,8 +207,6 @@ def main() -> int:
     for i in range(K):
         for d in range(1, cfg.depth + 1):
             for c, name in enumerate(D.KERNEL_NAMES):
-                if name == "state" and d == cfg.depth:
-                    continue
                 j = (d - 1) * nk + c
                 dur[name].append(kev[i][2 * j].elapsed_time(kev[i][2 * j + 1]) * 1e3)
                 if i == 0:

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define DARTREE_ABI_VERSION 1
+#define DARTREE_ABI_VERSION 2
 
 /* Limits of this implementation (calls beyond them return
  * DARTREE_ERR_UNSUPPORTED). */
@@ -162,16 +162,16 @@ dartree_status dartree_build_tree(const dartree_params* p, const dartree_inputs*
 /* Kernels of one round, in launch order, as indexed by dartree_build_tree_timed. */
 #define DARTREE_KERNEL_HEAD 0   /* t = A r, a = bf16(tanh(t + H_d)) */
 #define DARTREE_KERNEL_LOGITS 1 /* z = L_d^base + U a */
-#define DARTREE_KERNEL_LSE 2    /* log-softmax normaliser and per-row top-k */
-#define DARTREE_KERNEL_TOPW 3   /* segmented top-W */
-#define DARTREE_KERNEL_STATE 4  /* state update (not launched at d = L) */
-#define DARTREE_KERNELS_PER_DEPTH 5
+#define DARTREE_KERNEL_LSE 2    /* log-softmax normaliser and per-row top-k (row segments) */
+#define DARTREE_KERNEL_SELECT 3 /* segment merge, segmented top-W and the state update
+                                   of the kept children (no state update at d = L) */
+#define DARTREE_KERNELS_PER_DEPTH 4
 
 /* dartree_build_tree that also records `events` (created by the caller, for
  * instance with hipEventCreate) on `stream` around each launch: for depth d
  * and kernel kind c, events[2 i] before and events[2 i + 1] after, with
  * i = (d - 1) * DARTREE_KERNELS_PER_DEPTH + c; the prune is i = L *
- * DARTREE_KERNELS_PER_DEPTH.  `events` holds 2 (5 L + 1) entries; NULL
+ * DARTREE_KERNELS_PER_DEPTH.  `events` holds 2 (4 L + 1) entries; NULL
  * entries are not recorded.  For measuring kernel durations inside a round. */
 dartree_status dartree_build_tree_timed(const dartree_params* p, const dartree_inputs* in, void* ws,
                                         size_t ws_bytes, const dartree_tree* out, hipEvent_t* events,

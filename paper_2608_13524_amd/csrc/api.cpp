@@ -213,27 +213,43 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   tm.mark(tb + DARTREE_KERNEL_LOGITS, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
 
-  // K3: lse and top-k per parent row
+  // K3: lse and top-k per parent row (segment records, if any, are merged by K4)
   tm.mark(tb + DARTREE_KERNEL_LSE, 0);
-  err = launch_lse_topk(z, R, V, int(k), tau, lse, clp, cid, at<char>(ws, l.k3), st);
+  err = launch_lse_topk(z, R, V, int(k), tau, lse, clp, cid, at<char>(ws, l.k3), false, st);
   tm.mark(tb + DARTREE_KERNEL_LSE, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
 
-  // K4: S_d = segmented top-W; level arrays have stride W per request
-  tm.mark(tb + DARTREE_KERNEL_TOPW, 0);
-  err = launch_select_topw(int(b), int(np), int(k), int(nc), p.depth_bonus, int(W), int(W), parent_score, clp, cid,
-                           tok, par, score, st);
-  tm.mark(tb + DARTREE_KERNEL_TOPW, 1);
+  // K4 (+ K5): S_d = segmented top-W, level arrays with stride W per request,
+  // and the states of the kept children (unused after the last depth)
+  LevelArgs la{};
+  la.batch = int(b);
+  la.n_parent = int(np);
+  la.k = int(k);
+  la.n_keep = int(nc);
+  la.beta = p.depth_bonus;
+  la.tau = tau;
+  la.parent_stride = int(W);
+  la.out_stride = int(W);
+  la.parent_score = parent_score;
+  la.nseg = lse_topk_segments(R, V);
+  la.part = at<float>(ws, l.k3);
+  la.lse = lse;
+  la.cand_logp = clp;
+  la.cand_ids = cid;
+  la.out_tok = tok;
+  la.out_par = par;
+  la.out_score = score;
+  la.state = d < p.depth;
+  la.precision = p.precision;
+  la.hidden = int(h);
+  la.t = t;
+  la.U = in.head_U;
+  la.e = e;
+  la.r_out = r_out;
+  tm.mark(tb + DARTREE_KERNEL_SELECT, 0);
+  err = launch_select_level(la, st);
+  tm.mark(tb + DARTREE_KERNEL_SELECT, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
-
-  // K5: states of the kept children (unused after the last depth)
-  if (d < p.depth) {
-    tm.mark(tb + DARTREE_KERNEL_STATE, 0);
-    err = launch_state_update(p.precision, int(b), int(nc), int(np), int(h), int(W), tok, par, t, in.head_U, e, r_out,
-                             st);
-    tm.mark(tb + DARTREE_KERNEL_STATE, 1);
-    if (err != hipSuccess) return DARTREE_ERR_HIP;
-  }
   return DARTREE_OK;
 }
 
@@ -384,7 +400,7 @@ dartree_status dartree_lse_topk(const float* z, int32_t rows, int32_t vocab, int
   if (!z || !lse || !cand_logp || !cand_ids) return DARTREE_ERR_INVALID_ARG;
   if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return DARTREE_ERR_WORKSPACE;
   const float tau = temperature > 0.f ? temperature : 1.f;
-  return hip_status(launch_lse_topk(z, rows, vocab, k, tau, lse, cand_logp, cand_ids, ws, stream));
+  return hip_status(launch_lse_topk(z, rows, vocab, k, tau, lse, cand_logp, cand_ids, ws, true, stream));
 }
 
 dartree_status dartree_select_topw(int32_t batch, int32_t n_parent, int32_t k, int32_t n_keep, float depth_bonus,
@@ -395,8 +411,24 @@ dartree_status dartree_select_topw(int32_t batch, int32_t n_parent, int32_t k, i
   if (n_keep > n_parent * k) return DARTREE_ERR_INVALID_ARG;
   if (!isfinite(depth_bonus) || depth_bonus > 0.f) return DARTREE_ERR_INVALID_ARG;
   if (!cand_logp || !cand_ids || !out_tokens || !out_parents || !out_scores) return DARTREE_ERR_INVALID_ARG;
-  return hip_status(launch_select_topw(batch, n_parent, k, n_keep, depth_bonus, n_parent, n_keep, parent_score,
-                                       cand_logp, cand_ids, out_tokens, out_parents, out_scores, stream));
+  LevelArgs la{};
+  la.batch = batch;
+  la.n_parent = n_parent;
+  la.k = k;
+  la.n_keep = n_keep;
+  la.beta = depth_bonus;
+  la.tau = 1.f;
+  la.parent_stride = n_parent;
+  la.out_stride = n_keep;
+  la.parent_score = parent_score;
+  la.nseg = 1;
+  la.cand_logp = const_cast<float*>(cand_logp);      // read only when nseg == 1
+  la.cand_ids = const_cast<int32_t*>(cand_ids);
+  la.out_tok = out_tokens;
+  la.out_par = out_parents;
+  la.out_score = out_scores;
+  la.state = 0;
+  return hip_status(launch_select_level(la, stream));
 }
 
 dartree_status dartree_prune_levels(const dartree_params* p, const int32_t* tokens, const int32_t* parents,

@@ -58,27 +58,40 @@ struct ProjArgs {
 };
 hipError_t launch_project(const ProjArgs& a, hipStream_t s);
 
-// Row-wise online log-sum-exp and top-k (K3); scratch holds the per-segment
-// records when rows are split (lse_topk_scratch_bytes > 0).
+// Row-wise online log-sum-exp and top-k (K3).  Rows are split into
+// lse_topk_segments(rows, vocab) segments; with more than one, each segment
+// leaves a record in scratch (lse_topk_scratch_bytes) and, if `merge`, a
+// second kernel merges them into lse / cand_logp / cand_ids.  Without
+// `merge` the records are left for launch_select_level.
+int lse_topk_segments(int64_t rows, int64_t vocab);
 size_t lse_topk_scratch_bytes(int64_t rows, int64_t vocab, int k);
 hipError_t launch_lse_topk(const float* z, int64_t rows, int64_t vocab, int k, float tau,
                            float* lse, float* cand_logp, int32_t* cand_ids, void* scratch,
-                           hipStream_t s);
+                           bool merge, hipStream_t s);
 
-// Segmented top-W over n_parent * k candidates per request (K4).
-// Parent scores of request q start at parent_score + q * parent_stride (NULL:
-// all zero); outputs of request q at out + q * out_stride.
-hipError_t launch_select_topw(int batch, int n_parent, int k, int n_keep, float beta,
-                              int parent_stride, int out_stride,
-                              const float* parent_score, const float* cand_logp,
-                              const int32_t* cand_ids, int32_t* out_tok, int32_t* out_par,
-                              float* out_score, hipStream_t s);
-
-// State update of the kept children (K5); level entries of request q start at
-// q * lvl_stride.
-hipError_t launch_state_update(int precision, int batch, int n_child, int n_parent, int hidden, int lvl_stride,
-                               const int32_t* lvl_tok, const int32_t* lvl_par, const float* t,
-                               const void* U, float e, void* r_out, hipStream_t s);
+// One depth's selection (K4) with the K3 segment merge and the K5 state
+// update.  Rows of request q are q * n_parent .. q * n_parent + n_parent - 1.
+struct LevelArgs {
+  int batch, n_parent, k, n_keep;
+  float beta, tau;
+  int parent_stride, out_stride;  // level entries of request q start at q * stride
+  const float* parent_score;      // NULL: all zero (depth 1)
+  int nseg;                       // > 1: merge the records in `part` and store lse / cand_*
+  const float* part;
+  float* lse;
+  float* cand_logp;               // [rows][k]; read when nseg == 1
+  int32_t* cand_ids;
+  int32_t* out_tok;
+  int32_t* out_par;
+  float* out_score;
+  int state;                      // 0: no state update
+  int precision, hidden;
+  const float* t;                 // [rows][hidden]
+  const void* U;                  // act [V][hidden]
+  float e;
+  void* r_out;                    // act [batch * n_keep][hidden]
+};
+hipError_t launch_select_level(const LevelArgs& a, hipStream_t s);
 
 // Deferred top-B prune and tree emission (K6).
 struct LevelShape {

@@ -331,10 +331,12 @@ __global__ __launch_bounds__(256) void proj_bf16_big(KArgs a, int vec) {
   const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(X + int64_t(m0) * K), (short)0, min(GBM, M - m0) * K * 2, 0x00020000);
   // load i of wave w moves rows 64 w + 8 i + lane / 8; LDS chunk lane % 8 holds
-  // global chunk (lane % 8) ^ swizzle(row)
+  // global chunk (lane % 8) ^ swizzle(row).  The row offset is part of the
+  // per-lane offset, which the buffer range check covers (rows past the
+  // matrix read as zero); the scalar offset carries only the k position.
   const int lrow = lane >> 3, lcp = lane & 7;
-  const unsigned vo0 = unsigned(lrow * K * 2 + ((lcp ^ swz16(lrow)) * 16));
-  const unsigned vo1 = unsigned(lrow * K * 2 + ((lcp ^ swz16(8 + lrow)) * 16));
+  const unsigned vrow = unsigned((64 * wave + lrow) * K * 2);
+  const unsigned vc0 = unsigned((lcp ^ swz16(lrow)) * 16), vc1 = unsigned((lcp ^ swz16(8 + lrow)) * 16);
   const int ax0 = (wn * 128 + r16) * GBK + ((kg ^ swz16(r16)) * 8);
   const int ax1 = (wn * 128 + r16) * GBK + (((4 + kg) ^ swz16(r16)) * 8);
   const int bx0 = GBN * GBK + (wm * 128 + r16) * GBK + ((kg ^ swz16(r16)) * 8);
@@ -348,13 +350,13 @@ __global__ __launch_bounds__(256) void proj_bf16_big(KArgs a, int vec) {
 
   auto load = [&](int buf, int kt) {
     LDS_AS uint16_t* base = (LDS_AS uint16_t*)smem[buf];  // generic -> LDS address space
+    const unsigned so = unsigned(kt * GBK * 2);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const unsigned so = unsigned((64 * wave + 8 * i) * K * 2 + kt * GBK * 2);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (LDS_AS void*)(base + (64 * wave + 8 * i) * GBK), 16,
-                                               (i & 1) ? vo1 : vo0, so, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS_AS void*)(base + GBN * GBK + (64 * wave + 8 * i) * GBK), 16,
-                                               (i & 1) ? vo1 : vo0, so, 0, 0);
+      const unsigned vo = vrow + unsigned(8 * i * K * 2) + ((i & 1) ? vc1 : vc0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (LDS_AS void*)(base + (64 * wave + 8 * i) * GBK), 16, vo, so, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS_AS void*)(base + GBN * GBK + (64 * wave + 8 * i) * GBK), 16, vo,
+                                               so, 0, 0);
     }
   };
   auto rd = [&](const LDS_AS uint16_t* S, int off) {

@@ -1,10 +1,11 @@
 // Selection and tree kernels of one round:
-//  * select_topw  (Algorithm 1, "score each child ... retain the global top-W"):
-//    per request, the n_parent * k candidates get s = (s_parent + log q~) + beta
-//    (eq. (5) one depth at a time) and the best n_keep by
-//    (s desc, parent slot asc, token asc) become S_d, in that order.
-//  * state_update (Algorithm 1, "update their states"): r = act(tanh(t_parent
-//    + e U[token])) for every kept child.
+//  * select_level (Algorithm 1, scoring the children, keeping the global
+//    top-W and updating their states): per request, the n_parent * k
+//    candidates get s = (s_parent + log q~) + beta (eq. (5) one depth at a
+//    time), the best n_keep by (s desc, parent slot asc, token asc) become
+//    S_d in that order, and every kept child gets r = act(tanh(t_parent +
+//    e U[token])).  The kernel also finishes the softmax pass when that pass
+//    split its rows into segments.
 //  * prune_emit   (Sec. 3.3, deferred best-first pruning): top-B of the whole
 //    supertree by (s desc, depth asc, slot asc) - prefix-closed by Lemma 1 -
 //    flattened in canonical breadth-first order (depth, parent's output index,
@@ -15,7 +16,9 @@
 // result does not depend on thread timing.
 #include <float.h>
 
-#include "internal.hpp"
+#include <algorithm>
+
+#include "reduce.hpp"
 
 namespace dartree {
 namespace {
@@ -44,75 +47,127 @@ __device__ __forceinline__ int next_pow2(int n) {
   return p;
 }
 
-// grid: batch.  Low key word: parent slot (12 bits) << 20 | token (20 bits).
-__global__ __launch_bounds__(1024) void select_topw(int n_parent, int k, int n_keep, float beta,
-                                                    int parent_stride, int out_stride,
-                                                    const float* __restrict__ parent_score,
-                                                    const float* __restrict__ cand_logp,
-                                                    const int32_t* __restrict__ cand_ids, int32_t* out_tok,
-                                                    int32_t* out_par, float* out_score) {
-  __shared__ uint64_t keys[kSortMax];
-  const int q = blockIdx.x;
-  const int n = n_parent * k;
-  const int npad = next_pow2(n);
-  const int64_t rbase = int64_t(q) * n_parent;
-  for (int c = threadIdx.x; c < npad; c += blockDim.x) {
-    uint64_t key = ~0ull;
-    if (c < n) {
-      const int j = c / k;
-      const float sp = parent_score ? parent_score[int64_t(q) * parent_stride + j] : 0.f;
-      const float s = (sp + cand_logp[rbase * k + c]) + beta;
-      const uint32_t lo = (uint32_t(j) << 20) | uint32_t(cand_ids[rbase * k + c]);
-      key = (uint64_t(score_desc_key(s)) << 32) | lo;
-    }
-    keys[c] = key;
-  }
-  __syncthreads();
-  bitonic_sort(keys, npad);
-  for (int i = threadIdx.x; i < n_keep; i += blockDim.x) {
-    const uint64_t key = keys[i];
-    const uint32_t lo = uint32_t(key);
-    const int64_t o = int64_t(q) * out_stride + i;
-    out_tok[o] = int32_t(lo & 0xFFFFFu);
-    out_par[o] = int32_t(lo >> 20);
-    out_score[o] = score_from_desc_key(uint32_t(key >> 32));
-  }
-}
+// grid: batch * S, block (q, sl): request q, state slice sl.  Three steps of
+// one depth in one launch:
+//  1. the candidate log-probabilities of request q's parent rows: read as
+//     written by the softmax pass, or merged here from its per-segment
+//     records (one wave per row; block 0 of the request also stores them);
+//  2. s = (s_parent + log q~) + beta for every candidate and the best n_keep
+//     by (s desc, parent slot asc, token asc), from one bitonic sort of 64-bit
+//     keys (low word: parent slot (12 bits) << 20 | token (20 bits)); block 0
+//     of the request writes the level;
+//  3. the states r = act(tanh(t_parent + e U[token])) of kept children sl,
+//     sl + S, ... (child i of request q is row q * n_keep + i).
+// Steps 1-2 run in each of the S blocks of a request, which then need no
+// further synchronisation.
+template <int K>
+constexpr int select_threads() { return K >= 32 ? 256 : K >= 16 ? 512 : 1024; }  // registers per lane for wide lists
 
-// grid: batch * n_child rows.  Child row c = q * n_child + i is level entry
-// q * lvl_stride + i; its parent row is q * n_parent + (its parent slot).
-template <bool BF16>
-__global__ __launch_bounds__(256) void state_update(int n_child, int n_parent, int hidden, int lvl_stride,
-                                                    const int32_t* __restrict__ lvl_tok,
-                                                    const int32_t* __restrict__ lvl_par,
-                                                    const float* __restrict__ t, const void* __restrict__ U,
-                                                    float e, void* r_out) {
-  const int64_t c = blockIdx.x;
-  const int64_t q = c / n_child;
-  const int64_t li = q * lvl_stride + (c - q * n_child);
-  const int64_t prow = q * n_parent + lvl_par[li];
-  const int64_t tok = lvl_tok[li];
-  const float* tp = t + prow * hidden;
-  if constexpr (BF16) {
-    const uint16_t* up = static_cast<const uint16_t*>(U) + tok * hidden;
-    uint16_t* rp = static_cast<uint16_t*>(r_out) + c * hidden;
-    for (int i = threadIdx.x * 8; i < hidden; i += blockDim.x * 8) {
-      const f32x4 t0 = *reinterpret_cast<const f32x4*>(tp + i);
-      const f32x4 t1 = *reinterpret_cast<const f32x4*>(tp + i + 4);
-      typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
-      const u16x8 u = *reinterpret_cast<const u16x8*>(up + i);
-      u16x8 r;
+template <int K>
+__global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a, int S) {
+  __shared__ uint64_t keys[kSortMax];
+  __shared__ float c_logp[kSortMax];
+  __shared__ int32_t c_ids[kSortMax];
+  const int q = blockIdx.x / S, sl = blockIdx.x - q * S;
+  const int np = a.n_parent, k = a.k, n = np * k;
+  const int64_t rbase = int64_t(q) * np;
+  if (a.nseg > 1) {
+    constexpr int RF = record_floats<K>();
+    const float scale = kLog2e / a.tau;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nwaves = blockDim.x >> 6;
+    for (int j = wave; j < np; j += nwaves) {
+      uint64_t out[K];
+      const Partial p = wave_merge_records<K>(a.part + (rbase + j) * a.nseg * RF, a.nseg, k, scale, out);
+      const float log_s = logf(p.s);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        r[j] = f32_to_bf16(tanhf(t0[j] + e * bf16_to_f32(u[j])));
-        r[j + 4] = f32_to_bf16(tanhf(t1[j] + e * bf16_to_f32(u[j + 4])));
+      for (int r = 0; r < K; ++r) {
+        if (r < k && lane == r) {
+          const float lp = (key_value(out[r]) - p.m) / a.tau - log_s;
+          const int id = key_id(out[r]);
+          c_logp[j * k + r] = lp;
+          c_ids[j * k + r] = id;
+          if (sl == 0) {
+            a.cand_logp[(rbase + j) * k + r] = lp;
+            a.cand_ids[(rbase + j) * k + r] = id;
+          }
+        }
       }
-      *reinterpret_cast<u16x8*>(rp + i) = r;
+      if (sl == 0 && lane == 0) a.lse[rbase + j] = p.m / a.tau + log_s;
     }
   } else {
-    const float* up = static_cast<const float*>(U) + tok * hidden;
-    float* rp = static_cast<float*>(r_out) + c * hidden;
-    for (int i = threadIdx.x; i < hidden; i += blockDim.x) rp[i] = tanhf(tp[i] + e * up[i]);
+    for (int c = threadIdx.x; c < n; c += blockDim.x) {
+      c_logp[c] = a.cand_logp[rbase * k + c];
+      c_ids[c] = a.cand_ids[rbase * k + c];
+    }
+  }
+  __syncthreads();
+  auto key_of = [&](int c) {
+    const int j = c / k;
+    const float sp = a.parent_score ? a.parent_score[int64_t(q) * a.parent_stride + j] : 0.f;
+    const float sc = (sp + c_logp[c]) + a.beta;
+    return (uint64_t(score_desc_key(sc)) << 32) | (uint32_t(j) << 20) | uint32_t(c_ids[c]);
+  };
+  const uint64_t* kept = keys;   // the n_keep best, in order
+  if (n <= int(blockDim.x)) {
+    // few candidates: rank by counting (keys are distinct: (slot, token)
+    // pairs are), one barrier instead of a sorting network
+    uint64_t mine = ~0ull;
+    if (int(threadIdx.x) < n) mine = key_of(threadIdx.x);
+    keys[threadIdx.x] = mine;
+    __syncthreads();
+    int rank = 0;
+    if (int(threadIdx.x) < n)
+      for (int j = 0; j < n; ++j) rank += int(keys[j] < mine);
+    __syncthreads();
+    // n <= 1024 and n_keep <= n: the ranked copy sits above the keys
+    if (int(threadIdx.x) < n && rank < a.n_keep) keys[kSortMax / 2 + rank] = mine;
+    kept = keys + kSortMax / 2;
+    __syncthreads();
+  } else {
+    const int npad = next_pow2(n);
+    for (int c = threadIdx.x; c < npad; c += blockDim.x) keys[c] = c < n ? key_of(c) : ~0ull;
+    __syncthreads();
+    bitonic_sort(keys, npad);
+  }
+  if (sl == 0) {
+    for (int i = threadIdx.x; i < a.n_keep; i += blockDim.x) {
+      const uint64_t key = kept[i];
+      const uint32_t lo = uint32_t(key);
+      const int64_t o = int64_t(q) * a.out_stride + i;
+      a.out_tok[o] = int32_t(lo & 0xFFFFFu);
+      a.out_par[o] = int32_t(lo >> 20);
+      a.out_score[o] = score_from_desc_key(uint32_t(key >> 32));
+    }
+  }
+  if (!a.state) return;
+  const int h = a.hidden;
+  for (int i = sl; i < a.n_keep; i += S) {
+    const uint32_t lo = uint32_t(kept[i]);
+    const int64_t prow = rbase + (lo >> 20), tok = lo & 0xFFFFFu;
+    const int64_t c = int64_t(q) * a.n_keep + i;
+    const float* tp = a.t + prow * h;
+    if (a.precision == DARTREE_BF16) {
+      typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+      const uint16_t* up = static_cast<const uint16_t*>(a.U) + tok * h;
+      uint16_t* rp = static_cast<uint16_t*>(a.r_out) + c * h;
+      for (int x = threadIdx.x * 8; x < h; x += blockDim.x * 8) {
+        const f32x4 t0 = *reinterpret_cast<const f32x4*>(tp + x);
+        const f32x4 t1 = *reinterpret_cast<const f32x4*>(tp + x + 4);
+        const u16x8 u = *reinterpret_cast<const u16x8*>(up + x);
+        u16x8 r;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          r[j] = f32_to_bf16(tanhf(t0[j] + a.e * bf16_to_f32(u[j])));
+          r[j + 4] = f32_to_bf16(tanhf(t1[j] + a.e * bf16_to_f32(u[j + 4])));
+        }
+        *reinterpret_cast<u16x8*>(rp + x) = r;
+      }
+    } else {
+      const float* up = static_cast<const float*>(a.U) + tok * h;
+      float* rp = static_cast<float*>(a.r_out) + c * h;
+      for (int x = threadIdx.x; x < h; x += blockDim.x) rp[x] = tanhf(tp[x] + a.e * up[x]);
+    }
   }
 }
 
@@ -239,30 +294,19 @@ __global__ __launch_bounds__(1024) void prune_emit(LevelShape shape, int budget,
 
 }  // namespace
 
-hipError_t launch_select_topw(int batch, int n_parent, int k, int n_keep, float beta, int parent_stride,
-                              int out_stride, const float* parent_score, const float* cand_logp,
-                              const int32_t* cand_ids, int32_t* out_tok, int32_t* out_par, float* out_score,
-                              hipStream_t s) {
-  if (batch <= 0) return hipSuccess;
-  const int n = n_parent * k;
-  const int threads = n >= 1024 ? 1024 : (n >= 256 ? 256 : 64);
-  hipLaunchKernelGGL(select_topw, dim3(batch), dim3(threads), 0, s, n_parent, k, n_keep, beta, parent_stride,
-                     out_stride, parent_score,
-                     cand_logp, cand_ids, out_tok, out_par, out_score);
-  return hipGetLastError();
-}
-
-hipError_t launch_state_update(int precision, int batch, int n_child, int n_parent, int hidden, int lvl_stride,
-                               const int32_t* lvl_tok, const int32_t* lvl_par, const float* t, const void* U,
-                               float e, void* r_out, hipStream_t s) {
-  const unsigned rows = unsigned(batch) * unsigned(n_child);
-  if (rows == 0) return hipSuccess;
-  if (precision == DARTREE_BF16)
-    hipLaunchKernelGGL((state_update<true>), dim3(rows), dim3(256), 0, s, n_child, n_parent, hidden, lvl_stride, lvl_tok,
-                       lvl_par, t, U, e, r_out);
-  else
-    hipLaunchKernelGGL((state_update<false>), dim3(rows), dim3(256), 0, s, n_child, n_parent, hidden, lvl_stride, lvl_tok,
-                       lvl_par, t, U, e, r_out);
+hipError_t launch_select_level(const LevelArgs& a, hipStream_t s) {
+  if (a.batch <= 0) return hipSuccess;
+  // state slices: enough blocks to spread the state rows over the chip
+  const int S = a.state ? std::max(1, std::min(a.n_keep, (256 + a.batch - 1) / a.batch)) : 1;
+  const dim3 grid(unsigned(a.batch) * unsigned(S));
+  switch (topk_bucket(a.k)) {
+    case 1: hipLaunchKernelGGL((select_level<1>), grid, dim3(select_threads<1>()), 0, s, a, S); break;
+    case 2: hipLaunchKernelGGL((select_level<2>), grid, dim3(select_threads<2>()), 0, s, a, S); break;
+    case 4: hipLaunchKernelGGL((select_level<4>), grid, dim3(select_threads<4>()), 0, s, a, S); break;
+    case 8: hipLaunchKernelGGL((select_level<8>), grid, dim3(select_threads<8>()), 0, s, a, S); break;
+    case 16: hipLaunchKernelGGL((select_level<16>), grid, dim3(select_threads<16>()), 0, s, a, S); break;
+    default: hipLaunchKernelGGL((select_level<32>), grid, dim3(select_threads<32>()), 0, s, a, S); break;
+  }
   return hipGetLastError();
 }
 

@@ -270,7 +270,7 @@ def build_tree(p: Params, inputs: DeviceInputs, ws, out: DeviceTree, stream=None
                                     ctypes.byref(tc), _stream(stream)), "dartree_build_tree")
 
 
-KERNEL_NAMES = ["head", "logits", "lse_topk", "topw", "state"]   # per depth, launch order
+KERNEL_NAMES = ["head", "logits", "lse_topk", "select"]   # per depth, launch order
 
 
 def build_tree_timed(p: Params, inputs: DeviceInputs, ws, out: DeviceTree, events, stream=None) -> None:

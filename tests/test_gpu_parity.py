@@ -39,6 +39,8 @@ SMALL = {
     "bf16-k1": small(branch=1, budget=8, seed=37),
     "bf16-prune-all": small(budget=4096, seed=38),
     "bf16-B1": small(budget=1, seed=39),
+    "bf16-k12": small(branch=12, width=20, budget=50, seed=47),       # top-k bucket 16, row segments merged
+    "bf16-k20": small(branch=20, width=24, budget=70, seed=48),       # top-k bucket 32
     "fp32-small": small(precision=W.FP32, hidden=48, sigma_w=0.1, seed=40),
     "fp32-tiny-vocab": small(precision=W.FP32, vocab=7, hidden=5, branch=3, width=5, budget=12, seed=41),
 }
