@@ -39,6 +39,27 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch from the committed counter summary of this
+    workload and kernel, or None if there is none or the kernel's source has
+    changed since the counters were taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\s*(\{.*?\})\s*```", open(path).read(), re.S)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("kernel") != kernel:
+        return None
+    src = os.path.join(ROOT, rec["source"])
+    if not os.path.exists(src) or hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+        return None
+    return float(rec["traffic_bytes_per_launch"])
+
+
 def kernel_work(cfg, kind: str, d: int):
     """Algorithmic (bytes, flops) of one launch at depth d.
 
@@ -234,7 +255,7 @@ def main() -> int:
     else:
         roof = {"bound": "hbm", "achieved": bytes_round / t_round / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(cfg.name, dom)
     roof["kernel"] = dom
     roof["algorithmic_bytes_per_launch"] = bytes_round / launches
     roof["algorithmic_flops_per_launch"] = flops_round / launches
