@@ -11,7 +11,8 @@
 //    every weight element is read once from HBM with coalesced non-temporal
 //    loads and staged through LDS into MFMA operand layout.
 //  * proj_bf16_big: many rows (>= 512) against the vocabulary.  256x256 tiles,
-//    buffer loads straight to swizzled LDS, XCD-aware tile order.
+//    8 waves in two groups alternating LDS reads and MFMAs, buffer loads
+//    straight to swizzled LDS, XCD-aware tile order.
 //  * proj_bf16_tiled: other many-row products (the head, or a few hundred
 //    rows).  128x128 output tiles, 64-deep K steps staged through
 //    double-buffered, padded LDS tiles shared by 4 waves (64x64 each).
@@ -300,116 +301,152 @@ __global__ __launch_bounds__(256) void proj_bf16_tiled(KArgs a) {
 
 // ---------------------------------------------------------------------------
 // Many rows, long weight matrix (>= 512 node rows): 256x256 output tile per
-// block, 4 waves of 128x128 (64 MFMA accumulators each, held in AGPRs).
-// Both operand tiles move 64-k slices with buffer loads straight into LDS
-// (no VGPR staging; rows past the matrix read as zero through the buffer
-// resource's range), XOR-swizzled by row so that the MFMA-layout reads are
-// bank-conflict free, double-buffered over K.  Tiles are ordered so that
-// consecutive blocks on one XCD (blocks are dealt to the 8 XCDs round-robin)
-// cover the M-tiles of one weight tile, which then stays in that XCD's L2.
+// block, 8 waves, two per SIMD.  Wave w belongs to group w / 4 (each SIMD runs
+// one wave of each group) and owns weight rows [64 (w % 4), +64) x node rows
+// [128 (w / 4), +128) of the tile (32 MFMA accumulators).  The groups
+// alternate between a memory phase (reading the operand fragments of one
+// 64-deep K step from LDS) and a compute phase (the 64 MFMAs of that step),
+// one phase apart, so each SIMD always has one wave issuing MFMAs; a barrier
+// ends every phase.  Group 0 moves the K steps into double-buffered LDS with
+// buffer loads straight to LDS (XOR-swizzled rows: conflict-free for the
+// MFMA-layout reads): step s + 1 at the start of its memory phase for step s,
+// into the buffer of step s - 1, which both groups have finished reading.
+// Every wave executes the same number of barriers (2 nk + 2).  The ragged
+// last tile along M or N is shifted back to end at the matrix edge, so every
+// loaded row exists; that block stores only the rows the previous tile did
+// not cover.  Tiles are ordered so that the blocks of one XCD (blocks are
+// dealt to the 8 XCDs round-robin) cover the M-tiles of one weight tile,
+// which then stays in that XCD's L2.
 // ---------------------------------------------------------------------------
 constexpr int GBM = 256, GBN = 256, GBK = 64;
 #define LDS_AS __attribute__((address_space(3)))
 
 __device__ __forceinline__ int swz16(int r) { return (r ^ (r >> 3)) & 7; }  // r in 0..15
 
-__global__ __launch_bounds__(256) void proj_bf16_big(KArgs a, int vec) {
+__global__ __launch_bounds__(512) void proj_bf16_big(KArgs a, int vec) {
   __shared__ __attribute__((aligned(16))) uint16_t smem[2][(GBN + GBM) * GBK];  // [buf][W rows | X rows]
   const int lane = threadIdx.x & 63, r16 = lane & 15, kg = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int grp = wave >> 2, q = wave & 3;
   const int M = a.M, N = a.N, K = a.K;
   const int ntm = (M + GBM - 1) / GBM, ntn = (N + GBN - 1) / GBN, T = ntm * ntn;
   int t = blockIdx.x;
   const int q8 = T / 8;
   if (t < 8 * q8) t = (t % 8) * q8 + t / 8;
   const int n0 = (t / ntm) * GBN, m0 = (t % ntm) * GBM;
-  const int wm = wave & 1, wn = wave >> 1;
+  const int nl = min(n0, N - GBN), ml = min(m0, M - GBM);  // loaded tile origin (M, N >= 256)
   const uint16_t* X = static_cast<const uint16_t*>(a.x);
   const uint16_t* Wt = static_cast<const uint16_t*>(a.w);
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(Wt + int64_t(n0) * K), (short)0, min(GBN, N - n0) * K * 2, 0x00020000);
+      const_cast<uint16_t*>(Wt + int64_t(nl) * K), (short)0, GBN * K * 2, 0x00020000);
   const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(X + int64_t(m0) * K), (short)0, min(GBM, M - m0) * K * 2, 0x00020000);
-  // load i of wave w moves rows 64 w + 8 i + lane / 8; LDS chunk lane % 8 holds
-  // global chunk (lane % 8) ^ swizzle(row).  The row offset is part of the
-  // per-lane offset, which the buffer range check covers (rows past the
-  // matrix read as zero); the scalar offset carries only the k position.
+      const_cast<uint16_t*>(X + int64_t(ml) * K), (short)0, GBM * K * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs = q < 2 ? rw : rx;
+  // group 0 wave q moves stage rows [128 q, +128) (weight rows for q < 2, node
+  // rows otherwise), 8 rows per load: lane / 8 is the row, LDS chunk lane % 8
+  // holds global chunk (lane % 8) ^ swizzle(row)
   const int lrow = lane >> 3, lcp = lane & 7;
-  const unsigned vrow = unsigned((64 * wave + lrow) * K * 2);
-  const unsigned vc0 = unsigned((lcp ^ swz16(lrow)) * 16), vc1 = unsigned((lcp ^ swz16(8 + lrow)) * 16);
-  const int ax0 = (wn * 128 + r16) * GBK + ((kg ^ swz16(r16)) * 8);
-  const int ax1 = (wn * 128 + r16) * GBK + (((4 + kg) ^ swz16(r16)) * 8);
-  const int bx0 = GBN * GBK + (wm * 128 + r16) * GBK + ((kg ^ swz16(r16)) * 8);
-  const int bx1 = GBN * GBK + (wm * 128 + r16) * GBK + (((4 + kg) ^ swz16(r16)) * 8);
+  const unsigned vo0 = unsigned(lrow * K * 2 + ((lcp ^ swz16(lrow)) * 16));
+  const unsigned vo1 = unsigned(lrow * K * 2 + ((lcp ^ swz16(8 + lrow)) * 16));
+  const int sw = swz16(r16);
+  const int nk = K / GBK;
 
-  f32x4 acc[8][8];
+  f32x4 acc[4][8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto load = [&](int buf, int kt) {
-    LDS_AS uint16_t* base = (LDS_AS uint16_t*)smem[buf];  // generic -> LDS address space
-    const unsigned so = unsigned(kt * GBK * 2);
+  auto dma = [&](int buf, int kt) {
+    LDS_AS uint16_t* base = (LDS_AS uint16_t*)smem[buf] + 128 * q * GBK;  // generic -> LDS address space
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const unsigned vo = vrow + unsigned(8 * i * K * 2) + ((i & 1) ? vc1 : vc0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (LDS_AS void*)(base + (64 * wave + 8 * i) * GBK), 16, vo, so, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS_AS void*)(base + GBN * GBK + (64 * wave + 8 * i) * GBK), 16, vo,
-                                               so, 0, 0);
+    for (int i = 0; i < 16; ++i) {
+      const unsigned so = unsigned((128 * (q & 1) + 8 * i) * K * 2 + kt * GBK * 2);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (LDS_AS void*)(base + 8 * i * GBK), 16, (i & 1) ? vo1 : vo0, so, 0,
+                                               0);
     }
   };
-  auto rd = [&](const LDS_AS uint16_t* S, int off) {
-    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const LDS_AS u32x4*>(S + off));
-  };
-  auto block = [&](const bf16x8 (&av)[8], const bf16x8 (&bv)[4], int h) {
+  bf16x8 A[2][4], B[2][8];
+  auto fetch = [&](int buf) {
+    const LDS_AS uint16_t* S = (const LDS_AS uint16_t*)smem[buf];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int h = 0; h < 2; ++h) {
+      const int c = ((4 * h + kg) ^ sw) * 8;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][4 * h + j] = mfma16(av[i], bv[j], acc[i][4 * h + j]);
+      for (int i = 0; i < 4; ++i)
+        A[h][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const LDS_AS u32x4*>(S + (64 * q + 16 * i + r16) * GBK + c));
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        B[h][j] = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const LDS_AS u32x4*>(S + GBN * GBK + (128 * grp + 16 * j + r16) * GBK + c));
+    }
   };
+  auto compute = [&]() {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[i][j] = mfma16(A[h][i], B[h][j], acc[i][j]);
+  };
+  // A bare barrier: the workgroup fence of __syncthreads would also wait for
+  // the loads still in flight for the next step.  The waits that the data
+  // dependencies need are explicit.
+  auto barrier = [] { asm volatile("s_barrier" ::: "memory"); };
+  auto wait_lds_reads = [] { __builtin_amdgcn_s_waitcnt(0xC07F); };  // lgkmcnt(0)
+  auto wait_loads = [] { __builtin_amdgcn_s_waitcnt(0x0F70); };      // vmcnt(0)
 
-  const int nk = K / GBK;
-  load(0, 0);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's share of tile kt has landed
-    __syncthreads();                // ... every wave's; buffer cur ^ 1 is no longer read
-    const LDS_AS uint16_t* S = (const LDS_AS uint16_t*)smem[cur];
-    bf16x8 A0[8], A1[8], B00[4], B01[4], B10[4], B11[4];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) A0[i] = rd(S, ax0 + i * 16 * GBK);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) B00[j] = rd(S, bx0 + j * 16 * GBK);
-    if (kt + 1 < nk) load(cur ^ 1, kt + 1);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) B01[j] = rd(S, bx0 + (4 + j) * 16 * GBK);
-    // operand reads for the next quarter are issued ahead of each MFMA group
-    __builtin_amdgcn_sched_barrier(0);
-    block(A0, B00, 0);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) A1[i] = rd(S, ax1 + i * 16 * GBK);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) B10[j] = rd(S, bx1 + j * 16 * GBK);
-    __builtin_amdgcn_sched_barrier(0);
-    block(A0, B01, 1);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) B11[j] = rd(S, bx1 + (4 + j) * 16 * GBK);
-    __builtin_amdgcn_sched_barrier(0);
-    block(A1, B10, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    block(A1, B11, 1);
+  if (grp == 0) {
+    dma(0, 0);
+    if (nk > 1) {
+      dma(1, 1);
+      __builtin_amdgcn_s_waitcnt(0x4F70);  // vmcnt(16): step 0 landed, step 1 in flight
+    } else {
+      wait_loads();
+    }
+  }
+  barrier();  // step 0 in LDS
+  if (grp == 0) {
+    for (int st = 0; st < nk; ++st) {
+      if (st >= 1 && st + 1 < nk) dma((st + 1) & 1, st + 1);
+      fetch(st & 1);
+      wait_lds_reads();
+      barrier();  // end of phase 2 st
+      __builtin_amdgcn_sched_barrier(0);
+      compute();
+      __builtin_amdgcn_sched_barrier(0);
+      if (st + 1 < nk) wait_loads();  // this wave's share of step st + 1 landed
+      barrier();                      // end of phase 2 st + 1
+    }
+    barrier();  // phase 2 nk: group 1 multiplies the last step
+  } else {
+    barrier();  // phase 0: group 0 reads step 0
+    for (int st = 0; st < nk; ++st) {
+      fetch(st & 1);
+      wait_lds_reads();
+      barrier();  // end of phase 2 st + 1
+      __builtin_amdgcn_sched_barrier(0);
+      compute();
+      __builtin_amdgcn_sched_barrier(0);
+      barrier();  // end of phase 2 st + 2
+    }
   }
 
-  // lane holds D[n = 4 kg + q][m = r16] of each 16x16 sub-tile
+  // lane holds D[n = 4 kg + e][m = r16] of each 16x16 sub-tile
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const int m = m0 + wm * 128 + j * 16 + r16;
-      if (m < M) emit4<EPI_LOGITS>(a, m, n0 + wn * 128 + i * 16 + kg * 4, acc[i][j], vec != 0);
+      const int m = ml + 128 * grp + 16 * j + r16;
+      const int n = nl + 64 * q + 16 * i + 4 * kg;
+      if (m < m0) continue;
+      if (n >= n0) {
+        emit4<EPI_LOGITS>(a, m, n, acc[i][j], vec != 0);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (n + e >= n0) emit<EPI_LOGITS, true>(a, m, n + e, acc[i][j][e]);
+      }
     }
 }
 
@@ -490,7 +527,7 @@ hipError_t launch_project(const ProjArgs& p, hipStream_t s) {
   if (k.M <= 64) return launch_stream_nt<4>(k, p.epilogue, s);
   if (p.epilogue == EPI_LOGITS && k.M >= 2 * GBM && k.N >= 64 * GBN) {
     const int tiles = ((k.M + GBM - 1) / GBM) * ((k.N + GBN - 1) / GBN);
-    hipLaunchKernelGGL(proj_bf16_big, dim3(tiles), dim3(256), 0, s, k, int(epilogue_vec_ok(k, EPI_LOGITS)));
+    hipLaunchKernelGGL(proj_bf16_big, dim3(tiles), dim3(512), 0, s, k, int(epilogue_vec_ok(k, EPI_LOGITS)));
     return hipGetLastError();
   }
   const dim3 grid((k.M + TBM - 1) / TBM, (k.N + TBN - 1) / TBN);
