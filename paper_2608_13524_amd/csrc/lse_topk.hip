@@ -72,7 +72,6 @@ __device__ __forceinline__ void emit_row(int64_t row, Partial p, uint64_t key, i
   cand_ids[row * k + slot] = key_id(key);
 }
 
-constexpr int kChunk = 4;  // float4 loads in flight per thread
 
 // Fold the nseg records of one row into each thread's (Partial, top-K):
 // threads take single candidates, which keeps this tail small in registers.
@@ -94,13 +93,16 @@ __device__ void fold_records(const float* recs, int nseg, int k, float scale, Pa
 // grid: rows * nseg blocks, block = row * nseg + segment.  One segment per
 // row writes the result directly; otherwise every block writes its segment's
 // record for lse_topk_merge.
-template <int K, bool VEC>
+// CH float4 loads in flight per thread (at most 8: the candidate bitmask has
+// 32 bits); NTL: non-temporal loads (many rows: z is far larger than the caches).
+template <int K, bool VEC, int CH, bool NTL>
 __global__ __launch_bounds__(kBlock) void lse_topk_rows(const float* __restrict__ z, int vocab,
                                                         int nseg, int seg_len, int k, float tau,
                                                         float* lse, float* cand_logp,
                                                         int32_t* cand_ids, float* part) {
+  static_assert(CH >= 1 && CH <= 8, "bitmask holds 32 candidates");
   // per-thread staging row for the (rare) chunks that reach the top-K list
-  __shared__ float stage[kBlock][4 * kChunk + 1];
+  __shared__ float stage[kBlock][4 * CH + 1];
   const int64_t row = blockIdx.x / nseg;
   const int seg = blockIdx.x % nseg;
   const int v0 = seg * seg_len;
@@ -119,23 +121,24 @@ __global__ __launch_bounds__(kBlock) void lse_topk_rows(const float* __restrict_
     // Thread tid visits, per iteration, float4 c at base + 4 kBlock c: ids
     // ascend along the traversal.  The first float4 of an iteration is always
     // in range, so the running max is finite before any -inf padding is summed.
-    for (int base = v0 + 4 * tid; base < v1; base += 4 * kBlock * kChunk) {
-      f32x4 x[kChunk];
+    for (int base = v0 + 4 * tid; base < v1; base += 4 * kBlock * CH) {
+      f32x4 x[CH];
 #pragma unroll
-      for (int c = 0; c < kChunk; ++c) {
+      for (int c = 0; c < CH; ++c) {
         const int v = base + 4 * kBlock * c;
-        x[c] = v < v1 ? *reinterpret_cast<const f32x4*>(zr + v) : f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        const f32x4* src = reinterpret_cast<const f32x4*>(zr + v);
+        x[c] = v < v1 ? (NTL ? __builtin_nontemporal_load(src) : *src) : f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
       }
       float mx = -INFINITY;
 #pragma unroll
-      for (int c = 0; c < kChunk; ++c) mx = fmaxf(mx, fmaxf(fmaxf(x[c][0], x[c][1]), fmaxf(x[c][2], x[c][3])));
+      for (int c = 0; c < CH; ++c) mx = fmaxf(mx, fmaxf(fmaxf(x[c][0], x[c][1]), fmaxf(x[c][2], x[c][3])));
       if (mx > p.m) {
         p.s *= __builtin_amdgcn_exp2f((p.m - mx) * scale);
         p.m = mx;
       }
       float acc = 0.f;
 #pragma unroll
-      for (int c = 0; c < kChunk; ++c)
+      for (int c = 0; c < CH; ++c)
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc += __builtin_amdgcn_exp2f((x[c][i] - p.m) * scale);
       p.s += acc;
@@ -144,7 +147,7 @@ __global__ __launch_bounds__(kBlock) void lse_topk_rows(const float* __restrict_
         const float thr = tv[K - 1];
         uint32_t mask = 0;
 #pragma unroll
-        for (int c = 0; c < kChunk; ++c)
+        for (int c = 0; c < CH; ++c)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             stage[tid][4 * c + i] = x[c][i];
@@ -221,12 +224,15 @@ hipError_t launch_k(const float* z, int64_t rows, int64_t vocab, int k, float ta
   int seg_len = int((vocab + nseg - 1) / nseg);
   if (vec) seg_len = (seg_len + 3) & ~3;
   const dim3 grid(unsigned(rows * nseg));
-  if (vec)
-    hipLaunchKernelGGL((lse_topk_rows<K, true>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k, tau,
-                       lse, cand_logp, cand_ids, part);
+  if (vec && rows >= 512)  // z (R V floats) far exceeds the caches: stream it, 8 float4 per thread in flight
+    hipLaunchKernelGGL((lse_topk_rows<K, true, 8, true>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
+                       tau, lse, cand_logp, cand_ids, part);
+  else if (vec)
+    hipLaunchKernelGGL((lse_topk_rows<K, true, 4, false>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
+                       tau, lse, cand_logp, cand_ids, part);
   else
-    hipLaunchKernelGGL((lse_topk_rows<K, false>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k, tau,
-                       lse, cand_logp, cand_ids, part);
+    hipLaunchKernelGGL((lse_topk_rows<K, false, 4, false>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
+                       tau, lse, cand_logp, cand_ids, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || nseg == 1 || !merge) return e;
   hipLaunchKernelGGL((lse_topk_merge<K>), dim3(unsigned(rows)), dim3(kBlock), 0, s, nseg, k, tau, part, lse,
