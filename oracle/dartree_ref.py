@@ -19,6 +19,13 @@ eq. (5) and Lemma 1), for each request independently:
       S_d = first n_d candidates by (s desc, j asc, v asc)        (global top-W)
       r_child = rnd(tanh(t_j + e * U[v])), e = fp32(sqrt(h))      (state update)
   T = first min(B, |S|) nodes of S by (s desc, depth asc, slot asc)   (top-B, Lemma 1)
+
+With a shared candidate set (``candidates`` = K > 0; Alg. 1 as printed, the
+paper's default K = 64 of Sec. 4.1): C_d = TopK(L_d^base, K) by (value desc,
+id asc) for each request and depth, the head scores only C_d
+(z_j[v] = L_d^base[v] + U[v] a_j for v in C_d) and q~_d is normalised over
+C_d, i.e. the tokens outside C_d take z = -inf; the rest is unchanged (the
+per-parent cap k <= K, k = K keeping every token of C_d as in Alg. 1).
   emit T in canonical breadth-first order with parent indices and the
   ancestor-or-self tree-attention mask (Sec. 2.3 "Tree Verification").
 
@@ -26,7 +33,10 @@ Readings where the paper is silent (each is listed in the design doc):
   * the head form g and the state update (Alg. 1 gives only g(H_d, r(u_<d)) and
     "r(u_1:d) from r(u_<d) and u_d"): the Elman residual head above;
   * the candidate set is the per-parent top-k of the full-vocabulary corrected
-    logits (the "Full" vocabulary variant of Appendix D) with branching cap k;
+    logits (the "Full" vocabulary variant of Appendix D) with branching cap k,
+    or, with ``candidates`` = K, the shared C_d above with q~ normalised over
+    C_d (Alg. 1 writes q~_d(C_d | u_<d) = g_{C_d}(...) without stating the
+    normaliser; normalising over C_d keeps log q~ <= 0, which Lemma 1 needs);
   * tau = T for T > 0 and tau = 1 at T = 0 (q_T is defined for T > 0 only);
   * rounding points: with bf16 inputs, a and r are rounded to bf16 (through
     fp32, nearest-even) because they are operands of bf16 matrix products;
@@ -72,12 +82,13 @@ class Params:
     temperature: float
     depth_bonus: float
     precision: int
+    candidates: int = 0   # K of a shared C_d = TopK(L_d^base, K); 0 = the full vocabulary
 
     @staticmethod
     def of(cfg) -> "Params":
         return Params(cfg.batch, cfg.vocab, cfg.hidden, cfg.depth, cfg.width,
                       cfg.branch, cfg.budget, float(cfg.temperature),
-                      float(cfg.depth_bonus), int(cfg.precision))
+                      float(cfg.depth_bonus), int(cfg.precision), int(getattr(cfg, "candidates", 0)))
 
     @property
     def tau(self) -> float:
@@ -155,6 +166,21 @@ def vocab_logits(a: np.ndarray, U: np.ndarray, Lb_d: np.ndarray, chunk: int = 16
     return z
 
 
+def candidate_set(Lb_d: np.ndarray, K: int) -> np.ndarray:
+    """C_d = TopK(L_d^base, K) (Alg. 1): the K ids of the drafter's base logits
+    at position d, ordered by (value desc, id asc)."""
+    return topk_ids(Lb_d, K)
+
+
+def candidate_logits(a: np.ndarray, U: np.ndarray, Lb_d: np.ndarray, cset: np.ndarray) -> np.ndarray:
+    """Corrected logits on a shared candidate set (Alg. 1, g over C_d):
+    z_j[v] = L_d^base[v] + U[v] a_j for v in C_d and -inf elsewhere ([R][V]),
+    so that a softmax over the row is normalised over C_d."""
+    z = np.full((a.shape[0], U.shape[0]), -np.inf)
+    z[:, cset] = Lb_d[None, cset] + a @ U[cset].T
+    return z
+
+
 def log_softmax(z: np.ndarray, tau: float) -> np.ndarray:
     """log q_T: (z - m)/tau - log sum_v exp((z_v - m)/tau), row-wise."""
     m = z.max(axis=-1, keepdims=True)
@@ -204,6 +230,7 @@ class Level:
     cand_ids: Optional[np.ndarray] = None   # [n_{d-1}][k] top-k ids of each parent
     cand_logp: Optional[np.ndarray] = None  # [n_{d-1}][k] their log q~
     logp: Optional[np.ndarray] = None       # [n_{d-1}][V] full log q~ (kept on demand)
+    cset: Optional[np.ndarray] = None       # [K] shared candidate set C_d (candidates > 0)
 
 
 @dataclasses.dataclass
@@ -244,7 +271,12 @@ def build_supertree(dec: Decoded, requests=None, choose: Optional[Chooser] = Non
         levels = []
         for d in range(1, p.depth + 1):
             t, a = head_features(r, dec.A, dec.H[b, d - 1], p.precision)
-            z = vocab_logits(a, dec.U, dec.Lb[b, d - 1])
+            cset = None
+            if p.candidates > 0:
+                cset = candidate_set(dec.Lb[b, d - 1], p.candidates)
+                z = candidate_logits(a, dec.U, dec.Lb[b, d - 1], cset)
+            else:
+                z = vocab_logits(a, dec.U, dec.Lb[b, d - 1])
             lp = log_softmax(z, tau)
             m = z.max(axis=1)
             lse = m / tau + np.log(np.exp((z - m[:, None]) / tau).sum(axis=1))
@@ -259,7 +291,7 @@ def build_supertree(dec: Decoded, requests=None, choose: Optional[Chooser] = Non
             sc = path_score(s[par], clp.reshape(-1), beta)
             keep = choose(b, d, par, tok, sc, sizes[d - 1], None)
             lvl = Level(token=tok[keep], parent=par[keep], score=sc[keep], lse=lse,
-                        cand_ids=cids, cand_logp=clp, logp=lp if keep_logp else None)
+                        cand_ids=cids, cand_logp=clp, logp=lp if keep_logp else None, cset=cset)
             levels.append(lvl)
             r = child_states(t[lvl.parent], dec.U[lvl.token], e, p.precision)
             if adopt_states is not None and d < p.depth:

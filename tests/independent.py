@@ -72,6 +72,21 @@ class ScalarHead:
     def child(self, t, v):
         return [self._rnd(math.tanh(t[i] + self.e * self.U[v][i])) for i in range(self.h)]
 
+    def step_over(self, b, d, r, cset):
+        """As ``step`` with the head scoring only the tokens of ``cset`` and
+        q~ normalised over them: returns (t, {v: z_v}, {v: log q~_v})."""
+        h = self.h
+        t = [math.fsum(self.A[i][k] * r[k] for k in range(h)) for i in range(h)]
+        a = [self._rnd(math.tanh(t[i] + self.H[b][d - 1][i])) for i in range(h)]
+        z = {v: self.Lb[b][d - 1][v] + math.fsum(self.U[v][i] * a[i] for i in range(h)) for v in cset}
+        m = max(z.values())
+        lse = math.log(math.fsum(math.exp((zv - m) / self.tau) for zv in z.values()))
+        return t, z, {v: (zv - m) / self.tau - lse for v, zv in z.items()}
+
+    def cset(self, b, d, K):
+        """C_d = TopK(L_d^base, K) by a full sort of the drafter's base logits."""
+        return _ranked(self.Lb[b][d - 1], K)
+
 
 def _ranked(z, k):
     """Ids of the k best entries by (z desc, id asc), via a full sort."""
@@ -142,22 +157,71 @@ def brute_force(head: ScalarHead, b, budget, beta):
     return {p: scored[p] for p in best}
 
 
-def marginal_top_b(Lb, tau, L, budget, beta):
+def brute_force_shared(head: ScalarHead, b, budget, beta, K):
+    """Shared candidate sets: every prefix whose token at depth d lies in
+    C_d = TopK(L_d^base, K), scored along its own path with q~ normalised over
+    C_d; global top-B by (score desc, depth asc, path asc)."""
+    L = head.cfg.depth
+    scored = {}
+    frontier = [((), head.r0[b], 0.0)]
+    for d in range(1, L + 1):
+        cset = head.cset(b, d, K)
+        nxt = []
+        for path, state, score in frontier:
+            t, z, logp = head.step_over(b, d, state, cset)
+            for v in cset:
+                s = (score + logp[v]) + beta
+                scored[path + (v,)] = s
+                nxt.append((path + (v,), head.child(t, v), s))
+        frontier = nxt
+    best = sorted(scored, key=lambda p: (-scored[p], len(p), p))[:budget]
+    return {p: scored[p] for p in best}
+
+
+def sequential_heap_shared(head: ScalarHead, b, budget, branch, beta, K):
+    """Node-at-a-time construction over shared candidate sets: each pop runs
+    the head on the popped prefix over C_d and pushes its k best children."""
+    L = head.cfg.depth
+    heap = []
+
+    def expand(path, state, score):
+        d = len(path) + 1
+        cset = head.cset(b, d, K)
+        t, z, logp = head.step_over(b, d, state, cset)
+        best = [v for _, v in sorted((-z[v], v) for v in cset)][:branch]
+        for v in best:
+            heapq.heappush(heap, (-((score + logp[v]) + beta), d, path + (v,), t))
+
+    expand((), head.r0[b], 0.0)
+    out = {}
+    while heap and len(out) < budget:
+        negs, d, path, t_parent = heapq.heappop(heap)
+        out[path] = -negs
+        if d < L:
+            expand(path, head.child(t_parent, path[-1]), -negs)
+    return out
+
+
+def marginal_top_b(Lb, tau, L, budget, beta, K=None):
     """Zeroed correction: s(u) = sum_i log q_i(u_i) + beta*d with the drafter's
-    marginals q_i = softmax(Lb_i / tau); top-B prefixes by brute force."""
+    marginals q_i = softmax(Lb_i / tau); top-B prefixes by brute force.  With
+    K, tokens at position i range over TopK(Lb_i, K) and q_i is the softmax
+    restricted to those K tokens (a shared candidate set)."""
     Lb = np.asarray(Lb, np.float64)
     V = Lb.shape[1]
-    logq = []
+    logq, allowed = [], []
     for d in range(L):
-        m = max(Lb[d])
-        lse = math.log(math.fsum(math.exp((x - m) / tau) for x in Lb[d]))
-        logq.append([(x - m) / tau - lse for x in Lb[d]])
+        ids = list(range(V)) if K is None else _ranked(Lb[d].tolist(), K)
+        m = max(Lb[d][v] for v in ids)
+        lse = math.log(math.fsum(math.exp((Lb[d][v] - m) / tau) for v in ids))
+        logq.append({v: (Lb[d][v] - m) / tau - lse for v in ids})
+        allowed.append(ids)
     scored = {}
     frontier = [((), 0.0)]
     for d in range(L):
         nxt = []
         for path, score in frontier:
-            for v in range(V):
+            for v in allowed[d]:
                 s = (score + logq[d][v]) + beta
                 scored[path + (v,)] = s
                 nxt.append((path + (v,), s))

@@ -271,7 +271,68 @@ def pin_prune_ties_prefer_ancestors():
             assert all(d == 1 or (d - 1, int(levels[d - 1].parent[sl])) in ks for d, sl in kept)
 
 
+# ---------------------------------------------------------------------------
+# Shared candidate sets C_d = TopK(L_d^base, K) (Alg. 1 as printed)
+# ---------------------------------------------------------------------------
+def pin_shared_brute_force():
+    """K < V, k = K, W without truncation: the tree is the global top-B over
+    every prefix drawn from C_1 x ... x C_L, each scored along its own path
+    with q~ normalised over C_d (scalar loops, sets by a full sort)."""
+    for seed, prec, T in ((30, W.FP32, 0.0), (31, W.BF16, 0.0), (32, W.FP32, 0.7)):
+        cfg = tiny(seed=seed, precision=prec, vocab=7, depth=3, width=64, branch=3, candidates=3,
+                   budget=10, temperature=T)
+        inp, tree, st = run_oracle(cfg)
+        want = I.brute_force_shared(I.ScalarHead(inp, cfg), 0, cfg.budget, cfg.depth_bonus, cfg.candidates)
+        _check_against_paths(tree, 0, want, cfg.budget)
+
+
+def pin_shared_sequential_heap():
+    """W >= B, per-parent cap k < K: the tree equals node-at-a-time correction
+    over the shared sets with a best-first heap (Sec. 3.1 over C_d)."""
+    for seed, prec in ((33, W.FP32), (34, W.BF16)):
+        cfg = tiny(seed=seed, precision=prec, vocab=9, depth=4, width=8, branch=2, candidates=4, budget=8)
+        inp, tree, st = run_oracle(cfg)
+        want = I.sequential_heap_shared(I.ScalarHead(inp, cfg), 0, cfg.budget, cfg.branch, cfg.depth_bonus,
+                                        cfg.candidates)
+        _check_against_paths(tree, 0, want, cfg.budget)
+
+
+def pin_shared_zeroed_correction():
+    """U = 0 with shared sets: the tree is the top-B by factorised mass of the
+    drafter marginals restricted to (and renormalised over) TopK(L_d^base, K)."""
+    for T in (0.0, 0.7):
+        cfg = tiny(seed=35, vocab=6, depth=3, width=64, branch=3, candidates=3, budget=9, temperature=T)
+        inp = W.make_inputs(cfg)
+        inp.U[:] = 0
+        inp, tree, st = run_oracle(cfg, inp)
+        want, logq = I.marginal_top_b(inp.Lb[0], T or 1.0, cfg.depth, cfg.budget, cfg.depth_bonus,
+                                      K=cfg.candidates)
+        _check_against_paths(tree, 0, want, cfg.budget)
+
+
+def pin_shared_full_vocabulary():
+    """K = V: the shared set is the whole vocabulary and the tree equals the
+    full-vocabulary construction; every level's sets are TopK(L_d^base, K)."""
+    cfg = tiny(seed=36, vocab=8, depth=3, width=5, branch=3, budget=9)
+    inp, tree, st = run_oracle(cfg)
+    cfg2 = cfg.replace(candidates=cfg.vocab)
+    inp2 = W.Inputs(cfg=cfg2, Lb=inp.Lb, H=inp.H, r0=inp.r0, A=inp.A, U=inp.U)
+    _, tree2, st2 = run_oracle(cfg2, inp2)
+    for f in ("tokens", "parents", "depths", "mask", "num_nodes"):
+        assert np.array_equal(getattr(tree, f), getattr(tree2, f)), f
+    assert np.allclose(tree.scores, tree2.scores, atol=1e-12, equal_nan=True)
+    cfg3 = cfg.replace(candidates=4, branch=2)
+    inp3 = W.Inputs(cfg=cfg3, Lb=inp.Lb, H=inp.H, r0=inp.r0, A=inp.A, U=inp.U)
+    _, tree3, st3 = run_oracle(cfg3, inp3)
+    head = I.ScalarHead(inp3, cfg3)
+    for d, lvl in enumerate(st3.levels[0], start=1):
+        assert list(lvl.cset) == head.cset(0, d, 4)
+        assert set(lvl.token.tolist()) <= set(lvl.cset.tolist())
+
+
 PINS = [
+    pin_shared_brute_force, pin_shared_sequential_heap, pin_shared_zeroed_correction,
+    pin_shared_full_vocabulary,
     pin_log_softmax_library, pin_topk_sorted, pin_select_sorted, pin_bf16_rounding,
     pin_head_scalar, pin_prune_is_heap, pin_prune_ties_prefer_ancestors, pin_brute_force, pin_sequential_heap,
     pin_zeroed_correction, pin_greedy_chain, pin_whole_supertree, pin_monotone_scores,

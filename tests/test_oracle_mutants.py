@@ -12,7 +12,8 @@ from tests import pins
 
 _orig = {name: getattr(R, name) for name in (
     "head_features", "vocab_logits", "log_softmax", "topk_ids", "select_level",
-    "child_states", "path_score", "prune", "emit_tree", "rnd_bf16")}
+    "child_states", "path_score", "prune", "emit_tree", "rnd_bf16", "candidate_set",
+    "candidate_logits")}
 
 
 def _head_transposed(r, A, H_d, precision):
@@ -102,7 +103,29 @@ def _rnd_truncate(x):
     return u.view(np.float32).astype(np.float64)
 
 
+def _cset_lowest(Lb_d, K):
+    return np.lexsort((np.arange(len(Lb_d)), Lb_d))[:K]
+
+
+def _cset_id_order(Lb_d, K):
+    return np.arange(K)
+
+
+def _cand_logits_full_vocab(a, U, Lb_d, cset):
+    return R.vocab_logits(a, U, Lb_d)
+
+
+def _cand_logits_no_base(a, U, Lb_d, cset):
+    z = np.full((a.shape[0], U.shape[0]), -np.inf)
+    z[:, cset] = a @ U[cset].T
+    return z
+
+
 MUTANTS = {
+    "cset_lowest_values": ("candidate_set", _cset_lowest),
+    "cset_first_ids": ("candidate_set", _cset_id_order),
+    "cand_logits_full_vocab": ("candidate_logits", _cand_logits_full_vocab),
+    "cand_logits_drop_base": ("candidate_logits", _cand_logits_no_base),
     "head_transposed_A": ("head_features", _head_transposed),
     "head_drops_hidden": ("head_features", _head_no_hidden),
     "head_skips_bf16_rounding": ("head_features", _head_no_round),
