@@ -51,15 +51,18 @@
 extern "C" {
 #endif
 
-#define DARTREE_ABI_VERSION 2
+#define DARTREE_ABI_VERSION 3
 
 /* Limits of this implementation (calls beyond them return
  * DARTREE_ERR_UNSUPPORTED). */
 #define DARTREE_MAX_VOCAB (1 << 20)      /* V */
 #define DARTREE_MAX_DEPTH 64             /* L */
 #define DARTREE_MAX_WIDTH 2048           /* W */
-#define DARTREE_MAX_BRANCH 32            /* k */
+#define DARTREE_MAX_BRANCH 32            /* k over the full vocabulary */
+#define DARTREE_MAX_CANDIDATES 256       /* K of a shared candidate set (k <= K) */
 #define DARTREE_MAX_SORT 4096            /* n_{d-1}*k candidates, |S| nodes, B */
+#define DARTREE_CSET_CHUNK 8192          /* a shared set is picked from chunks of this many logits;
+                                            ceil(V / DARTREE_CSET_CHUNK) * K <= 8192 */
 
 typedef enum dartree_status {
   DARTREE_OK = 0,
@@ -86,6 +89,14 @@ typedef struct dartree_params {
   int32_t precision;   /* dartree_precision */
   float temperature;   /* T >= 0, finite; tau = T if T > 0 else 1 */
   float depth_bonus;   /* beta <= 0, finite (Lemma 1 needs beta <= 0) */
+  int32_t candidates;  /* K >= 0.  0: every node is scored over the whole vocabulary
+                          and keeps its own top-k (the "Full" variant of Appendix D;
+                          k <= DARTREE_MAX_BRANCH).  K > 0: Alg. 1 as printed - each
+                          request and depth uses the shared candidate set
+                          C_d = TopK(L_d^base, K) by (value desc, id asc); the head
+                          scores only C_d and log q~ is normalised over C_d; each
+                          node keeps its top-k of C_d, 1 <= k <= K <= V (k = K keeps
+                          all of C_d, the paper's default K = 64) */
 } dartree_params;
 
 /* Device inputs of one round (Algorithm 1, "Require"). */
@@ -124,6 +135,7 @@ typedef struct dartree_supertree {
   float* lse;         /* [L][b*W] log sum_v exp(z_v / tau) of each parent row */
   float* cand_logp;   /* [L][b*W][k] log q~ of the row's top-k candidates, best first */
   int32_t* cand_ids;  /* [L][b*W][k] their token ids */
+  int32_t* csets;     /* [b][L][K] shared candidate sets C_d, best first (candidates > 0 only) */
 } dartree_supertree;
 
 /* ABI version (DARTREE_ABI_VERSION of the built library). */
@@ -161,10 +173,13 @@ dartree_status dartree_build_tree(const dartree_params* p, const dartree_inputs*
 
 /* Kernels of one round, in launch order, as indexed by dartree_build_tree_timed. */
 #define DARTREE_KERNEL_HEAD 0   /* t = A r, a = bf16(tanh(t + H_d)) */
-#define DARTREE_KERNEL_LOGITS 1 /* z = L_d^base + U a */
-#define DARTREE_KERNEL_LSE 2    /* log-softmax normaliser and per-row top-k (row segments) */
-#define DARTREE_KERNEL_SELECT 3 /* segment merge, segmented top-W and the state update
-                                   of the kept children (no state update at d = L) */
+#define DARTREE_KERNEL_LOGITS 1 /* z = L_d^base + U a (over C_d with shared candidate sets) */
+#define DARTREE_KERNEL_LSE 2    /* log-softmax normaliser and per-row top-k (row segments);
+                                   with shared candidate sets: the sets of every depth,
+                                   at d = 1 only (nothing at d > 1) */
+#define DARTREE_KERNEL_SELECT 3 /* segment merge (or the softmax over C_d), segmented top-W
+                                   and the state update of the kept children (no state
+                                   update at d = L) */
 #define DARTREE_KERNELS_PER_DEPTH 4
 
 /* dartree_build_tree that also records `events` (created by the caller, for
@@ -214,6 +229,15 @@ dartree_status dartree_lse_topk_workspace_size(int32_t rows, int32_t vocab, int3
 dartree_status dartree_lse_topk(const float* z, int32_t rows, int32_t vocab, int32_t k,
                                 float temperature, float* lse, float* cand_logp,
                                 int32_t* cand_ids, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Shared candidate sets (Alg. 1, C_d = TopK(L_d^base, K)) of `rows` rows of
+ * fp32 logits [rows][vocab]: ids [rows][K] in (value desc, id asc) order.
+ * 1 <= K <= min(vocab, DARTREE_MAX_CANDIDATES) and
+ * ceil(vocab / DARTREE_CSET_CHUNK) * K <= 8192; the workspace (size from
+ * dartree_candidate_sets_workspace_size) holds the per-chunk winners. */
+dartree_status dartree_candidate_sets_workspace_size(int32_t rows, int32_t vocab, int32_t K, size_t* bytes);
+dartree_status dartree_candidate_sets(const float* logits, int32_t rows, int32_t vocab, int32_t K, int32_t* ids,
+                                      void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Segmented top-W (Algorithm 1, "retain the global top-W child prefixes"):
  * for each request q < batch, candidates (j, i) for parent j < n_parent and

@@ -48,15 +48,18 @@ Shape shape_of(const dartree_params& p) {
 //   lse: f32 [L][R]   cand_logp: f32 [L][R][k]   cand_ids: i32 [L][R][k]
 //   state: act [2][R][h]   t: f32 [R][h]   a: act [R][h]   z: f32 [R][V]
 //   k3: the row-split partials of the largest depth
+//   cset: i32 [b][L][K] shared candidate sets and their chunk winners (K > 0)
 struct Layout {
-  size_t lvl_tok, lvl_par, lvl_score, lse, cand_logp, cand_ids, state0, state1, t, a, z, k3, total;
+  size_t lvl_tok, lvl_par, lvl_score, lse, cand_logp, cand_ids, state0, state1, t, a, z, k3, cset, cset_scratch, total;
 };
 
 Layout layout_of(const dartree_params& p, const Shape& s) {
   const size_t L = p.depth, b = p.batch, W = p.width, k = p.branch, h = p.hidden, V = p.vocab;
   const size_t R = b * W;
+  const size_t K = size_t(p.candidates);
   size_t k3 = 0;
-  for (int d = 1; d <= p.depth; ++d) k3 = std::max(k3, lse_topk_scratch_bytes(int64_t(b) * s.n[d - 1], V, int(k)));
+  if (K == 0)
+    for (int d = 1; d <= p.depth; ++d) k3 = std::max(k3, lse_topk_scratch_bytes(int64_t(b) * s.n[d - 1], V, int(k)));
   Layout l{};
   size_t o = 0;
   auto take = [&](size_t bytes) { const size_t at = o; o = align_up(o + bytes); return at; };
@@ -70,8 +73,10 @@ Layout layout_of(const dartree_params& p, const Shape& s) {
   l.state1 = take(R * h * act_bytes(p.precision));
   l.t = take(R * h * 4);
   l.a = take(R * h * act_bytes(p.precision));
-  l.z = take(R * V * 4);
+  l.z = take(R * (K > 0 ? K : V) * 4);   // logits over C_d only with a shared set
   l.k3 = take(k3);
+  l.cset = take(b * L * K * 4);
+  l.cset_scratch = take(K > 0 ? candidate_sets_scratch_bytes(int64_t(b) * L, V, int(K)) : 0);
   l.total = o;
   return l;
 }
@@ -82,11 +87,17 @@ dartree_status validate(const dartree_params* p) {
       p->budget < 1)
     return DARTREE_ERR_INVALID_ARG;
   if (p->branch > p->vocab) return DARTREE_ERR_INVALID_ARG;
+  if (p->candidates < 0) return DARTREE_ERR_INVALID_ARG;
+  if (p->candidates > 0 && (p->candidates > p->vocab || p->branch > p->candidates)) return DARTREE_ERR_INVALID_ARG;
   if (p->precision != DARTREE_FP32 && p->precision != DARTREE_BF16) return DARTREE_ERR_INVALID_ARG;
   if (!isfinite(p->temperature) || p->temperature < 0.f) return DARTREE_ERR_INVALID_ARG;
   if (!isfinite(p->depth_bonus) || p->depth_bonus > 0.f) return DARTREE_ERR_INVALID_ARG;
   if (p->vocab > DARTREE_MAX_VOCAB || p->depth > DARTREE_MAX_DEPTH || p->width > DARTREE_MAX_WIDTH ||
-      p->branch > DARTREE_MAX_BRANCH || p->budget > DARTREE_MAX_SORT)
+      p->budget > DARTREE_MAX_SORT)
+    return DARTREE_ERR_UNSUPPORTED;
+  if (p->candidates == 0 && p->branch > DARTREE_MAX_BRANCH) return DARTREE_ERR_UNSUPPORTED;
+  if (p->candidates > 0 &&
+      (p->candidates > DARTREE_MAX_CANDIDATES || !candidate_sets_supported(p->vocab, p->candidates)))
     return DARTREE_ERR_UNSUPPORTED;
   if (p->precision == DARTREE_BF16 && p->hidden % 64 != 0) return DARTREE_ERR_UNSUPPORTED;
   const Shape s = shape_of(*p);
@@ -153,6 +164,64 @@ struct Timer {
   }
 };
 
+// Depth d with a shared candidate set (after K1): the sets of every depth at
+// d = 1, the logits over C_d, then selection and state update.
+dartree_status expand_shared(const dartree_params& p, const dartree_inputs& in, int d, void* ws, const Layout& l,
+                             const Shape& s, hipStream_t st, const Timer& tm, const float* t, const void* a, float* z,
+                             void* r_out) {
+  const int tb = (d - 1) * DARTREE_KERNELS_PER_DEPTH;
+  const int64_t b = p.batch, V = p.vocab, h = p.hidden, L = p.depth, W = p.width, k = p.branch;
+  const int K = p.candidates;
+  const int64_t np = s.n[d - 1], nc = s.n[d];
+  int32_t* csets = at<int32_t>(ws, l.cset);
+  const float tau = p.temperature > 0.f ? p.temperature : 1.f;
+  hipError_t err;
+  tm.mark(tb + DARTREE_KERNEL_LSE, 0);   // marked at every depth; the sets are built at d = 1
+  if (d == 1) {
+    err = launch_candidate_sets(in.drafter_logits, b * L, V, K, csets, at<char>(ws, l.cset_scratch), st);
+    if (err != hipSuccess) return DARTREE_ERR_HIP;
+  }
+  tm.mark(tb + DARTREE_KERNEL_LSE, 1);
+  tm.mark(tb + DARTREE_KERNEL_LOGITS, 0);
+  err = launch_shared_logits(p.precision, int(b), int(np), K, int(h), a, in.head_U,
+                             in.drafter_logits + size_t(d - 1) * V, L * V, csets + (d - 1) * K, L * K, z, st);
+  tm.mark(tb + DARTREE_KERNEL_LOGITS, 1);
+  if (err != hipSuccess) return DARTREE_ERR_HIP;
+
+  LevelArgs la{};
+  la.batch = int(b);
+  la.n_parent = int(np);
+  la.k = int(k);
+  la.n_keep = int(nc);
+  la.beta = p.depth_bonus;
+  la.tau = tau;
+  la.parent_stride = int(W);
+  la.out_stride = int(W);
+  la.parent_score = d == 1 ? nullptr : at<float>(ws, l.lvl_score) + (d - 2) * b * W;
+  la.nseg = 1;
+  la.lse = at<float>(ws, l.lse) + (d - 1) * b * W;
+  la.cand_logp = at<float>(ws, l.cand_logp) + (d - 1) * b * W * k;
+  la.cand_ids = at<int32_t>(ws, l.cand_ids) + (d - 1) * b * W * k;
+  la.out_tok = at<int32_t>(ws, l.lvl_tok) + (d - 1) * b * W;
+  la.out_par = at<int32_t>(ws, l.lvl_par) + (d - 1) * b * W;
+  la.out_score = at<float>(ws, l.lvl_score) + (d - 1) * b * W;
+  la.shared_k = K;
+  la.zsh = z;
+  la.cset = csets + (d - 1) * K;
+  la.cset_stride = L * K;
+  la.state = d < p.depth;
+  la.precision = p.precision;
+  la.hidden = int(h);
+  la.t = t;
+  la.U = in.head_U;
+  la.e = float(sqrt(double(p.hidden)));
+  la.r_out = r_out;
+  tm.mark(tb + DARTREE_KERNEL_SELECT, 0);
+  err = launch_select_level(la, st);
+  tm.mark(tb + DARTREE_KERNEL_SELECT, 1);
+  return err == hipSuccess ? DARTREE_OK : DARTREE_ERR_HIP;
+}
+
 // Enqueue depth d (validated arguments).
 dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, void* ws, const Layout& l,
                       const Shape& s, hipStream_t st, const Timer& tm = Timer()) {
@@ -194,6 +263,8 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   hipError_t err = launch_project(head, st);
   tm.mark(tb + DARTREE_KERNEL_HEAD, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
+
+  if (p.candidates > 0) return expand_shared(p, in, d, ws, l, s, st, tm, t, a, z, r_out);
 
   // K2: z = L_d^base + U a
   ProjArgs lg{};
@@ -342,6 +413,7 @@ dartree_status dartree_export_supertree(const dartree_params* p, const void* ws,
       {dst->tokens, l.lvl_tok, L * b * W * 4},   {dst->parents, l.lvl_par, L * b * W * 4},
       {dst->scores, l.lvl_score, L * b * W * 4}, {dst->lse, l.lse, L * b * W * 4},
       {dst->cand_logp, l.cand_logp, L * b * W * k * 4}, {dst->cand_ids, l.cand_ids, L * b * W * k * 4},
+      {p->candidates > 0 ? dst->csets : nullptr, l.cset, b * L * size_t(p->candidates) * 4},
   };
   for (const Item& it : items)
     if (it.to && hipMemcpyAsync(it.to, at<char>(ws, it.off), it.bytes, hipMemcpyDeviceToDevice, stream) != hipSuccess)
@@ -401,6 +473,24 @@ dartree_status dartree_lse_topk(const float* z, int32_t rows, int32_t vocab, int
   if (need > 0 && (!ws || ws_bytes < need || !aligned16(ws))) return DARTREE_ERR_WORKSPACE;
   const float tau = temperature > 0.f ? temperature : 1.f;
   return hip_status(launch_lse_topk(z, rows, vocab, k, tau, lse, cand_logp, cand_ids, ws, true, stream));
+}
+
+dartree_status dartree_candidate_sets_workspace_size(int32_t rows, int32_t vocab, int32_t K, size_t* bytes) {
+  if (!bytes || rows < 1 || vocab < 1 || K < 1 || K > vocab) return DARTREE_ERR_INVALID_ARG;
+  if (vocab > DARTREE_MAX_VOCAB || K > DARTREE_MAX_CANDIDATES || !candidate_sets_supported(vocab, K))
+    return DARTREE_ERR_UNSUPPORTED;
+  *bytes = candidate_sets_scratch_bytes(rows, vocab, K);
+  return DARTREE_OK;
+}
+
+dartree_status dartree_candidate_sets(const float* logits, int32_t rows, int32_t vocab, int32_t K, int32_t* ids,
+                                      void* ws, size_t ws_bytes, hipStream_t stream) {
+  size_t need = 0;
+  dartree_status v = dartree_candidate_sets_workspace_size(rows, vocab, K, &need);
+  if (v != DARTREE_OK) return v;
+  if (!logits || !ids) return DARTREE_ERR_INVALID_ARG;
+  if (!ws || ws_bytes < need || !aligned16(ws)) return DARTREE_ERR_WORKSPACE;
+  return hip_status(launch_candidate_sets(logits, rows, vocab, K, ids, ws, stream));
 }
 
 dartree_status dartree_select_topw(int32_t batch, int32_t n_parent, int32_t k, int32_t n_keep, float depth_bonus,

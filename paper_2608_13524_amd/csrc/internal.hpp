@@ -84,6 +84,10 @@ struct LevelArgs {
   int32_t* out_tok;
   int32_t* out_par;
   float* out_score;
+  int shared_k;                   // K > 0: candidates from logits over the shared set C_d
+  const float* zsh;               // [rows][K] corrected logits over C_d (shared_k > 0)
+  const int32_t* cset;            // request q's C_d at cset + q * cset_stride
+  int64_t cset_stride;
   int state;                      // 0: no state update
   int precision, hidden;
   const float* t;                 // [rows][hidden]
@@ -92,6 +96,19 @@ struct LevelArgs {
   void* r_out;                    // act [batch * n_keep][hidden]
 };
 hipError_t launch_select_level(const LevelArgs& a, hipStream_t s);
+
+// Shared candidate sets C = TopK(logits row, K) of `rows` fp32 rows, ids in
+// (value desc, id asc) order; scratch holds the per-chunk winners.
+size_t candidate_sets_scratch_bytes(int64_t rows, int64_t vocab, int K);
+bool candidate_sets_supported(int64_t vocab, int K);
+hipError_t launch_candidate_sets(const float* logits, int64_t rows, int64_t vocab, int K, int32_t* ids,
+                                 void* scratch, hipStream_t s);
+
+// Corrected logits over the shared set: z[q*np + j][c] = lb[q*lb_stride + C[c]]
+// + U[C[c]] . a[q*np + j], with C = cset + q * cset_stride.
+hipError_t launch_shared_logits(int precision, int batch, int np, int K, int hidden, const void* a, const void* U,
+                                const float* lb, int64_t lb_stride, const int32_t* cset, int64_t cset_stride,
+                                float* z, hipStream_t s);
 
 // Deferred top-B prune and tree emission (K6).
 struct LevelShape {

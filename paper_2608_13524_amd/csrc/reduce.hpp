@@ -212,4 +212,28 @@ __device__ __forceinline__ Partial wave_merge_records(const float* recs, int nse
   return wp;
 }
 
+// Ascending bitonic sort of npad (a power of two, >= 2) keys in LDS by the
+// whole block; returns after a barrier.
+__device__ inline void bitonic_sort(uint64_t* keys, int npad) {
+  for (int size = 2; size <= npad; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = threadIdx.x; i < npad; i += blockDim.x) {
+        const int j = i ^ stride;
+        if (j > i) {
+          const uint64_t a = keys[i], b = keys[j];
+          const bool up = (i & size) == 0;
+          if ((a > b) == up) { keys[i] = b; keys[j] = a; }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+__host__ __device__ inline int next_pow2(int n) {
+  int p = 2;
+  while (p < n) p <<= 1;
+  return p;
+}
+
 }  // namespace dartree

@@ -25,33 +25,12 @@ namespace {
 
 constexpr int kSortMax = DARTREE_MAX_SORT;
 
-__device__ void bitonic_sort(uint64_t* keys, int npad) {
-  for (int size = 2; size <= npad; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = threadIdx.x; i < npad; i += blockDim.x) {
-        const int j = i ^ stride;
-        if (j > i) {
-          const uint64_t a = keys[i], b = keys[j];
-          const bool up = (i & size) == 0;
-          if ((a > b) == up) { keys[i] = b; keys[j] = a; }
-        }
-      }
-      __syncthreads();
-    }
-  }
-}
-
-__device__ __forceinline__ int next_pow2(int n) {
-  int p = 2;
-  while (p < n) p <<= 1;
-  return p;
-}
-
 // grid: batch * S, block (q, sl): request q, state slice sl.  Three steps of
 // one depth in one launch:
 //  1. the candidate log-probabilities of request q's parent rows: read as
 //     written by the softmax pass, or merged here from its per-segment
-//     records (one wave per row; block 0 of the request also stores them);
+//     records, or (shared candidate set) computed here from the row's logits
+//     over C_d (one wave per row; block 0 of the request also stores them);
 //  2. s = (s_parent + log q~) + beta for every candidate and the best n_keep
 //     by (s desc, parent slot asc, token asc), from one bitonic sort of 64-bit
 //     keys (low word: parent slot (12 bits) << 20 | token (20 bits)); block 0
@@ -71,7 +50,50 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
   const int q = blockIdx.x / S, sl = blockIdx.x - q * S;
   const int np = a.n_parent, k = a.k, n = np * k;
   const int64_t rbase = int64_t(q) * np;
-  if (a.nseg > 1) {
+  if (a.shared_k > 0) {
+    // shared candidate set: row j's K corrected logits over C_d -> log q~
+    // normalised over C_d, and its k best by (z desc, id asc), ranked by
+    // counting over the row (staged in this wave's LDS row)
+    __shared__ float rz[16][DARTREE_MAX_CANDIDATES];
+    __shared__ int32_t rid[16][DARTREE_MAX_CANDIDATES];
+    const int nk = a.shared_k;
+    const float scale = kLog2e / a.tau;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nwaves = blockDim.x >> 6;
+    const int32_t* set = a.cset + q * a.cset_stride;
+    for (int j = wave; j < np; j += nwaves) {
+      const float* zr = a.zsh + (rbase + j) * nk;
+      float m = -INFINITY;
+      for (int c = lane; c < nk; c += 64) {
+        const float v = zr[c];
+        rz[wave][c] = v;
+        rid[wave][c] = set[c];
+        m = fmaxf(m, v);
+      }
+      m = wave_max(m);
+      float sum = 0.f;
+      for (int c = lane; c < nk; c += 64) sum += __builtin_amdgcn_exp2f((rz[wave][c] - m) * scale);
+      const float log_s = logf(wave_sum(sum));
+      __builtin_amdgcn_wave_barrier();
+      for (int c = lane; c < nk; c += 64) {
+        const float v = rz[wave][c];
+        const int id = rid[wave][c];
+        int rank = 0;
+        for (int o = 0; o < nk; ++o) rank += int(better(rz[wave][o], rid[wave][o], v, id));
+        if (rank < k) {
+          const float lp = (v - m) / a.tau - log_s;
+          c_logp[j * k + rank] = lp;
+          c_ids[j * k + rank] = id;
+          if (sl == 0) {
+            a.cand_logp[(rbase + j) * k + rank] = lp;
+            a.cand_ids[(rbase + j) * k + rank] = id;
+          }
+        }
+      }
+      if (sl == 0 && lane == 0) a.lse[rbase + j] = m / a.tau + log_s;
+      __builtin_amdgcn_wave_barrier();   // the LDS row is rewritten for the next row
+    }
+  } else if (a.nseg > 1) {
     constexpr int RF = record_floats<K>();
     const float scale = kLog2e / a.tau;
     const int lane = threadIdx.x & 63;

@@ -23,6 +23,7 @@ MAX_VOCAB = 1 << 20
 MAX_DEPTH = 64
 MAX_WIDTH = 2048
 MAX_BRANCH = 32
+MAX_CANDIDATES = 256
 MAX_SORT = 4096
 
 SYMBOLS = [
@@ -30,7 +31,7 @@ SYMBOLS = [
     "dartree_workspace_size", "dartree_expand_depth", "dartree_prune",
     "dartree_build_tree", "dartree_build_tree_timed", "dartree_export_supertree", "dartree_export_states", "dartree_project",
     "dartree_lse_topk_workspace_size", "dartree_lse_topk", "dartree_select_topw",
-    "dartree_prune_levels",
+    "dartree_prune_levels", "dartree_candidate_sets_workspace_size", "dartree_candidate_sets",
     "dartree_calib_read", "dartree_calib_copy", "dartree_calib_mfma",
 ]
 CALIB_SINK_FLOATS = 4096
@@ -40,12 +41,14 @@ class Params(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("vocab", ctypes.c_int32), ("hidden", ctypes.c_int32),
                 ("depth", ctypes.c_int32), ("width", ctypes.c_int32), ("branch", ctypes.c_int32),
                 ("budget", ctypes.c_int32), ("precision", ctypes.c_int32),
-                ("temperature", ctypes.c_float), ("depth_bonus", ctypes.c_float)]
+                ("temperature", ctypes.c_float), ("depth_bonus", ctypes.c_float),
+                ("candidates", ctypes.c_int32)]
 
     @staticmethod
     def of(cfg) -> "Params":
         return Params(cfg.batch, cfg.vocab, cfg.hidden, cfg.depth, cfg.width, cfg.branch,
-                      cfg.budget, cfg.precision, float(cfg.temperature), float(cfg.depth_bonus))
+                      cfg.budget, cfg.precision, float(cfg.temperature), float(cfg.depth_bonus),
+                      int(getattr(cfg, "candidates", 0)))
 
     def level_sizes(self) -> list[int]:
         n, out = 1, []
@@ -68,7 +71,8 @@ class TreeC(ctypes.Structure):
 
 class SupertreeC(ctypes.Structure):
     _fields_ = [("tokens", ctypes.c_void_p), ("parents", ctypes.c_void_p), ("scores", ctypes.c_void_p),
-                ("lse", ctypes.c_void_p), ("cand_logp", ctypes.c_void_p), ("cand_ids", ctypes.c_void_p)]
+                ("lse", ctypes.c_void_p), ("cand_logp", ctypes.c_void_p), ("cand_ids", ctypes.c_void_p),
+                ("csets", ctypes.c_void_p)]
 
 
 class DartreeError(RuntimeError):
@@ -110,6 +114,8 @@ def lib() -> ctypes.CDLL:
     L.dartree_lse_topk.argtypes = [vp, i32, i32, i32, f32, vp, vp, vp, vp, sz, vp]
     L.dartree_select_topw.argtypes = [i32, i32, i32, i32, f32, vp, vp, vp, vp, vp, vp, vp]
     L.dartree_prune_levels.argtypes = [P, vp, vp, vp, ctypes.POINTER(TreeC), vp]
+    L.dartree_candidate_sets_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(sz)]
+    L.dartree_candidate_sets.argtypes = [vp, i32, i32, i32, vp, vp, sz, vp]
     L.dartree_calib_read.argtypes = [vp, sz, vp, vp]
     L.dartree_calib_copy.argtypes = [vp, vp, sz, vp]
     L.dartree_calib_mfma.argtypes = [i32, i32, vp, vp]
@@ -236,6 +242,7 @@ class DeviceSupertree:
     lse: object
     cand_logp: object
     cand_ids: object
+    csets: object = None   # [b][L][K] shared candidate sets (candidates > 0)
 
     def c(self) -> SupertreeC:
         return SupertreeC(*(_ptr(getattr(self, f.name)) for f in dataclasses.fields(self)))
@@ -246,12 +253,15 @@ class DeviceSupertree:
         L, b, W, k = p.depth, p.batch, p.width, p.branch
         i32 = dict(dtype=torch.int32, device=device)
         f32 = dict(dtype=torch.float32, device=device)
+        K = p.candidates
         return DeviceSupertree(torch.empty(L, b, W, **i32), torch.empty(L, b, W, **i32),
                                torch.empty(L, b, W, **f32), torch.empty(L, b * W, **f32),
-                               torch.empty(L, b * W, k, **f32), torch.empty(L, b * W, k, **i32))
+                               torch.empty(L, b * W, k, **f32), torch.empty(L, b * W, k, **i32),
+                               torch.empty(b, L, K, **i32) if K > 0 else None)
 
     def host(self) -> dict:
-        return {f.name: getattr(self, f.name).cpu().numpy() for f in dataclasses.fields(self)}
+        return {f.name: getattr(self, f.name).cpu().numpy() for f in dataclasses.fields(self)
+                if getattr(self, f.name) is not None}
 
 
 def alloc_workspace(p: Params, device="cuda"):
@@ -353,3 +363,18 @@ def calib_mfma(blocks: int, iters: int, sink, stream=None) -> float:
     """Launch the MFMA-only loop; returns its flop count."""
     _check(lib().dartree_calib_mfma(blocks, iters, _ptr(sink), _stream(stream)), "dartree_calib_mfma")
     return float(blocks) * 4 * iters * 64 * (2 * 16 * 16 * 32)
+
+
+def candidate_sets(logits, K: int, ids, ws=None, stream=None) -> None:
+    """Shared candidate sets: ids [rows][K] = TopK of each fp32 row by (value desc, id asc)."""
+    rows, vocab = logits.shape
+    _check(lib().dartree_candidate_sets(_ptr(logits), rows, vocab, K, _ptr(ids), _ptr(ws),
+                                        0 if ws is None else ws.numel(), _stream(stream)),
+           "dartree_candidate_sets")
+
+
+def candidate_sets_workspace_size(rows: int, vocab: int, K: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().dartree_candidate_sets_workspace_size(rows, vocab, K, ctypes.byref(n)),
+           "dartree_candidate_sets_workspace_size")
+    return n.value

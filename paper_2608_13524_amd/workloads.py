@@ -53,6 +53,7 @@ class Config:
     temperature: float
     precision: int
     seed: int
+    candidates: int = 0           # 0: full vocabulary; K > 0: shared C_d = TopK(L_d^base, K)
     depth_bonus: float = -0.2
     sigma_w: float = 0.02
     sigma_l: float = 2.0
@@ -95,7 +96,18 @@ CONFIGS = {
                          depth=16, width=64, branch=8, budget=512,
                          temperature=1.0, precision=BF16, seed=4, n_boost=64),
 }
-CONFIG_ORDER = ["tiny", "qwen3-4b", "qwen3-4b-wide", "qwen3-8b-x4", "stress-x16"]
+# The paper's default candidate set (Alg. 1 as printed; Sec. 4.1 "DARTree
+# (pruned)": K = 64 candidates per position, width 12, B = 64, beta = -0.2):
+# every node of a depth is scored over the same C_d = TopK(L_d^base, 64) and
+# keeps all of it (branching k = K).
+CONFIGS["qwen3-4b-shared"] = Config("qwen3-4b-shared", batch=1, vocab=151936, hidden=2560, depth=16,
+                                    width=12, branch=64, budget=64, temperature=0.0,
+                                    precision=BF16, seed=5, candidates=64)
+CONFIGS["qwen3-8b-shared-x4"] = Config("qwen3-8b-shared-x4", batch=4, vocab=151936, hidden=4096,
+                                       depth=16, width=12, branch=64, budget=64,
+                                       temperature=1.0, precision=BF16, seed=6, candidates=64)
+CONFIG_ORDER = ["tiny", "qwen3-4b", "qwen3-4b-wide", "qwen3-8b-x4", "stress-x16",
+                "qwen3-4b-shared", "qwen3-8b-shared-x4"]
 
 
 def fp32_to_bf16_bits(x: np.ndarray) -> np.ndarray:

@@ -171,6 +171,10 @@ def follow(dec, sup: dict, tree: dict, batch_index: list, requests: list, gpu_st
         st = R.build_supertree(dec, requests=[i], choose=choose, choose_topk=choose_topk,
                                adopt_states=adopt if gpu_states is not None else None)
         followed.append(st.levels[0])
+        if p.candidates > 0:   # shared sets depend on the drafter logits only: bit-exact
+            for d, lvl in enumerate(st.levels[0], start=1):
+                if not np.array_equal(sup["csets"][q, d - 1].astype(np.int64), lvl.cset):
+                    raise ParityError(f"request {b} depth {d}: shared candidate set differs")
 
         # top-B: the GPU's kept set, read back from its emitted tree
         levels = st.levels[0]

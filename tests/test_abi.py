@@ -22,7 +22,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     syms = declared_symbols()
-    assert len(syms) == 18, syms
+    assert len(syms) == 20, syms
     lib = D.lib()
     for s in syms:
         assert hasattr(lib, s), s
@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert D.abi_version() == 2
+    assert D.abi_version() == 3
     for s in range(5):
         assert D.status_string(s)
     assert D.status_string(99) == "unknown status"
@@ -153,3 +153,34 @@ def test_calibration_kernels_reject_bad_arguments():
     assert lib.dartree_calib_mfma(D.CALIB_SINK_FLOATS + 1, 10, sink, None) == D.ERR_INVALID_ARG
     assert lib.dartree_calib_mfma(4, 0, sink, None) == D.ERR_INVALID_ARG
     assert lib.dartree_calib_mfma(4, 10, None, None) == D.ERR_INVALID_ARG
+
+
+def test_validate_shared_candidate_sets():
+    p = D.Params.of(W.CONFIGS["qwen3-4b-shared"])
+    assert D.validate(p) == D.OK
+    assert D.validate(_p(candidates=-1)) == D.ERR_INVALID_ARG
+    assert D.validate(_p(candidates=4, branch=8)) == D.ERR_INVALID_ARG        # k > K
+    assert D.validate(_p(candidates=64, branch=64)) == D.OK                   # k may exceed 32 with a shared set
+    assert D.validate(_p(candidates=0, branch=64)) == D.ERR_UNSUPPORTED       # not over the full vocabulary
+    assert D.validate(_p(candidates=257, branch=8)) == D.ERR_UNSUPPORTED
+    small = D.Params.of(W.CONFIGS["tiny"])
+    small.candidates = small.vocab + 1
+    assert D.validate(small) == D.ERR_INVALID_ARG                              # K > V
+    big = _p(candidates=256, branch=8)
+    big.vocab = 1 << 20                                                        # 128 chunks x 256 > 8192
+    assert D.validate(big) == D.ERR_UNSUPPORTED
+    assert D.workspace_size(p) < D.workspace_size(D.Params.of(W.CONFIGS["qwen3-4b"]))   # logits over C_d only
+
+
+def test_candidate_sets_reject_bad_arguments():
+    lib = D.lib()
+    n = ctypes.c_size_t(0)
+    assert lib.dartree_candidate_sets_workspace_size(4, 100, 0, ctypes.byref(n)) == D.ERR_INVALID_ARG
+    assert lib.dartree_candidate_sets_workspace_size(4, 100, 101, ctypes.byref(n)) == D.ERR_INVALID_ARG
+    assert lib.dartree_candidate_sets_workspace_size(4, 100000, 257, ctypes.byref(n)) == D.ERR_UNSUPPORTED
+    assert lib.dartree_candidate_sets_workspace_size(4, 151936, 64, ctypes.byref(n)) == D.OK
+    assert n.value == 4 * 19 * 64 * 8
+    ws = ctypes.c_void_p(FAKE)
+    assert lib.dartree_candidate_sets(None, 4, 151936, 64, ctypes.c_void_p(FAKE), ws, n.value, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_candidate_sets(ctypes.c_void_p(FAKE), 4, 151936, 64, ctypes.c_void_p(FAKE), ws, n.value - 1,
+                                      None) == D.ERR_WORKSPACE

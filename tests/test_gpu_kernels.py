@@ -272,3 +272,27 @@ def test_calibration_kernels():
     want = 4 * 5 * tile
     got = sink[:3].cpu()
     assert torch.allclose(got, torch.full((3,), want), rtol=1e-6), (got, want)
+
+
+@pytest.mark.parametrize("rows,vocab,K,dist", [
+    (3, 151936, 64, "normal"), (2, 151936, 256, "ties"), (4, 20001, 17, "ties"), (2, 8193, 64, "normal"),
+    (5, 100, 7, "ties"), (3, 8192, 1, "normal"), (2, 40, 40, "ties"),
+])
+def test_candidate_sets_bit_exact(rows, vocab, K, dist):
+    """C = TopK(row, K) by (value desc, id asc), bit for bit, ties included."""
+    g = np.random.default_rng(rows * 1000 + K)
+    if dist == "ties":
+        x = g.integers(-3, 4, size=(rows, vocab)).astype(np.float32)
+    else:
+        x = g.standard_normal((rows, vocab)).astype(np.float32)
+    dev = device()
+    xd = torch.from_numpy(x).to(dev)
+    ids = torch.empty(rows, K, dtype=torch.int32, device=dev)
+    ws = torch.empty(max(D.candidate_sets_workspace_size(rows, vocab, K), 16), dtype=torch.uint8, device=dev)
+    say(f"candidate sets rows={rows} V={vocab} K={K} {dist}")
+    D.candidate_sets(xd, K, ids, ws)
+    torch.cuda.synchronize()
+    got = ids.cpu().numpy()
+    for r in range(rows):
+        want = np.lexsort((np.arange(vocab), -x[r]))[:K]
+        assert np.array_equal(got[r], want), (r, got[r][:10], want[:10])

@@ -43,6 +43,17 @@ SMALL = {
     "bf16-k20": small(branch=20, width=24, budget=70, seed=48),       # top-k bucket 32
     "fp32-small": small(precision=W.FP32, hidden=48, sigma_w=0.1, seed=40),
     "fp32-tiny-vocab": small(precision=W.FP32, vocab=7, hidden=5, branch=3, width=5, budget=12, seed=41),
+    # shared candidate sets C_d = TopK(L_d^base, K)
+    "shared-bf16": small(candidates=12, branch=12, width=10, budget=30, seed=50),
+    "shared-k<K": small(candidates=20, branch=5, width=8, seed=51),
+    "shared-T0.7": small(candidates=16, branch=16, temperature=0.7, seed=52),
+    "shared-wide-rows": small(batch=2, candidates=10, branch=10, width=80, budget=150, vocab=3001, hidden=128,
+                              seed=53),   # 80 parent rows: two row blocks of the gather product
+    "shared-sort": small(batch=2, candidates=40, branch=40, width=40, budget=100, vocab=2053, hidden=128,
+                         seed=57),        # 1600 candidates per request: the bitonic path
+    "shared-fp32": small(precision=W.FP32, hidden=48, candidates=9, branch=9, sigma_w=0.1, seed=54),
+    "shared-K-eq-V": small(vocab=40, candidates=40, branch=6, width=6, hidden=64, seed=55),
+    "shared-k1": small(candidates=8, branch=1, budget=8, seed=56),
 }
 
 
@@ -115,7 +126,7 @@ def test_expand_then_prune_equals_build():
 
 # Full-size workloads: which requests the oracle re-derives.
 FULL_SAMPLE = {"tiny": [0], "qwen3-4b": [0], "qwen3-4b-wide": [0], "qwen3-8b-x4": [0, 3],
-               "stress-x16": [0, 15]}
+               "stress-x16": [0, 15], "qwen3-4b-shared": [0], "qwen3-8b-shared-x4": [0, 3]}
 
 
 def _log_report(name, mode, rep):
