@@ -73,6 +73,14 @@ def kernel_work(cfg, kind: str, d: int):
     R = cfg.batch * sizes[d - 1]
     h, V, b = cfg.hidden, cfg.vocab, cfg.batch
     act = 2 if cfg.precision == W.BF16 else 4
+    K = getattr(cfg, "candidates", 0)
+    if K and kind == "logits":
+        # shared set: the K gathered rows of U and the bias entries once per
+        # request, the R feature rows, one fp32 logit per (row, candidate)
+        return b * K * (act * h + 4) + act * h * R + 4 * R * K, 2.0 * R * h * K
+    if K and kind == "lse_topk":
+        # the candidate sets of all depths, built at d = 1: one read of L^base
+        return (4 * b * cfg.depth * V, 0.0) if d == 1 else (0, 0.0)
     if kind == "logits":
         return V * (act * h + 4 * b + 4 * R) + act * h * R, 2.0 * R * h * V
     if kind == "lse_topk":
@@ -260,13 +268,16 @@ def main() -> int:
     roof["algorithmic_bytes_per_launch"] = bytes_round / launches
     roof["algorithmic_flops_per_launch"] = flops_round / launches
     roof["avg_launch_us"] = kernels[dom]["avg_us_per_launch"]
-    # second roofline of the per-row softmax/top-k pass (HBM)
+    # second roofline of the per-row softmax/top-k pass (HBM); with a shared
+    # candidate set this slot is the candidate-set pass over L^base at d = 1
     lb, _ = work["lse_topk"]
     lse_t = kernels["lse_topk"]["us_per_round"] * 1e-6
     lse_roof = {"bound": "hbm", "achieved": lb / lse_t / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": lb / lse_t / 1e9 / HBM_PEAK_GBS,
-                "note": "z is written by the projection just before; below ~256 MB it can be served "
-                        "from the Infinity Cache rather than HBM"}
+                "note": ("candidate sets TopK(L^base, K) of every depth, built once per round"
+                         if getattr(cfg, "candidates", 0) else
+                         "z is written by the projection just before; below ~256 MB it can be served "
+                         "from the Infinity Cache rather than HBM")}
     proj_flops = work["logits"][1] / (kernels["logits"]["us_per_round"] * 1e-6) / 1e12
 
     # achievable ceilings measured in this job: stream U once (the projection's
@@ -282,7 +293,8 @@ def main() -> int:
 
     sizes = [1] + cfg.level_sizes()
     nodes = cfg.batch * sum(sizes[d - 1] * cfg.branch for d in range(1, cfg.depth + 1))
-    vocab_entries = cfg.batch * sum(sizes[d - 1] for d in range(1, cfg.depth + 1)) * cfg.vocab
+    per_row = getattr(cfg, "candidates", 0) or cfg.vocab   # entries scored per parent row
+    vocab_entries = cfg.batch * sum(sizes[d - 1] for d in range(1, cfg.depth + 1)) * per_row
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -296,7 +308,8 @@ def main() -> int:
         "vs_baseline": None, "dtype": "bf16" if cfg.precision == W.BF16 else "f32", "data": "synthetic",
         "config": {"workload": cfg.name, "batch": cfg.batch, "vocab": cfg.vocab, "hidden": cfg.hidden,
                    "depth": cfg.depth, "width": cfg.width, "branch": cfg.branch, "budget": cfg.budget,
-                   "temperature": cfg.temperature, "depth_bonus": cfg.depth_bonus},
+                   "temperature": cfg.temperature, "depth_bonus": cfg.depth_bonus,
+                   "candidates": getattr(cfg, "candidates", 0)},
         "timing": "HIP graph replay of dartree_build_tree",
         "eager_us_per_round": eager_us,
         "us_per_round_p10": float(np.percentile(per_step_ms, 10) * 1e3),

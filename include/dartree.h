@@ -61,8 +61,6 @@ extern "C" {
 #define DARTREE_MAX_BRANCH 32            /* k over the full vocabulary */
 #define DARTREE_MAX_CANDIDATES 256       /* K of a shared candidate set (k <= K) */
 #define DARTREE_MAX_SORT 4096            /* n_{d-1}*k candidates, |S| nodes, B */
-#define DARTREE_CSET_CHUNK 8192          /* a shared set is picked from chunks of this many logits;
-                                            ceil(V / DARTREE_CSET_CHUNK) * K <= 8192 */
 
 typedef enum dartree_status {
   DARTREE_OK = 0,
@@ -231,10 +229,9 @@ dartree_status dartree_lse_topk(const float* z, int32_t rows, int32_t vocab, int
                                 int32_t* cand_ids, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Shared candidate sets (Alg. 1, C_d = TopK(L_d^base, K)) of `rows` rows of
- * fp32 logits [rows][vocab]: ids [rows][K] in (value desc, id asc) order.
- * 1 <= K <= min(vocab, DARTREE_MAX_CANDIDATES) and
- * ceil(vocab / DARTREE_CSET_CHUNK) * K <= 8192; the workspace (size from
- * dartree_candidate_sets_workspace_size) holds the per-chunk winners. */
+ * fp32 logits [rows][vocab]: ids [rows][K] in (value desc, id asc) order,
+ * 1 <= K <= min(vocab, DARTREE_MAX_CANDIDATES).  The workspace (size from
+ * dartree_candidate_sets_workspace_size) holds per-row group maxima. */
 dartree_status dartree_candidate_sets_workspace_size(int32_t rows, int32_t vocab, int32_t K, size_t* bytes);
 dartree_status dartree_candidate_sets(const float* logits, int32_t rows, int32_t vocab, int32_t K, int32_t* ids,
                                       void* ws, size_t ws_bytes, hipStream_t stream);

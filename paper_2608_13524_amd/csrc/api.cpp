@@ -199,6 +199,7 @@ dartree_status expand_shared(const dartree_params& p, const dartree_inputs& in, 
   la.out_stride = int(W);
   la.parent_score = d == 1 ? nullptr : at<float>(ws, l.lvl_score) + (d - 2) * b * W;
   la.nseg = 1;
+  la.rows_ranked = 1;
   la.lse = at<float>(ws, l.lse) + (d - 1) * b * W;
   la.cand_logp = at<float>(ws, l.cand_logp) + (d - 1) * b * W * k;
   la.cand_ids = at<int32_t>(ws, l.cand_ids) + (d - 1) * b * W * k;
@@ -303,6 +304,7 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   la.out_stride = int(W);
   la.parent_score = parent_score;
   la.nseg = lse_topk_segments(R, V);
+  la.rows_ranked = 1;
   la.part = at<float>(ws, l.k3);
   la.lse = lse;
   la.cand_logp = clp;

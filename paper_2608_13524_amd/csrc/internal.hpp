@@ -84,6 +84,8 @@ struct LevelArgs {
   int32_t* out_tok;
   int32_t* out_par;
   float* out_score;
+  int rows_ranked;                // each row's candidates are in rank order (only the first
+                                  // min(k, n_keep) of a row can be kept)
   int shared_k;                   // K > 0: candidates from logits over the shared set C_d
   const float* zsh;               // [rows][K] corrected logits over C_d (shared_k > 0)
   const int32_t* cset;            // request q's C_d at cset + q * cset_stride

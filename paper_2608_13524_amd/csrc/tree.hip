@@ -48,7 +48,8 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
   __shared__ float c_logp[kSortMax];
   __shared__ int32_t c_ids[kSortMax];
   const int q = blockIdx.x / S, sl = blockIdx.x - q * S;
-  const int np = a.n_parent, k = a.k, n = np * k;
+  const int np = a.n_parent, k = a.k;
+  int n = np * k;
   const int64_t rbase = int64_t(q) * np;
   if (a.shared_k > 0) {
     // shared candidate set: row j's K corrected logits over C_d -> log q~
@@ -79,6 +80,7 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
         const float v = rz[wave][c];
         const int id = rid[wave][c];
         int rank = 0;
+#pragma unroll 8
         for (int o = 0; o < nk; ++o) rank += int(better(rz[wave][o], rid[wave][o], v, id));
         if (rank < k) {
           const float lp = (v - m) / a.tau - log_s;
@@ -124,11 +126,32 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
     }
   }
   __syncthreads();
-  auto key_of = [&](int c) {
-    const int j = c / k;
+  auto score_at = [&](int j, int r) {   // s of row j's candidate r, as in the keys below
     const float sp = a.parent_score ? a.parent_score[int64_t(q) * a.parent_stride + j] : 0.f;
-    const float sc = (sp + c_logp[c]) + a.beta;
-    return (uint64_t(score_desc_key(sc)) << 32) | (uint32_t(j) << 20) | uint32_t(c_ids[c]);
+    return (sp + c_logp[j * k + r]) + a.beta;
+  };
+  // With rows in rank order, a row's candidates from position n_keep on have
+  // scores <= its candidate n_keep's; if that is strictly below its candidate
+  // n_keep - 1's in every row, each of them is beaten by n_keep children of its
+  // own parent and can never be kept, so only the first n_keep of each row
+  // compete.  (Equal fp32 scores order by token, not by rank, so a row with
+  // such a tie keeps every candidate in play.)
+  int kk = k;
+  if (a.rows_ranked && a.n_keep < k) {
+    __shared__ int tie;
+    if (threadIdx.x == 0) tie = 0;
+    __syncthreads();
+    for (int j = threadIdx.x; j < np; j += blockDim.x)
+      if (!(score_at(j, a.n_keep - 1) > score_at(j, a.n_keep))) tie = 1;
+    __syncthreads();
+    if (!tie) kk = a.n_keep;
+  }
+  n = np * kk;
+  auto key_of = [&](int c) {
+    const int j = c / kk;
+    const int r = c - j * kk;
+    const float sc = score_at(j, r);
+    return (uint64_t(score_desc_key(sc)) << 32) | (uint32_t(j) << 20) | uint32_t(c_ids[j * k + r]);
   };
   const uint64_t* kept = keys;   // the n_keep best, in order
   if (n <= int(blockDim.x)) {
@@ -139,8 +162,18 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
     keys[threadIdx.x] = mine;
     __syncthreads();
     int rank = 0;
-    if (int(threadIdx.x) < n)
-      for (int j = 0; j < n; ++j) rank += int(keys[j] < mine);
+    if (int(threadIdx.x) < n) {
+      // 16-byte reads of key pairs, unrolled so that the reads overlap
+      typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+      const u64x2* kp = reinterpret_cast<const u64x2*>(keys);
+      const int n2 = n >> 1;
+#pragma unroll 8
+      for (int j = 0; j < n2; ++j) {
+        const u64x2 kk = kp[j];
+        rank += int(kk.x < mine) + int(kk.y < mine);
+      }
+      if (n & 1) rank += int(keys[n - 1] < mine);
+    }
     __syncthreads();
     // n <= 1024 and n_keep <= n: the ranked copy sits above the keys
     if (int(threadIdx.x) < n && rank < a.n_keep) keys[kSortMax / 2 + rank] = mine;
@@ -321,7 +354,8 @@ hipError_t launch_select_level(const LevelArgs& a, hipStream_t s) {
   // state slices: enough blocks to spread the state rows over the chip
   const int S = a.state ? std::max(1, std::min(a.n_keep, (256 + a.batch - 1) / a.batch)) : 1;
   const dim3 grid(unsigned(a.batch) * unsigned(S));
-  switch (topk_bucket(a.k)) {
+  // the top-k bucket only sizes the segment merge; without one the widest block serves
+  switch ((a.shared_k > 0 || a.nseg <= 1) ? 1 : topk_bucket(a.k)) {
     case 1: hipLaunchKernelGGL((select_level<1>), grid, dim3(select_threads<1>()), 0, s, a, S); break;
     case 2: hipLaunchKernelGGL((select_level<2>), grid, dim3(select_threads<2>()), 0, s, a, S); break;
     case 4: hipLaunchKernelGGL((select_level<4>), grid, dim3(select_threads<4>()), 0, s, a, S); break;
