@@ -47,6 +47,15 @@ Readings where the paper is silent (each is listed in the design doc):
     are preferred under ties";
   * the root is not a node of T and does not count toward B.
 
+The node-at-a-time baseline DARTree replaces (Sec. 3.1, "Seq. Correction w.
+Heap" of Table 2) is ``sequential_heap``: a max-heap over candidate prefixes;
+the head is run on the root and its k best children are pushed; each pop adds
+the best prefix to the tree, runs the head on it under its own token history
+(state from its parent's t and its token) and pushes its k best children,
+until B prefixes have been popped.  Pop order: (s desc, depth asc, parent node
+asc, child rank asc) - depth asc again prefers ancestors, the last two fields
+make the order total.  The popped prefixes are emitted like DARTree's tree.
+
 Parity status: every function here is pinned by the CPU tests (brute force,
 Lemma 1's heap, the sequential-heap algorithm of Sec. 3.1, special cases and
 library routines).  The head form itself is this oracle's reading of a passage
@@ -55,6 +64,7 @@ the paper leaves open; its arithmetic is pinned by scalar-loop evaluation only.
 from __future__ import annotations
 
 import dataclasses
+import heapq
 from typing import Callable, Optional
 
 import numpy as np
@@ -374,3 +384,130 @@ def emit_batch(st: Supertree, kept_sets=None) -> Tree:
     return Tree(tokens=np.stack([o[0] for o in outs]), parents=np.stack([o[1] for o in outs]),
                 depths=np.stack([o[2] for o in outs]), scores=np.stack([o[3] for o in outs]),
                 mask=np.stack([o[4] for o in outs]), num_nodes=np.array([o[5] for o in outs], np.int32))
+
+
+# ----------------------------------------------------------------------------
+# Sequential correction with a best-first heap (Sec. 3.1; Table 2's baseline)
+# ----------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class Expansion:
+    """The head's output on one expanded node (its children's distribution)."""
+
+    lse: float                 # log sum_v exp(z_v / tau) of the node's row
+    cand_ids: np.ndarray       # [k] its k best children, (z desc, id asc)
+    cand_logp: np.ndarray      # [k] their log q~
+    cset: Optional[np.ndarray] = None   # C_d scored for it (candidates > 0)
+
+
+@dataclasses.dataclass
+class HeapRun:
+    """One request's node-at-a-time construction.  Node 0 is the root, node
+    i >= 1 the i-th popped prefix."""
+
+    token: list       # token of node i (-1 for the root)
+    parent: list      # node index of its parent (-1 for the root)
+    depth: list       # 0 for the root
+    score: list       # s_beta(u) (0 for the root)
+    expansions: dict  # node index -> Expansion, for every node the head ran on
+
+
+def heap_entry(score: float, depth: int, parent: int, rank: int, token: int) -> tuple:
+    """Ordering key of a candidate prefix in the heap; the smallest key is
+    popped first: (s desc, depth asc, parent node asc, child rank asc)."""
+    return (-score, depth, parent, rank, token)
+
+
+def sequential_heap(dec: Decoded, requests=None, choose_topk: Optional[Callable] = None,
+                    choose_pop: Optional[Callable] = None,
+                    adopt_states: Optional[Callable] = None) -> list:
+    """Sec. 3.1's exact best-first construction with the correction head run
+    once per popped prefix (B pops per request).
+
+    ``choose_topk(req, node, d, z_row, logp_row, k)`` may replace a node's
+    k best children, ``choose_pop(req, step, heap)`` the index of the heap
+    item popped at a step (items are (key, (score, depth, parent, token))), and ``adopt_states(req, node, r)`` a popped node's
+    state (to follow another implementation's choices and rounding).
+    """
+    p = dec.p
+    tau, e, beta = p.tau, p.embed_scale, p.depth_bonus
+    k = min(p.branch, p.vocab)
+    reqs = range(p.batch) if requests is None else requests
+    runs = []
+    for b in reqs:
+        run = HeapRun(token=[-1], parent=[-1], depth=[0], score=[0.0], expansions={})
+        t_of = {}
+        heap: list = []
+
+        def expand(n: int, r: np.ndarray):
+            d = run.depth[n] + 1
+            t, a = head_features(r[None, :], dec.A, dec.H[b, d - 1], p.precision)
+            t_of[n] = t[0]
+            cset = None
+            if p.candidates > 0:
+                cset = candidate_set(dec.Lb[b, d - 1], p.candidates)
+                z = candidate_logits(a, dec.U, dec.Lb[b, d - 1], cset)[0]
+            else:
+                z = vocab_logits(a, dec.U, dec.Lb[b, d - 1])[0]
+            lp = log_softmax(z[None, :], tau)[0]
+            m = z.max()
+            lse = m / tau + np.log(np.exp((z - m) / tau).sum())
+            ids = (np.asarray(choose_topk(b, n, d, z, lp, k), np.int64) if choose_topk
+                   else topk_ids(z, k))
+            run.expansions[n] = Expansion(lse=float(lse), cand_ids=ids, cand_logp=lp[ids], cset=cset)
+            for rank, v in enumerate(ids):
+                sc = float(path_score(run.score[n], lp[v], beta))
+                heapq.heappush(heap, (heap_entry(sc, d, n, rank, int(v)), (sc, d, n, int(v))))
+
+        expand(0, dec.r0[b])
+        while heap and len(run.token) - 1 < p.budget:
+            step = len(run.token) - 1
+            i = choose_pop(b, step, heap) if choose_pop else 0
+            entry = heap[i]
+            heap[i] = heap[-1]
+            heap.pop()
+            heapq.heapify(heap)
+            sc, d, par, v = entry[1]
+            n = len(run.token)
+            run.token.append(v)
+            run.parent.append(par)
+            run.depth.append(d)
+            run.score.append(sc)
+            if d < p.depth and len(run.token) - 1 < p.budget:   # the last pop's children are never popped
+                r = child_states(t_of[par][None, :], dec.U[v][None, :], e, p.precision)[0]
+                if adopt_states is not None:
+                    r = adopt_states(b, n, r)
+                expand(n, r)
+        runs.append(run)
+    return runs
+
+
+def heap_levels(run: HeapRun):
+    """The popped prefixes as levels (depth by depth, in pop order) and the
+    (depth, slot) list of every node, for ``emit_tree``."""
+    slot_of, by_depth = {}, {}
+    for n in range(1, len(run.token)):
+        lst = by_depth.setdefault(run.depth[n], [])
+        slot_of[n] = len(lst)
+        lst.append(n)
+    levels = []
+    for d in range(1, max(by_depth, default=0) + 1):
+        ns = by_depth[d]   # prefix-closed: every depth up to the deepest is present
+        levels.append(Level(token=np.array([run.token[n] for n in ns], np.int64),
+                            parent=np.array([slot_of[run.parent[n]] if d > 1 else 0 for n in ns], np.int64),
+                            score=np.array([run.score[n] for n in ns], np.float64)))
+    kept = [(run.depth[n], slot_of[n]) for n in range(1, len(run.token))]
+    return levels, kept
+
+
+def emit_heap(runs: list, budget: int) -> Tree:
+    outs = [emit_tree(*heap_levels(run), budget) for run in runs]
+    return Tree(tokens=np.stack([o[0] for o in outs]), parents=np.stack([o[1] for o in outs]),
+                depths=np.stack([o[2] for o in outs]), scores=np.stack([o[3] for o in outs]),
+                mask=np.stack([o[4] for o in outs]), num_nodes=np.array([o[5] for o in outs], np.int32))
+
+
+def sequential_heap_tree(dec: Decoded, requests=None) -> tuple[Tree, list]:
+    """Sec. 3.1's baseline end to end: B pops per request, emitted trees."""
+    runs = sequential_heap(dec, requests)
+    return emit_heap(runs, dec.p.budget), runs

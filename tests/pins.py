@@ -330,6 +330,127 @@ def pin_shared_full_vocabulary():
         assert set(lvl.token.tolist()) <= set(lvl.cset.tolist())
 
 
+# ---------------------------------------------------------------------------
+# Sequential correction with a best-first heap (Sec. 3.1; Table 2's baseline)
+# ---------------------------------------------------------------------------
+def run_heap(cfg, inputs=None):
+    inputs = inputs if inputs is not None else W.make_inputs(cfg)
+    tree, runs = R.sequential_heap_tree(R.prepare(inputs))
+    return inputs, tree, runs
+
+
+def pin_heap_brute_force():
+    """k = V: best-first pops over the untruncated prefix tree are the global
+    top-B over every prefix, each scored along its own path (scores never rise
+    along a path, so the B best prefixes are prefix-closed)."""
+    for seed, prec, T, B in ((60, W.FP32, 0.0, 11), (61, W.BF16, 0.0, 7), (62, W.FP32, 0.7, 30),
+                             (63, W.FP32, 0.0, 84)):
+        cfg = tiny(seed=seed, precision=prec, vocab=4, depth=3, branch=4, budget=B, temperature=T)
+        inp, tree, runs = run_heap(cfg)
+        want = I.brute_force(I.ScalarHead(inp, cfg), 0, B, cfg.depth_bonus)
+        _check_against_paths(tree, 0, want, B)
+
+
+def pin_heap_equals_wide_dartree():
+    """W >= B with the same cap k: the depth-wise supertree contains the heap's
+    tree (its top-B is prefix-closed and every member ranks within the top-W
+    of its depth), so DARTree's pruned tree is the heap's tree."""
+    for seed, prec, T, K in ((64, W.FP32, 0.0, 0), (65, W.BF16, 0.7, 0), (66, W.FP32, 0.0, 5)):
+        cfg = tiny(seed=seed, precision=prec, batch=2, vocab=9, depth=4, width=10, branch=3, budget=10,
+                   temperature=T, candidates=K)
+        inp, tree, runs = run_heap(cfg)
+        _, want, _ = run_oracle(cfg, inp)
+        for f in ("tokens", "parents", "depths", "mask", "num_nodes"):
+            assert np.array_equal(getattr(tree, f), getattr(want, f)), f
+        assert np.allclose(tree.scores, want.scores, atol=1e-9, equal_nan=True)
+
+
+def pin_heap_scalar():
+    """The node-at-a-time construction against a scalar-loop implementation
+    that orders equal scores by token path (W < B: no DARTree equivalent)."""
+    for seed, prec in ((67, W.FP32), (68, W.BF16)):
+        cfg = tiny(seed=seed, precision=prec, vocab=7, depth=4, width=2, branch=3, budget=9)
+        inp, tree, runs = run_heap(cfg)
+        want = I.sequential_heap(I.ScalarHead(inp, cfg), 0, cfg.budget, cfg.branch, cfg.depth_bonus)
+        _check_against_paths(tree, 0, want, cfg.budget)
+    cfg = tiny(seed=69, precision=W.BF16, vocab=9, depth=3, width=2, branch=2, candidates=4, budget=7)
+    inp, tree, runs = run_heap(cfg)
+    want = I.sequential_heap_shared(I.ScalarHead(inp, cfg), 0, cfg.budget, cfg.branch, cfg.depth_bonus,
+                                    cfg.candidates)
+    _check_against_paths(tree, 0, want, cfg.budget)
+
+
+def pin_heap_zeroed_correction():
+    """U = 0, k = V: the heap's tree is DDTree's optimum, the top-B prefixes by
+    factorised marginal mass plus beta*d (Sec. 2.3)."""
+    for T, K in ((0.0, 0), (0.7, 0), (0.0, 3)):
+        cfg = tiny(seed=70, vocab=5, depth=3, branch=K or 5, candidates=K, budget=12, temperature=T)
+        inp = W.make_inputs(cfg)
+        inp.U[:] = 0
+        inp, tree, runs = run_heap(cfg, inp)
+        want, _ = I.marginal_top_b(inp.Lb[0], T or 1.0, cfg.depth, cfg.budget, cfg.depth_bonus, K=K or None)
+        _check_against_paths(tree, 0, want, cfg.budget)
+
+
+def pin_heap_shared_brute_force():
+    """Shared sets with k = K: the global top-B over C_1 x ... x C_L."""
+    cfg = tiny(seed=71, precision=W.BF16, vocab=7, depth=3, branch=3, candidates=3, budget=10)
+    inp, tree, runs = run_heap(cfg)
+    want = I.brute_force_shared(I.ScalarHead(inp, cfg), 0, cfg.budget, cfg.depth_bonus, cfg.candidates)
+    _check_against_paths(tree, 0, want, cfg.budget)
+
+
+def pin_heap_chain():
+    """k = 1: every pop exposes one child, so the tree is the first min(B, L)
+    prefixes of the corrected greedy chain."""
+    for B in (2, 16):
+        cfg = tiny(seed=72, vocab=9, depth=5, branch=1, budget=B)
+        inp, tree, runs = run_heap(cfg)
+        path, scores = I.greedy_chain(I.ScalarHead(inp, cfg), 0, cfg.depth_bonus)
+        want = {path[:d]: scores[d - 1] for d in range(1, min(B, len(path)) + 1)}
+        _check_against_paths(tree, 0, want, B)
+
+
+def pin_heap_ties_prefer_ancestors():
+    """Exact ties across depths (U = 0, beta = 0, a probability-1 token at
+    depth 2): a depth-1 prefix and a depth-2 prefix share a score, and the
+    shallower one is popped first, as the global order (s desc, depth asc,
+    path asc) requires."""
+    cfg = tiny(seed=73, vocab=4, depth=3, branch=4, budget=1, depth_bonus=0.0)
+    inp = W.make_inputs(cfg)
+    inp.U[:] = 0
+    inp.Lb[:] = 0
+    inp.Lb[0, 0, [0, 1]] = 1000.0   # two equally likely tokens: log q = -log 2 each
+    inp.Lb[0, 1, 2] = 1000.0        # one certain token: log q = 0
+    inp.Lb[0, 2, [1, 3]] = 1000.0
+    head = I.ScalarHead(inp, cfg)
+    for B in range(1, 10):
+        c = cfg.replace(budget=B)
+        i2 = W.Inputs(cfg=c, Lb=inp.Lb, H=inp.H, r0=inp.r0, A=inp.A, U=inp.U)
+        _, tree, runs = run_heap(c, i2)
+        want = I.brute_force(head, 0, B, 0.0)
+        _check_against_paths(tree, 0, want, B)
+
+
+def pin_heap_invariants():
+    """Pops come in non-increasing score order (children never outscore their
+    parent); every node's parent was popped before it at depth - 1; every
+    popped node below depth L except the last pop was expanded; the pop count
+    is min(B, size of the k-capped tree)."""
+    for B, L in ((40, 4), (200, 3)):
+        cfg = tiny(seed=74, batch=2, vocab=8, depth=L, branch=3, budget=B)
+        inp, tree, runs = run_heap(cfg)
+        for run in runs:
+            n = len(run.token) - 1
+            assert n == min(B, sum(3 ** d for d in range(1, L + 1)))
+            assert all(run.score[i + 1] <= run.score[i] + 1e-12 for i in range(1, n))
+            for i in range(1, n + 1):
+                assert 0 <= run.parent[i] < i and run.depth[i] == run.depth[run.parent[i]] + 1
+                assert run.score[i] <= run.score[run.parent[i]] + cfg.depth_bonus + 1e-12
+            want_expanded = {0} | {i for i in range(1, n) if run.depth[i] < L}
+            assert set(run.expansions) == want_expanded
+
+
 PINS = [
     pin_shared_brute_force, pin_shared_sequential_heap, pin_shared_zeroed_correction,
     pin_shared_full_vocabulary,
@@ -337,4 +458,6 @@ PINS = [
     pin_head_scalar, pin_prune_is_heap, pin_prune_ties_prefer_ancestors, pin_brute_force, pin_sequential_heap,
     pin_zeroed_correction, pin_greedy_chain, pin_whole_supertree, pin_monotone_scores,
     pin_batch_independence, pin_vocab_permutation,
+    pin_heap_brute_force, pin_heap_equals_wide_dartree, pin_heap_scalar, pin_heap_zeroed_correction,
+    pin_heap_shared_brute_force, pin_heap_chain, pin_heap_ties_prefer_ancestors, pin_heap_invariants,
 ]

@@ -13,7 +13,7 @@ from tests import pins
 _orig = {name: getattr(R, name) for name in (
     "head_features", "vocab_logits", "log_softmax", "topk_ids", "select_level",
     "child_states", "path_score", "prune", "emit_tree", "rnd_bf16", "candidate_set",
-    "candidate_logits")}
+    "candidate_logits", "heap_entry")}
 
 
 def _head_transposed(r, A, H_d, precision):
@@ -121,7 +121,22 @@ def _cand_logits_no_base(a, U, Lb_d, cset):
     return z
 
 
+def _heap_breadth_first(score, depth, parent, rank, token):
+    return (depth, parent, rank, token)
+
+
+def _heap_prefers_descendants(score, depth, parent, rank, token):
+    return (-score, -depth, parent, rank, token)
+
+
+def _heap_min_first(score, depth, parent, rank, token):
+    return (score, depth, parent, rank, token)
+
+
 MUTANTS = {
+    "heap_breadth_first": ("heap_entry", _heap_breadth_first),
+    "heap_prefers_descendants": ("heap_entry", _heap_prefers_descendants),
+    "heap_pops_worst": ("heap_entry", _heap_min_first),
     "cset_lowest_values": ("candidate_set", _cset_lowest),
     "cset_first_ids": ("candidate_set", _cset_id_order),
     "cand_logits_full_vocab": ("candidate_logits", _cand_logits_full_vocab),
