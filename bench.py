@@ -119,6 +119,30 @@ def calibrate(torch, dev, U, stream, reps: int = 5) -> dict:
             "mfma_TFs": flops / mfma_us / 1e6}
 
 
+def time_heap(torch, cfg, di, stream, steps: int, timed) -> dict:
+    """The node-at-a-time baseline (Sec. 3.1, "Seq. Correction w. Heap" of
+    Table 2) on the same inputs: one round is B pops, each after a head,
+    logits and softmax pass on the popped prefix, captured in a HIP graph."""
+    p = D.Params.of(cfg)
+    dev = di.U.device
+    ws = D.alloc_heap_workspace(p, dev)
+    out = D.DeviceTree.alloc(cfg.batch, cfg.budget, dev)
+    for _ in range(2):
+        D.build_tree_heap(p, di, ws, out)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        D.build_tree_heap(p, di, ws, out)
+    graph.replay()
+    torch.cuda.synchronize()
+    per_ms, total_ms, _ = timed(graph.replay, steps)
+    pops = int(out.num_nodes.max().item())
+    del graph
+    return {"us_per_round": total_ms * 1e3 / steps, "us_per_round_p50": float(np.percentile(per_ms, 50) * 1e3),
+            "steps": steps, "pops_per_round": pops, "head_evaluations_per_round": cfg.budget,
+            "timing": "HIP graph replay of dartree_build_tree_heap"}
+
+
 def cpu_baseline(cfg, inputs, budget_s: float = 20.0) -> dict:
     """The oracle (fp64 NumPy) on the host cores, on the first D depths of
     request 0 with D chosen to take ~budget_s; scaled to us per full round."""
@@ -296,6 +320,16 @@ def main() -> int:
     per_row = getattr(cfg, "candidates", 0) or cfg.vocab   # entries scored per parent row
     vocab_entries = cfg.batch * sum(sizes[d - 1] for d in range(1, cfg.depth + 1)) * per_row
 
+    # the node-at-a-time baseline DARTree's depth-wise schedule replaces,
+    # a few rounds (each is B head evaluations)
+    heap = None
+    if cfg.budget <= D.MAX_HEAP_BUDGET:
+        heap_steps = max(3, min(K, int(2e6 / max(us_round * cfg.budget / cfg.depth, 1.0))))
+        log(f"sequential heap: {heap_steps} rounds")
+        heap = time_heap(torch, cfg, di, stream, heap_steps, timed)
+        heap["vs_dartree"] = heap["us_per_round"] / us_round
+        log(f"  {heap['us_per_round']:.1f} us/round, {heap['vs_dartree']:.2f}x DARTree's round")
+
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle on host cores)")
@@ -320,7 +354,8 @@ def main() -> int:
         "projection_tflops": proj_flops,
         "projection_mfma_frac": proj_flops / MFMA_BF16_PEAK_TFS,
         "kernels": kernels, "instrumented_us_per_round": instrumented_us,
-        "roofline": roof, "lse_topk_roofline": lse_roof, "calibration": cal, "cpu_baseline": cpu,
+        "roofline": roof, "lse_topk_roofline": lse_roof, "calibration": cal, "sequential_heap": heap,
+        "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
     return 0

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define DARTREE_ABI_VERSION 3
+#define DARTREE_ABI_VERSION 4
 
 /* Limits of this implementation (calls beyond them return
  * DARTREE_ERR_UNSUPPORTED). */
@@ -61,6 +61,7 @@ extern "C" {
 #define DARTREE_MAX_BRANCH 32            /* k over the full vocabulary */
 #define DARTREE_MAX_CANDIDATES 256       /* K of a shared candidate set (k <= K) */
 #define DARTREE_MAX_SORT 4096            /* n_{d-1}*k candidates, |S| nodes, B */
+#define DARTREE_MAX_HEAP_BUDGET 1024     /* B of the sequential heap (pops per round) */
 
 typedef enum dartree_status {
   DARTREE_OK = 0,
@@ -255,6 +256,53 @@ dartree_status dartree_select_topw(int32_t batch, int32_t n_parent, int32_t k, i
 dartree_status dartree_prune_levels(const dartree_params* p, const int32_t* tokens,
                                     const int32_t* parents, const float* scores,
                                     const dartree_tree* out, hipStream_t stream);
+
+/* ---- the node-at-a-time baseline ------------------------------------------
+ * Sequential correction with a best-first heap (Sec. 3.1; "Seq. Correction
+ * w. Heap" of Table 2), the exact construction DARTree's depth-wise schedule
+ * replaces.  Per request: the head is run on the root and its k best children
+ * (by z desc, id asc) are candidates; then B times: pop the best candidate
+ * prefix by (s desc, depth asc, parent's pop index asc, child rank asc), add
+ * it to the tree and, if its depth is below L, run the head on it under its
+ * own token history (r = bf16(tanh(t_parent + e U[token])), then t, a, z,
+ * log q~ as in Algorithm 1's loop body, over the full vocabulary or over C_d
+ * when candidates > 0) and make its k best children candidates.  The head
+ * therefore runs once per pop, on one prefix per request at a time.  Scores,
+ * precision, temperature and the shared sets follow dartree_params as above;
+ * `width` is not used.  The popped prefixes (min(B, size of the k-capped
+ * prefix tree) of them, prefix-closed) are emitted as dartree_tree.
+ * B <= DARTREE_MAX_HEAP_BUDGET. */
+
+/* Device destination of dartree_export_heap.  Slot i of request q is its i-th
+ * popped prefix (slot 0: the root); step i ran the head on slot i.  Any
+ * member may be NULL (not copied). */
+typedef struct dartree_heap_trace {
+  int32_t* tokens;     /* [b][B+1] token of slot i (-1 for the root) */
+  int32_t* parents;    /* [b][B+1] slot of its parent (-1 for the root) */
+  int32_t* depths;     /* [b][B+1] depth (0 for the root) */
+  float* scores;       /* [b][B+1] s_beta (0 for the root) */
+  int32_t* num_popped; /* [b] prefixes popped */
+  float* lse;          /* [B][b] log sum_v exp(z_v / tau) of slot i's row (slots the head ran on) */
+  float* cand_logp;    /* [B][b][k] log q~ of slot i's k best children, best first */
+  int32_t* cand_ids;   /* [B][b][k] their token ids */
+  void* states;        /* act [B+1][b][h] r of slot i (slots 1.. the head ran on) */
+  int32_t* csets;      /* [b][L][K] shared candidate sets (candidates > 0 only) */
+} dartree_heap_trace;
+
+/* Bytes of device workspace for dartree_build_tree_heap (host only). */
+dartree_status dartree_heap_workspace_size(const dartree_params* p, size_t* bytes);
+
+/* One round of the sequential heap for every request, enqueued on `stream`
+ * as 4 launches per pop (3 with shared candidate sets, plus the sets once)
+ * and one emission; no host synchronisation, so the round can be captured in
+ * a graph.  ws: device, 256-byte aligned, >= dartree_heap_workspace_size. */
+dartree_status dartree_build_tree_heap(const dartree_params* p, const dartree_inputs* in, void* ws,
+                                       size_t ws_bytes, const dartree_tree* out, hipStream_t stream);
+
+/* Copy the pops, the per-step children and states of the last
+ * dartree_build_tree_heap on `ws` into the caller's buffers (for inspection). */
+dartree_status dartree_export_heap(const dartree_params* p, const void* ws, size_t ws_bytes,
+                                   const dartree_heap_trace* dst, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -81,10 +81,11 @@ Layout layout_of(const dartree_params& p, const Shape& s) {
   return l;
 }
 
-dartree_status validate(const dartree_params* p) {
+// Checks shared by the depth-wise construction and the sequential heap
+// (which does not use the width).
+dartree_status validate_common(const dartree_params* p) {
   if (!p) return DARTREE_ERR_INVALID_ARG;
-  if (p->batch < 1 || p->vocab < 1 || p->hidden < 1 || p->depth < 1 || p->width < 1 || p->branch < 1 ||
-      p->budget < 1)
+  if (p->batch < 1 || p->vocab < 1 || p->hidden < 1 || p->depth < 1 || p->branch < 1 || p->budget < 1)
     return DARTREE_ERR_INVALID_ARG;
   if (p->branch > p->vocab) return DARTREE_ERR_INVALID_ARG;
   if (p->candidates < 0) return DARTREE_ERR_INVALID_ARG;
@@ -92,14 +93,20 @@ dartree_status validate(const dartree_params* p) {
   if (p->precision != DARTREE_FP32 && p->precision != DARTREE_BF16) return DARTREE_ERR_INVALID_ARG;
   if (!isfinite(p->temperature) || p->temperature < 0.f) return DARTREE_ERR_INVALID_ARG;
   if (!isfinite(p->depth_bonus) || p->depth_bonus > 0.f) return DARTREE_ERR_INVALID_ARG;
-  if (p->vocab > DARTREE_MAX_VOCAB || p->depth > DARTREE_MAX_DEPTH || p->width > DARTREE_MAX_WIDTH ||
-      p->budget > DARTREE_MAX_SORT)
-    return DARTREE_ERR_UNSUPPORTED;
+  if (p->vocab > DARTREE_MAX_VOCAB || p->depth > DARTREE_MAX_DEPTH) return DARTREE_ERR_UNSUPPORTED;
   if (p->candidates == 0 && p->branch > DARTREE_MAX_BRANCH) return DARTREE_ERR_UNSUPPORTED;
   if (p->candidates > 0 &&
       (p->candidates > DARTREE_MAX_CANDIDATES || !candidate_sets_supported(p->vocab, p->candidates)))
     return DARTREE_ERR_UNSUPPORTED;
   if (p->precision == DARTREE_BF16 && p->hidden % 64 != 0) return DARTREE_ERR_UNSUPPORTED;
+  return DARTREE_OK;
+}
+
+dartree_status validate(const dartree_params* p) {
+  dartree_status v = validate_common(p);
+  if (v != DARTREE_OK) return v;
+  if (p->width < 1) return DARTREE_ERR_INVALID_ARG;
+  if (p->width > DARTREE_MAX_WIDTH || p->budget > DARTREE_MAX_SORT) return DARTREE_ERR_UNSUPPORTED;
   const Shape s = shape_of(*p);
   if (s.max_cand > DARTREE_MAX_SORT || s.total > DARTREE_MAX_SORT) return DARTREE_ERR_UNSUPPORTED;
   // row counts and element offsets must stay within 32-bit grid/row indexing
@@ -184,7 +191,7 @@ dartree_status expand_shared(const dartree_params& p, const dartree_inputs& in, 
   tm.mark(tb + DARTREE_KERNEL_LSE, 1);
   tm.mark(tb + DARTREE_KERNEL_LOGITS, 0);
   err = launch_shared_logits(p.precision, int(b), int(np), K, int(h), a, in.head_U,
-                             in.drafter_logits + size_t(d - 1) * V, L * V, csets + (d - 1) * K, L * K, z, st);
+                             in.drafter_logits + size_t(d - 1) * V, L * V, csets + (d - 1) * K, L * K, nullptr, z, st);
   tm.mark(tb + DARTREE_KERNEL_LOGITS, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
 
@@ -213,6 +220,7 @@ dartree_status expand_shared(const dartree_params& p, const dartree_inputs& in, 
   la.state = d < p.depth;
   la.precision = p.precision;
   la.hidden = int(h);
+  la.vocab = int(V);
   la.t = t;
   la.U = in.head_U;
   la.e = float(sqrt(double(p.hidden)));
@@ -315,6 +323,7 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   la.state = d < p.depth;
   la.precision = p.precision;
   la.hidden = int(h);
+  la.vocab = int(V);
   la.t = t;
   la.U = in.head_U;
   la.e = e;
@@ -324,6 +333,162 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   tm.mark(tb + DARTREE_KERNEL_SELECT, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
   return DARTREE_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Sequential correction with a best-first heap (Sec. 3.1)
+// ---------------------------------------------------------------------------
+dartree_status validate_heap(const dartree_params* p) {
+  dartree_status v = validate_common(p);
+  if (v != DARTREE_OK) return v;
+  if (p->budget > DARTREE_MAX_HEAP_BUDGET) return DARTREE_ERR_UNSUPPORTED;
+  if (int64_t(p->batch) * (p->budget + 1) > (int64_t(1) << 24)) return DARTREE_ERR_UNSUPPORTED;
+  return DARTREE_OK;
+}
+
+// Heap workspace (each region 256-byte aligned), S = b (B + 1) slots:
+//   slot_tok, slot_par, slot_depth, slot_next, slot_nch: i32 [b][B+1]
+//   slot_score: f32 [b][B+1]   cand_key: u64 [b][B+1]
+//   ch_lse: f32 [B][b]   ch_lp: f32 [B][b][k]   ch_tok: i32 [B][b][k]
+//   n_pop, gidx: i32 [b]
+//   r_store: act [B+1][b][h]   t_store: f32 [B][b][h]   a: act [b][h]
+//   z: f32 [b][V] (or [b][K])   k3: the row-split partials of b rows
+//   cset: i32 [b][L][K] and its scratch (K > 0)
+struct HeapLayout {
+  size_t slot_tok, slot_par, slot_depth, slot_score, slot_next, slot_nch, cand_key, ch_lse, ch_lp, ch_tok, n_pop,
+      gidx, r_store, t_store, a, z, k3, cset, cset_scratch, total;
+};
+
+HeapLayout heap_layout_of(const dartree_params& p) {
+  const size_t L = p.depth, b = p.batch, B = p.budget, k = p.branch, h = p.hidden, V = p.vocab;
+  const size_t K = size_t(p.candidates), ab = act_bytes(p.precision);
+  const size_t S = b * (B + 1);
+  HeapLayout l{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) { const size_t at = o; o = align_up(o + bytes); return at; };
+  l.slot_tok = take(S * 4);
+  l.slot_par = take(S * 4);
+  l.slot_depth = take(S * 4);
+  l.slot_score = take(S * 4);
+  l.slot_next = take(S * 4);
+  l.slot_nch = take(S * 4);
+  l.cand_key = take(S * 8);
+  l.ch_lse = take(B * b * 4);
+  l.ch_lp = take(B * b * k * 4);
+  l.ch_tok = take(B * b * k * 4);
+  l.n_pop = take(b * 4);
+  l.gidx = take(b * 4);
+  l.r_store = take((B + 1) * b * h * ab);
+  l.t_store = take(B * b * h * 4);
+  l.a = take(b * h * ab);
+  l.z = take(b * (K > 0 ? K : V) * 4);
+  l.k3 = take(K > 0 ? 0 : lse_topk_scratch_bytes(int64_t(b), V, int(k)));
+  l.cset = take(b * L * K * 4);
+  l.cset_scratch = take(K > 0 ? candidate_sets_scratch_bytes(int64_t(b) * L, V, int(K)) : 0);
+  l.total = o;
+  return l;
+}
+
+dartree_status check_heap_ws(const dartree_params& p, const void* ws, size_t ws_bytes, HeapLayout* out) {
+  const HeapLayout l = heap_layout_of(p);
+  if (!ws || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0 || ws_bytes < l.total) return DARTREE_ERR_WORKSPACE;
+  *out = l;
+  return DARTREE_OK;
+}
+
+// One round: B steps of (head, logits, softmax pass, heap step) on the prefix
+// popped at the previous step (step 0: the root), then the emission.  Step 0
+// reads depth 1's rows directly; later steps read the rows the heap step
+// chose (group index q L + depth of the popped prefix).
+dartree_status build_heap(const dartree_params& p, const dartree_inputs& in, void* ws, const HeapLayout& l,
+                          const dartree_tree& out, hipStream_t st) {
+  const int64_t b = p.batch, V = p.vocab, h = p.hidden, L = p.depth, B = p.budget, k = p.branch;
+  const int K = p.candidates;
+  const size_t ab = act_bytes(p.precision);
+  int32_t* gidx = at<int32_t>(ws, l.gidx);
+  int32_t* csets = at<int32_t>(ws, l.cset);
+  float* z = at<float>(ws, l.z);
+  void* a = at<char>(ws, l.a);
+  HeapArgs ha{};
+  ha.batch = int(b);
+  ha.budget = int(B);
+  ha.depth = int(L);
+  ha.k = int(k);
+  ha.vocab = int(V);
+  ha.shared_k = K;
+  ha.beta = p.depth_bonus;
+  ha.tau = p.temperature > 0.f ? p.temperature : 1.f;
+  ha.e = float(sqrt(double(p.hidden)));
+  ha.precision = p.precision;
+  ha.hidden = int(h);
+  ha.nseg = K > 0 ? 1 : lse_topk_segments(b, V);
+  ha.part = at<float>(ws, l.k3);
+  ha.zsh = z;
+  ha.cset = csets;
+  ha.slot_tok = at<int32_t>(ws, l.slot_tok);
+  ha.slot_par = at<int32_t>(ws, l.slot_par);
+  ha.slot_depth = at<int32_t>(ws, l.slot_depth);
+  ha.slot_score = at<float>(ws, l.slot_score);
+  ha.slot_next = at<int32_t>(ws, l.slot_next);
+  ha.slot_nch = at<int32_t>(ws, l.slot_nch);
+  ha.cand_key = at<uint64_t>(ws, l.cand_key);
+  ha.ch_lse = at<float>(ws, l.ch_lse);
+  ha.ch_lp = at<float>(ws, l.ch_lp);
+  ha.ch_tok = at<int32_t>(ws, l.ch_tok);
+  ha.n_pop = at<int32_t>(ws, l.n_pop);
+  ha.group_index = gidx;
+  ha.t_store = at<float>(ws, l.t_store);
+  ha.U = in.head_U;
+  ha.r_store = at<char>(ws, l.r_store);
+  hipError_t err = hipSuccess;
+  if (K > 0) {
+    err = launch_candidate_sets(in.drafter_logits, b * L, V, K, csets, at<char>(ws, l.cset_scratch), st);
+    if (err != hipSuccess) return DARTREE_ERR_HIP;
+  }
+  for (int64_t i = 0; i < B; ++i) {
+    const int32_t* gi = i == 0 ? nullptr : gidx;
+    ProjArgs head{};
+    head.precision = p.precision;
+    head.epilogue = EPI_HEAD;
+    head.M = b;
+    head.N = h;
+    head.K = h;
+    head.rows_per_group = 1;
+    head.x = i == 0 ? in.prefix_state : static_cast<const void*>(at<char>(ws, l.r_store) + size_t(i) * b * h * ab);
+    head.w = in.head_A;
+    head.bias_act = in.drafter_hidden;
+    head.bias_stride = i == 0 ? L * h : h;
+    head.group_index = gi;
+    head.out = at<float>(ws, l.t_store) + size_t(i) * b * h;
+    head.act_out = a;
+    if ((err = launch_project(head, st)) != hipSuccess) return DARTREE_ERR_HIP;
+    if (K > 0) {
+      err = launch_shared_logits(p.precision, int(b), 1, K, int(h), a, in.head_U, in.drafter_logits,
+                                 i == 0 ? L * V : V, csets, i == 0 ? L * K : K, gi, z, st);
+      if (err != hipSuccess) return DARTREE_ERR_HIP;
+    } else {
+      ProjArgs lg{};
+      lg.precision = p.precision;
+      lg.epilogue = EPI_LOGITS;
+      lg.M = b;
+      lg.N = V;
+      lg.K = h;
+      lg.rows_per_group = 1;
+      lg.x = a;
+      lg.w = in.head_U;
+      lg.bias_f32 = in.drafter_logits;
+      lg.bias_stride = i == 0 ? L * V : V;
+      lg.group_index = gi;
+      lg.out = z;
+      if ((err = launch_project(lg, st)) != hipSuccess) return DARTREE_ERR_HIP;
+      err = launch_lse_topk(z, b, V, int(k), ha.tau, ha.ch_lse + i * b, ha.ch_lp + i * b * k, ha.ch_tok + i * b * k,
+                            at<char>(ws, l.k3), false, st);
+      if (err != hipSuccess) return DARTREE_ERR_HIP;
+    }
+    ha.step = int(i);
+    if ((err = launch_heap_step(ha, st)) != hipSuccess) return DARTREE_ERR_HIP;
+  }
+  return hip_status(launch_heap_emit(ha, out, st));
 }
 
 }  // namespace
@@ -532,6 +697,48 @@ dartree_status dartree_prune_levels(const dartree_params* p, const int32_t* toke
   const Shape s = shape_of(*p);
   return hip_status(
       launch_prune_emit(p->batch, level_shape(*p, s), p->budget, tokens, parents, scores, *out, stream));
+}
+
+dartree_status dartree_heap_workspace_size(const dartree_params* p, size_t* bytes) {
+  if (!bytes) return DARTREE_ERR_INVALID_ARG;
+  const dartree_status v = validate_heap(p);
+  if (v != DARTREE_OK) return v;
+  *bytes = heap_layout_of(*p).total;
+  return DARTREE_OK;
+}
+
+dartree_status dartree_build_tree_heap(const dartree_params* p, const dartree_inputs* in, void* ws, size_t ws_bytes,
+                                       const dartree_tree* out, hipStream_t stream) {
+  dartree_status v = validate_heap(p);
+  if (v != DARTREE_OK) return v;
+  if ((v = check_inputs(in)) != DARTREE_OK) return v;
+  if ((v = check_tree(out)) != DARTREE_OK) return v;
+  HeapLayout l;
+  if ((v = check_heap_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
+  return build_heap(*p, *in, ws, l, *out, stream);
+}
+
+dartree_status dartree_export_heap(const dartree_params* p, const void* ws, size_t ws_bytes,
+                                   const dartree_heap_trace* dst, hipStream_t stream) {
+  dartree_status v = validate_heap(p);
+  if (v != DARTREE_OK) return v;
+  if (!dst) return DARTREE_ERR_INVALID_ARG;
+  HeapLayout l;
+  if ((v = check_heap_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
+  const size_t L = p->depth, b = p->batch, B = p->budget, k = p->branch, h = p->hidden;
+  const size_t S = b * (B + 1);
+  struct Item { void* to; size_t off; size_t bytes; } items[] = {
+      {dst->tokens, l.slot_tok, S * 4},      {dst->parents, l.slot_par, S * 4},
+      {dst->depths, l.slot_depth, S * 4},    {dst->scores, l.slot_score, S * 4},
+      {dst->num_popped, l.n_pop, b * 4},     {dst->lse, l.ch_lse, B * b * 4},
+      {dst->cand_logp, l.ch_lp, B * b * k * 4}, {dst->cand_ids, l.ch_tok, B * b * k * 4},
+      {dst->states, l.r_store, (B + 1) * b * h * act_bytes(p->precision)},
+      {p->candidates > 0 ? dst->csets : nullptr, l.cset, b * L * size_t(p->candidates) * 4},
+  };
+  for (const Item& it : items)
+    if (it.to && hipMemcpyAsync(it.to, at<char>(ws, it.off), it.bytes, hipMemcpyDeviceToDevice, stream) != hipSuccess)
+      return DARTREE_ERR_HIP;
+  return DARTREE_OK;
 }
 
 }  // extern "C"

@@ -37,7 +37,8 @@ __device__ __forceinline__ float score_from_desc_key(uint32_t k) {
 // ---------------------------------------------------------------------------
 
 // out[m][n] = epilogue(bias, sum_k x[m][k] * w[n][k]); row m belongs to group
-// m / rows_per_group, whose bias row starts at bias + group * bias_stride.
+// g = m / rows_per_group, whose bias row starts at bias + row(g) * bias_stride
+// with row(g) = group_index[g] (device memory) if group_index is set, else g.
 enum ProjEpilogue {
   EPI_LOGITS = 0,  // out (fp32) = acc + bias_f32
   EPI_HEAD = 1     // out (fp32) = acc ; act_out = act(tanh(acc + bias_act))
@@ -53,6 +54,7 @@ struct ProjArgs {
   const float* bias_f32; // EPI_LOGITS
   const void* bias_act;  // EPI_HEAD
   int64_t bias_stride;   // elements between consecutive group bias rows
+  const int32_t* group_index;  // optional device [M / rows_per_group]: bias row of each group
   float* out;            // fp32 [M][N]
   void* act_out;         // EPI_HEAD: act [M][N]
 };
@@ -91,7 +93,7 @@ struct LevelArgs {
   const int32_t* cset;            // request q's C_d at cset + q * cset_stride
   int64_t cset_stride;
   int state;                      // 0: no state update
-  int precision, hidden;
+  int precision, hidden, vocab;
   const float* t;                 // [rows][hidden]
   const void* U;                  // act [V][hidden]
   float e;
@@ -106,11 +108,12 @@ bool candidate_sets_supported(int64_t vocab, int K);
 hipError_t launch_candidate_sets(const float* logits, int64_t rows, int64_t vocab, int K, int32_t* ids,
                                  void* scratch, hipStream_t s);
 
-// Corrected logits over the shared set: z[q*np + j][c] = lb[q*lb_stride + C[c]]
-// + U[C[c]] . a[q*np + j], with C = cset + q * cset_stride.
+// Corrected logits over the shared set: z[q*np + j][c] = lb[g*lb_stride + C[c]]
+// + U[C[c]] . a[q*np + j], with C = cset + g * cset_stride and g =
+// group_index[q] (device memory) if group_index is set, else q.
 hipError_t launch_shared_logits(int precision, int batch, int np, int K, int hidden, const void* a, const void* U,
                                 const float* lb, int64_t lb_stride, const int32_t* cset, int64_t cset_stride,
-                                float* z, hipStream_t s);
+                                const int32_t* group_index, float* z, hipStream_t s);
 
 // Deferred top-B prune and tree emission (K6).
 struct LevelShape {
@@ -122,5 +125,40 @@ struct LevelShape {
 hipError_t launch_prune_emit(int batch, const LevelShape& shape, int budget,
                              const int32_t* lvl_tok, const int32_t* lvl_par,
                              const float* lvl_score, const dartree_tree& out, hipStream_t s);
+
+// Sequential correction with a best-first heap (the node-at-a-time
+// construction of Sec. 3.1): one step per pop, after the head, logits and
+// softmax pass of the node popped at the previous step (rows: one per
+// request).  Slot i of request q is the i-th popped prefix (slot 0 = the
+// root); per-slot arrays are [batch][budget + 1], per-step arrays
+// [budget][batch][...] (step i expands slot i).
+struct HeapArgs {
+  int batch, budget, depth, k, vocab;
+  int shared_k;                 // K > 0: the step's row holds logits over C_d in zsh
+  float beta, tau, e;
+  int precision, hidden;
+  int step;
+  int nseg;                     // > 1: merge the row records in `part`
+  const float* part;
+  const float* zsh;             // [batch][K]
+  const int32_t* cset;          // [batch][depth][K]
+  int32_t* slot_tok;
+  int32_t* slot_par;
+  int32_t* slot_depth;
+  float* slot_score;
+  int32_t* slot_next;           // rank of the slot's next child not yet popped
+  int32_t* slot_nch;            // number of children the slot was given
+  uint64_t* cand_key;           // heap key of the slot's next child (~0: none)
+  float* ch_lse;                // [budget][batch]
+  float* ch_lp;                 // [budget][batch][k], children in rank order
+  int32_t* ch_tok;
+  int32_t* n_pop;               // [batch] prefixes popped so far
+  int32_t* group_index;         // [batch] H / L^base / C_d row of the next expansion
+  const float* t_store;         // [budget][batch][hidden]: t of slot i
+  const void* U;
+  void* r_store;                // act [budget + 1][batch][hidden]: r of slot i
+};
+hipError_t launch_heap_step(const HeapArgs& a, hipStream_t s);
+hipError_t launch_heap_emit(const HeapArgs& a, const dartree_tree& out, hipStream_t s);
 
 }  // namespace dartree

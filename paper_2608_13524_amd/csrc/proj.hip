@@ -32,21 +32,28 @@ struct KArgs {
   int64_t bias_stride;
   const float* bias_f32;
   const void* bias_act;
+  const int32_t* group_index;
   float* out;
   void* act_out;
 };
 
+// first element of row m's bias row
+__device__ __forceinline__ int64_t bias_base(const KArgs& a, int m) {
+  const int g = m / a.rows_per_group;
+  return int64_t(a.group_index ? a.group_index[g] : g) * a.bias_stride;
+}
+
 template <int EPI, bool BF16>
 __device__ __forceinline__ void emit(const KArgs& a, int m, int n, float acc) {
-  const int64_t g = m / a.rows_per_group;
+  const int64_t bb = bias_base(a, m);
   const int64_t o = int64_t(m) * a.N + n;
   if constexpr (EPI == EPI_LOGITS) {
-    a.out[o] = acc + a.bias_f32[g * a.bias_stride + n];
+    a.out[o] = acc + a.bias_f32[bb + n];
   } else {
     a.out[o] = acc;
     float hb;
-    if constexpr (BF16) hb = bf16_to_f32(static_cast<const uint16_t*>(a.bias_act)[g * a.bias_stride + n]);
-    else hb = static_cast<const float*>(a.bias_act)[g * a.bias_stride + n];
+    if constexpr (BF16) hb = bf16_to_f32(static_cast<const uint16_t*>(a.bias_act)[bb + n]);
+    else hb = static_cast<const float*>(a.bias_act)[bb + n];
     const float v = tanhf(acc + hb);
     if constexpr (BF16) static_cast<uint16_t*>(a.act_out)[o] = f32_to_bf16(v);
     else static_cast<float*>(a.act_out)[o] = v;
@@ -83,15 +90,15 @@ __device__ __forceinline__ int lds_swizzle(int row) { return (row ^ (row >> 3)) 
 
 template <int EPI>
 __device__ __forceinline__ void emit4(const KArgs& a, int m, int n, f32x4 v, bool vec) {
-  const int64_t g = m / a.rows_per_group;
+  const int64_t bb = bias_base(a, m);
   const int64_t o = int64_t(m) * a.N + n;
   if (vec && n + 3 < a.N) {
     if constexpr (EPI == EPI_LOGITS) {
-      const f32x4 b = *reinterpret_cast<const f32x4*>(a.bias_f32 + g * a.bias_stride + n);
+      const f32x4 b = *reinterpret_cast<const f32x4*>(a.bias_f32 + bb + n);
       *reinterpret_cast<f32x4*>(a.out + o) = v + b;
     } else {
       typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
-      const u16x4 hb = *reinterpret_cast<const u16x4*>(static_cast<const uint16_t*>(a.bias_act) + g * a.bias_stride + n);
+      const u16x4 hb = *reinterpret_cast<const u16x4*>(static_cast<const uint16_t*>(a.bias_act) + bb + n);
       *reinterpret_cast<f32x4*>(a.out + o) = v;
       u16x4 r;
 #pragma unroll
@@ -510,6 +517,7 @@ hipError_t launch_project(const ProjArgs& p, hipStream_t s) {
   k.bias_stride = p.bias_stride;
   k.bias_f32 = p.bias_f32;
   k.bias_act = p.bias_act;
+  k.group_index = p.group_index;
   k.out = p.out;
   k.act_out = p.act_out;
   if (k.M <= 0 || k.N <= 0) return hipSuccess;

@@ -184,7 +184,7 @@ __global__ __launch_bounds__(1024) void shared_logits_bf16(int np, int K, int hi
                                                           const uint16_t* __restrict__ U,
                                                           const float* __restrict__ lb, int64_t lb_stride,
                                                           const int32_t* __restrict__ cset, int64_t cset_stride,
-                                                          float* z) {
+                                                          const int32_t* __restrict__ group_index, float* z) {
   constexpr int kWaves = 16;   // split h
   __shared__ f32x4 red[kWaves][kRowTiles][64];
   const int q = blockIdx.x / (ncb * nrb);
@@ -192,7 +192,8 @@ __global__ __launch_bounds__(1024) void shared_logits_bf16(int np, int K, int hi
   const int cb = rest / nrb, rb = rest % nrb;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
-  const int32_t* set = cset + q * cset_stride;
+  const int64_t g = group_index ? group_index[q] : q;   // L^base / C_d row of request q
+  const int32_t* set = cset + g * cset_stride;
   const int c = min(16 * cb + r16, K - 1);
   const uint16_t* urow = U + int64_t(set[c]) * hidden + kg * 8;
   const uint16_t* arow[kRowTiles];
@@ -220,7 +221,7 @@ __global__ __launch_bounds__(1024) void shared_logits_bf16(int np, int K, int hi
   for (int t = 0; t < kRowTiles; ++t) red[wave][t][lane] = acc[t];
   __syncthreads();
   if (wave != 0) return;
-  const float* lbq = lb + q * lb_stride;
+  const float* lbq = lb + g * lb_stride;
   // lane holds D[candidate 4 kg + i][node row r16] of each tile; waves summed in order
 #pragma unroll
   for (int t = 0; t < kRowTiles; ++t) {
@@ -242,17 +243,19 @@ __global__ __launch_bounds__(1024) void shared_logits_bf16(int np, int K, int hi
 __global__ __launch_bounds__(256) void shared_logits_f32(int np, int K, int hidden, int nblk, const float* __restrict__ a,
                                                          const float* __restrict__ U, const float* __restrict__ lb,
                                                          int64_t lb_stride, const int32_t* __restrict__ cset,
-                                                         int64_t cset_stride, float* z) {
+                                                         int64_t cset_stride, const int32_t* __restrict__ group_index,
+                                                         float* z) {
   const int q = blockIdx.x / nblk;
   const int e = (blockIdx.x % nblk) * blockDim.x + threadIdx.x;
   if (e >= np * K) return;
   const int j = e / K, cc = e % K;
-  const int tok = cset[q * cset_stride + cc];
+  const int64_t g = group_index ? group_index[q] : q;
+  const int tok = cset[g * cset_stride + cc];
   const float* ar = a + (int64_t(q) * np + j) * hidden;
   const float* ur = U + int64_t(tok) * hidden;
   float acc = 0.f;
   for (int k = 0; k < hidden; ++k) acc = fmaf(ar[k], ur[k], acc);
-  z[(int64_t(q) * np + j) * K + cc] = acc + lb[q * lb_stride + tok];
+  z[(int64_t(q) * np + j) * K + cc] = acc + lb[g * lb_stride + tok];
 }
 
 }  // namespace
@@ -278,18 +281,18 @@ hipError_t launch_candidate_sets(const float* logits, int64_t rows, int64_t voca
 
 hipError_t launch_shared_logits(int precision, int batch, int np, int K, int hidden, const void* a, const void* U,
                                 const float* lb, int64_t lb_stride, const int32_t* cset, int64_t cset_stride,
-                                float* z, hipStream_t s) {
+                                const int32_t* group_index, float* z, hipStream_t s) {
   if (batch <= 0) return hipSuccess;
   if (precision == DARTREE_BF16) {
     const int ncb = (K + 15) / 16, nrb = (np + 16 * kRowTiles - 1) / (16 * kRowTiles);
     hipLaunchKernelGGL(shared_logits_bf16, dim3(unsigned(batch * ncb * nrb)), dim3(1024), 0, s, np, K, hidden, ncb, nrb,
                        static_cast<const uint16_t*>(a), static_cast<const uint16_t*>(U), lb, lb_stride, cset,
-                       cset_stride, z);
+                       cset_stride, group_index, z);
   } else {
     const int nblk = (np * K + 255) / 256;
     hipLaunchKernelGGL(shared_logits_f32, dim3(unsigned(batch * nblk)), dim3(256), 0, s, np, K, hidden, nblk,
                        static_cast<const float*>(a), static_cast<const float*>(U), lb, lb_stride, cset, cset_stride,
-                       z);
+                       group_index, z);
   }
   return hipGetLastError();
 }

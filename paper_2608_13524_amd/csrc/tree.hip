@@ -199,7 +199,8 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
   const int h = a.hidden;
   for (int i = sl; i < a.n_keep; i += S) {
     const uint32_t lo = uint32_t(kept[i]);
-    const int64_t prow = rbase + (lo >> 20), tok = lo & 0xFFFFFu;
+    // an empty candidate (a row without finite values) is clamped into U
+    const int64_t prow = rbase + (lo >> 20), tok = min(int(lo & 0xFFFFFu), a.vocab - 1);
     const int64_t c = int64_t(q) * a.n_keep + i;
     const float* tp = a.t + prow * h;
     if (a.precision == DARTREE_BF16) {

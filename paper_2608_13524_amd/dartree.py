@@ -25,6 +25,7 @@ MAX_WIDTH = 2048
 MAX_BRANCH = 32
 MAX_CANDIDATES = 256
 MAX_SORT = 4096
+MAX_HEAP_BUDGET = 1024
 
 SYMBOLS = [
     "dartree_abi_version", "dartree_status_string", "dartree_validate",
@@ -32,6 +33,7 @@ SYMBOLS = [
     "dartree_build_tree", "dartree_build_tree_timed", "dartree_export_supertree", "dartree_export_states", "dartree_project",
     "dartree_lse_topk_workspace_size", "dartree_lse_topk", "dartree_select_topw",
     "dartree_prune_levels", "dartree_candidate_sets_workspace_size", "dartree_candidate_sets",
+    "dartree_heap_workspace_size", "dartree_build_tree_heap", "dartree_export_heap",
     "dartree_calib_read", "dartree_calib_copy", "dartree_calib_mfma",
 ]
 CALIB_SINK_FLOATS = 4096
@@ -72,6 +74,13 @@ class TreeC(ctypes.Structure):
 class SupertreeC(ctypes.Structure):
     _fields_ = [("tokens", ctypes.c_void_p), ("parents", ctypes.c_void_p), ("scores", ctypes.c_void_p),
                 ("lse", ctypes.c_void_p), ("cand_logp", ctypes.c_void_p), ("cand_ids", ctypes.c_void_p),
+                ("csets", ctypes.c_void_p)]
+
+
+class HeapTraceC(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.c_void_p), ("parents", ctypes.c_void_p), ("depths", ctypes.c_void_p),
+                ("scores", ctypes.c_void_p), ("num_popped", ctypes.c_void_p), ("lse", ctypes.c_void_p),
+                ("cand_logp", ctypes.c_void_p), ("cand_ids", ctypes.c_void_p), ("states", ctypes.c_void_p),
                 ("csets", ctypes.c_void_p)]
 
 
@@ -116,6 +125,9 @@ def lib() -> ctypes.CDLL:
     L.dartree_prune_levels.argtypes = [P, vp, vp, vp, ctypes.POINTER(TreeC), vp]
     L.dartree_candidate_sets_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(sz)]
     L.dartree_candidate_sets.argtypes = [vp, i32, i32, i32, vp, vp, sz, vp]
+    L.dartree_heap_workspace_size.argtypes = [P, ctypes.POINTER(sz)]
+    L.dartree_build_tree_heap.argtypes = [P, ctypes.POINTER(InputsC), vp, sz, ctypes.POINTER(TreeC), vp]
+    L.dartree_export_heap.argtypes = [P, vp, sz, ctypes.POINTER(HeapTraceC), vp]
     L.dartree_calib_read.argtypes = [vp, sz, vp, vp]
     L.dartree_calib_copy.argtypes = [vp, vp, sz, vp]
     L.dartree_calib_mfma.argtypes = [i32, i32, vp, vp]
@@ -162,6 +174,12 @@ def validate(p: Params) -> int:
 def workspace_size(p: Params) -> int:
     n = ctypes.c_size_t(0)
     _check(lib().dartree_workspace_size(ctypes.byref(p), ctypes.byref(n)), "dartree_workspace_size")
+    return n.value
+
+
+def heap_workspace_size(p: Params) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().dartree_heap_workspace_size(ctypes.byref(p), ctypes.byref(n)), "dartree_heap_workspace_size")
     return n.value
 
 
@@ -264,10 +282,49 @@ class DeviceSupertree:
                 if getattr(self, f.name) is not None}
 
 
+@dataclasses.dataclass
+class DeviceHeapTrace:
+    tokens: object
+    parents: object
+    depths: object
+    scores: object
+    num_popped: object
+    lse: object
+    cand_logp: object
+    cand_ids: object
+    states: object = None   # act [B+1][b][h] (int16 bit patterns in bf16 mode)
+    csets: object = None    # [b][L][K] (candidates > 0)
+
+    def c(self) -> HeapTraceC:
+        return HeapTraceC(*(_ptr(getattr(self, f.name)) for f in dataclasses.fields(self)))
+
+    @staticmethod
+    def alloc(p: Params, states: bool = True, device="cuda") -> "DeviceHeapTrace":
+        import torch
+        b, B, k, h, L, K = p.batch, p.budget, p.branch, p.hidden, p.depth, p.candidates
+        i32 = dict(dtype=torch.int32, device=device)
+        f32 = dict(dtype=torch.float32, device=device)
+        act = torch.int16 if p.precision == BF16 else torch.float32
+        return DeviceHeapTrace(torch.empty(b, B + 1, **i32), torch.empty(b, B + 1, **i32),
+                               torch.empty(b, B + 1, **i32), torch.empty(b, B + 1, **f32), torch.empty(b, **i32),
+                               torch.empty(B, b, **f32), torch.empty(B, b, k, **f32), torch.empty(B, b, k, **i32),
+                               torch.empty(B + 1, b, h, dtype=act, device=device) if states else None,
+                               torch.empty(b, L, K, **i32) if K > 0 else None)
+
+    def host(self) -> dict:
+        return {f.name: getattr(self, f.name).cpu().numpy() for f in dataclasses.fields(self)
+                if getattr(self, f.name) is not None}
+
+
 def alloc_workspace(p: Params, device="cuda"):
     import torch
     # torch's caching allocator returns blocks aligned to at least 512 bytes
     return torch.empty(max(workspace_size(p), 1), dtype=torch.uint8, device=device)
+
+
+def alloc_heap_workspace(p: Params, device="cuda"):
+    import torch
+    return torch.empty(max(heap_workspace_size(p), 1), dtype=torch.uint8, device=device)
 
 
 # ---------------------------------------------------------------------------
@@ -278,6 +335,19 @@ def build_tree(p: Params, inputs: DeviceInputs, ws, out: DeviceTree, stream=None
     ic, tc = inputs.c(), out.c()
     _check(lib().dartree_build_tree(ctypes.byref(p), ctypes.byref(ic), _ptr(ws), ws.numel(),
                                     ctypes.byref(tc), _stream(stream)), "dartree_build_tree")
+
+
+def build_tree_heap(p: Params, inputs: DeviceInputs, ws, out: DeviceTree, stream=None) -> None:
+    """Sequential correction with a best-first heap (the node-at-a-time baseline)."""
+    ic, tc = inputs.c(), out.c()
+    _check(lib().dartree_build_tree_heap(ctypes.byref(p), ctypes.byref(ic), _ptr(ws), ws.numel(),
+                                         ctypes.byref(tc), _stream(stream)), "dartree_build_tree_heap")
+
+
+def export_heap(p: Params, ws, dst: DeviceHeapTrace, stream=None) -> None:
+    hc = dst.c()
+    _check(lib().dartree_export_heap(ctypes.byref(p), _ptr(ws), ws.numel(), ctypes.byref(hc), _stream(stream)),
+           "dartree_export_heap")
 
 
 KERNEL_NAMES = ["head", "logits", "lse_topk", "select"]   # per depth, launch order

@@ -46,6 +46,7 @@ class Report:
     topk_events: int = 0
     topw_events: int = 0
     topb_events: int = 0
+    pop_events: int = 0          # sequential heap: a pop other than the oracle's own best
     max_logp_err: float = 0.0
     max_lse_err: float = 0.0
     max_score_err: float = 0.0
@@ -55,7 +56,7 @@ class Report:
 
     @property
     def events(self) -> int:
-        return self.topk_events + self.topw_events + self.topb_events
+        return self.topk_events + self.topw_events + self.topb_events + self.pop_events
 
 
 class ParityError(AssertionError):
@@ -89,6 +90,57 @@ def free_running_tol(p) -> float:
     return 2.0 * np.sqrt(p.depth) * 2.0 ** -7 * np.sqrt(p.hidden)
 
 
+def _check_topk(ids, glp, glse, z_row, lp_row, kk, tau, what, eps, rep):
+    """A node's k children chosen by the GPU against the oracle's row."""
+    if len(set(ids.tolist())) != kk or ids.min() < 0 or ids.max() >= len(z_row):
+        raise ParityError(f"{what}: malformed candidate ids {ids}")
+    mine = set(ids.tolist())
+    ref = R.topk_ids(z_row, min(kk + 1, len(z_row)))
+    best_un = next((lp_row[v] for v in ref if v not in mine), -np.inf)
+    _valid_choice(lp_row[ids], best_un, f"top-k {what}", eps)
+    if mine != set(ref[:kk].tolist()):
+        rep.topk_events += 1
+    rep.max_logp_err = max(rep.max_logp_err, float(np.abs(glp - lp_row[ids]).max()))
+    m = z_row.max()
+    lse = m / tau + np.log(np.exp((z_row - m) / tau).sum())
+    rep.max_lse_err = max(rep.max_lse_err, abs(float(glse) - lse))
+    rep.checked_rows += 1
+
+
+def _check_state(r, g, precision, what, rep):
+    """The GPU's bf16 state against the oracle's: equal or one rounding step
+    apart (fp32 mode: the fp32 noise alone)."""
+    err = np.abs(r - g)
+    if precision == R.BF16:
+        diff = err > 0
+        far = err > 2.0 ** -7 * np.maximum(np.abs(r), np.abs(g)) + STATE_ABS_TOL
+    else:
+        diff = err > 1e-6
+        far = err > STATE_ABS_TOL
+    if far.any():
+        raise ParityError(f"{what}: {int(far.sum())} state elements differ by more than one rounding step")
+    rep.state_elems += r.size
+    rep.state_mismatch += int(diff.sum())
+
+
+def _check_emitted(tree, q, b, want, n, score_tol, rep):
+    tok, par, dep, sco, mask, nn = want
+    for name, arr in (("tokens", tok), ("parents", par), ("depths", dep)):
+        if not np.array_equal(tree[name][q], arr):
+            raise ParityError(f"request {b}: {name} differ\nGPU    {tree[name][q][:n]}\noracle {arr[:n]}")
+    if not np.array_equal(tree["mask"][q], mask):
+        raise ParityError(f"request {b}: mask differs")
+    if nn != n:
+        raise ParityError(f"request {b}: num_nodes {n} vs {nn}")
+    fin = np.isfinite(sco)
+    if not np.array_equal(fin, np.isfinite(tree["scores"][q])):
+        raise ParityError(f"request {b}: padding of scores differs")
+    err = float(np.abs(tree["scores"][q][fin] - sco[fin]).max()) if fin.any() else 0.0
+    rep.max_score_err = max(rep.max_score_err, err)
+    if err > score_tol:
+        raise ParityError(f"request {b}: emitted score error {err}")
+
+
 def follow(dec, sup: dict, tree: dict, batch_index: list, requests: list, gpu_states: dict | None = None,
            eps: float = EPS, score_tol: float = SCORE_TOL, rep: Report | None = None) -> Report:
     """Check GPU results against the oracle.
@@ -113,19 +165,7 @@ def follow(dec, sup: dict, tree: dict, batch_index: list, requests: list, gpu_st
             row = q * sizes[d - 2] + j if d > 1 else q  # parent row of this depth
             ids = sup["cand_ids"][d - 1, row, :kk].astype(np.int64)
             glp = sup["cand_logp"][d - 1, row, :kk].astype(np.float64)
-            if len(set(ids.tolist())) != kk or ids.min() < 0 or ids.max() >= len(z_row):
-                raise ParityError(f"depth {d} row {row}: malformed candidate ids {ids}")
-            mine = set(ids.tolist())
-            ref = R.topk_ids(z_row, min(kk + 1, len(z_row)))
-            best_un = next((lp_row[v] for v in ref if v not in mine), -np.inf)
-            _valid_choice(lp_row[ids], best_un, f"top-k depth {d} row {row}", eps)
-            if mine != set(ref[:kk].tolist()):
-                rep.topk_events += 1
-            rep.max_logp_err = max(rep.max_logp_err, float(np.abs(glp - lp_row[ids]).max()))
-            m = z_row.max()
-            lse = m / p.tau + np.log(np.exp((z_row - m) / p.tau).sum())
-            rep.max_lse_err = max(rep.max_lse_err, abs(float(sup["lse"][d - 1, row]) - lse))
-            rep.checked_rows += 1
+            _check_topk(ids, glp, sup["lse"][d - 1, row], z_row, lp_row, kk, p.tau, f"depth {d} row {row}", eps, rep)
             return ids
 
         def choose(req, d, par, tok, sc, n_keep, _unused, q=q):
@@ -153,19 +193,7 @@ def follow(dec, sup: dict, tree: dict, batch_index: list, requests: list, gpu_st
         def adopt(req, d, r, q=q):
             n = sizes[d - 1]
             g = gpu_states[d][q * n:(q + 1) * n]
-            # one bf16 rounding step (2^-7 relative) plus the fp32 noise of the
-            # value before rounding; in fp32 mode the fp32 noise alone
-            err = np.abs(r - g)
-            if p.precision == R.BF16:
-                diff = err > 0
-                far = err > 2.0 ** -7 * np.maximum(np.abs(r), np.abs(g)) + STATE_ABS_TOL
-            else:
-                diff = err > 1e-6
-                far = err > STATE_ABS_TOL
-            if far.any():
-                raise ParityError(f"depth {d}: {int(far.sum())} state elements differ by more than one rounding step")
-            rep.state_elems += r.size
-            rep.state_mismatch += int(diff.sum())
+            _check_state(r, g, p.precision, f"depth {d}", rep)
             return g
 
         st = R.build_supertree(dec, requests=[i], choose=choose, choose_topk=choose_topk,
@@ -203,19 +231,72 @@ def follow(dec, sup: dict, tree: dict, batch_index: list, requests: list, gpu_st
                       max((score[x] for x in all_nodes if x not in ks), default=-np.inf), "top-B", eps)
         if ks != set(R.prune(levels, p.budget)):
             rep.topb_events += 1
-        tok, par, dep, sco, mask, nn = R.emit_tree(levels, kept, p.budget)
-        for name, want in (("tokens", tok), ("parents", par), ("depths", dep)):
-            if not np.array_equal(tree[name][q], want):
-                raise ParityError(f"request {b}: {name} differ\nGPU    {tree[name][q][:n]}\noracle {want[:n]}")
-        if not np.array_equal(tree["mask"][q], mask):
-            raise ParityError(f"request {b}: mask differs")
-        if nn != n:
-            raise ParityError(f"request {b}: num_nodes {n} vs {nn}")
-        fin = np.isfinite(sco)
-        if not np.array_equal(fin, np.isfinite(tree["scores"][q])):
-            raise ParityError(f"request {b}: padding of scores differs")
-        err = float(np.abs(tree["scores"][q][fin] - sco[fin]).max()) if fin.any() else 0.0
-        rep.max_score_err = max(rep.max_score_err, err)
-        if err > score_tol:
-            raise ParityError(f"request {b}: emitted score error {err}")
+        _check_emitted(tree, q, b, R.emit_tree(levels, kept, p.budget), n, score_tol, rep)
+    return rep
+
+
+def follow_heap(dec, trace: dict, tree: dict, batch_index: list, requests: list, gpu_states=None,
+                eps: float = EPS, score_tol: float = SCORE_TOL, rep: Report | None = None) -> Report:
+    """The sequential heap (oracle.sequential_heap) along the GPU's choices.
+
+    trace        host copy of dartree_export_heap (slot i = the i-th pop; step
+                 i ran the head on slot i)
+    gpu_states   decoded states [B+1][b][h] (slot order), or None to run free
+    At every pop the GPU's prefix must be a candidate whose oracle score is
+    within ``eps`` of the best candidate's (else a failure; a different
+    choice within the window is a near-tie event the oracle adopts), and
+    every expanded node's k children are checked like a top-k of the
+    depth-wise construction.  The emitted tree must then equal the oracle's
+    flattening of the followed pops bit for bit, scores within score_tol.
+    """
+    rep = rep or Report()
+    p = dec.p
+    for i, b in enumerate(requests):
+        q = batch_index[i]
+        n_gpu = int(trace["num_popped"][q])
+
+        def choose_topk(req, node, d, z_row, lp_row, kk, q=q):
+            ids = trace["cand_ids"][node, q, :kk].astype(np.int64)
+            glp = trace["cand_logp"][node, q, :kk].astype(np.float64)
+            _check_topk(ids, glp, trace["lse"][node, q], z_row, lp_row, kk, p.tau, f"slot {node}", eps, rep)
+            return ids
+
+        def choose_pop(req, step, heap, q=q):
+            slot = step + 1
+            if slot > n_gpu:
+                raise ParityError(f"request {b}: the GPU stopped after {n_gpu} pops with {len(heap)} candidates left")
+            gp, gt = int(trace["parents"][q, slot]), int(trace["tokens"][q, slot])
+            match = [j for j, (_, (sc, d, par, v)) in enumerate(heap) if par == gp and v == gt]
+            if not match:
+                raise ParityError(f"request {b} pop {slot}: (parent slot {gp}, token {gt}) is not a candidate")
+            j = match[0]
+            best = min(range(len(heap)), key=lambda x: heap[x][0])
+            chosen, top = heap[j][1][0], heap[best][1][0]
+            _valid_choice(np.array([chosen]), top, f"pop {slot}", eps)
+            if j != best:
+                rep.pop_events += 1
+            if int(trace["depths"][q, slot]) != heap[j][1][1]:
+                raise ParityError(f"request {b} pop {slot}: depth {trace['depths'][q, slot]} vs {heap[j][1][1]}")
+            err = abs(float(trace["scores"][q, slot]) - chosen)
+            rep.max_score_err = max(rep.max_score_err, err)
+            if err > score_tol:
+                raise ParityError(f"request {b} pop {slot}: score error {err}")
+            return j
+
+        def adopt(req, node, r, q=q):
+            g = gpu_states[node, q]
+            _check_state(r, g, p.precision, f"slot {node}", rep)
+            return g
+
+        run = R.sequential_heap(dec, requests=[i], choose_topk=choose_topk, choose_pop=choose_pop,
+                                adopt_states=adopt if gpu_states is not None else None)[0]
+        n = len(run.token) - 1
+        if n != n_gpu:
+            raise ParityError(f"request {b}: the GPU popped {n_gpu} prefixes, the oracle {n}")
+        if p.candidates > 0:
+            for d in {run.depth[x] + 1 for x in run.expansions}:
+                if not np.array_equal(trace["csets"][q, d - 1].astype(np.int64),
+                                      R.candidate_set(dec.Lb[i, d - 1], p.candidates)):
+                    raise ParityError(f"request {b} depth {d}: shared candidate set differs")
+        _check_emitted(tree, q, b, R.emit_tree(*R.heap_levels(run), p.budget), n, score_tol, rep)
     return rep

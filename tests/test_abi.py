@@ -22,7 +22,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     syms = declared_symbols()
-    assert len(syms) == 20, syms
+    assert len(syms) == 23, syms
     lib = D.lib()
     for s in syms:
         assert hasattr(lib, s), s
@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert D.abi_version() == 3
+    assert D.abi_version() == 4
     for s in range(5):
         assert D.status_string(s)
     assert D.status_string(99) == "unknown status"
@@ -184,3 +184,34 @@ def test_candidate_sets_reject_bad_arguments():
     assert lib.dartree_candidate_sets(None, 4, 151936, 64, ctypes.c_void_p(FAKE), ws, n.value, None) == D.ERR_INVALID_ARG
     assert lib.dartree_candidate_sets(ctypes.c_void_p(FAKE), 4, 151936, 64, ctypes.c_void_p(FAKE), ws, n.value - 1,
                                       None) == D.ERR_WORKSPACE
+
+
+def test_sequential_heap_validation_and_rejects():
+    lib = D.lib()
+    byref = ctypes.byref
+    for name in W.CONFIG_ORDER:
+        cfg = W.CONFIGS[name]
+        if cfg.budget <= D.MAX_HEAP_BUDGET:
+            assert D.heap_workspace_size(D.Params.of(cfg)) > 0, name
+    p = _p(width=0)                                  # the width is not used by the heap
+    n = D.heap_workspace_size(p)
+    b, B, h, V = p.batch, p.budget, p.hidden, p.vocab
+    assert n >= (B + 1) * b * h * 2 + B * b * h * 4 + b * V * 4   # states, t per slot, one row of logits
+    assert n % 256 == 0
+    with pytest.raises(D.DartreeError) as e:
+        D.heap_workspace_size(_p(budget=D.MAX_HEAP_BUDGET + 1))
+    assert e.value.status == D.ERR_UNSUPPORTED
+    with pytest.raises(D.DartreeError) as e:
+        D.heap_workspace_size(_p(depth_bonus=0.5))
+    assert e.value.status == D.ERR_INVALID_ARG
+    assert D.heap_workspace_size(_p(candidates=64, branch=64)) < n          # logits over C_d only
+    assert lib.dartree_build_tree_heap(byref(p), byref(_inputs()), FAKE, n - 1, byref(_tree()), None) == D.ERR_WORKSPACE
+    assert lib.dartree_build_tree_heap(byref(p), byref(_inputs()), FAKE + 16, n, byref(_tree()), None) == D.ERR_WORKSPACE
+    bad_in = D.InputsC(FAKE, None, FAKE, FAKE, FAKE)
+    assert lib.dartree_build_tree_heap(byref(p), byref(bad_in), FAKE, n, byref(_tree()), None) == D.ERR_INVALID_ARG
+    bad_tree = D.TreeC(FAKE, FAKE, FAKE + 8, FAKE, FAKE, FAKE)
+    assert lib.dartree_build_tree_heap(byref(p), byref(_inputs()), FAKE, n, byref(bad_tree), None) == D.ERR_INVALID_ARG
+    assert lib.dartree_build_tree_heap(byref(_p(batch=0)), byref(_inputs()), FAKE, n, byref(_tree()),
+                                       None) == D.ERR_INVALID_ARG
+    assert lib.dartree_export_heap(byref(p), FAKE, n, None, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_export_heap(byref(p), FAKE, n - 1, byref(D.HeapTraceC()), None) == D.ERR_WORKSPACE
