@@ -186,6 +186,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="qwen3-4b", choices=W.CONFIG_ORDER)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-heap", action="store_true", help="skip the sequential-heap comparison")
+    ap.add_argument("--schedule", default="dartree", choices=["dartree", "heap"],
+                    help="heap: time only the sequential-heap baseline (for a kernel trace of it alone)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: requests are independent trees and this build has no "
@@ -200,10 +203,36 @@ def main() -> int:
     inputs = W.make_inputs(cfg)
     p = D.Params.of(cfg)
     di = D.DeviceInputs.from_host(inputs, dev)
-    ws = D.alloc_workspace(p, dev)
-    out = D.DeviceTree.alloc(cfg.batch, cfg.budget, dev)
     stream = torch.cuda.current_stream()
 
+    def timed(run_round, K):
+        """K rounds, an event pair around each; returns (per-round ms, total ms, wall s)."""
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev[0].record(stream)
+        for i in range(K):
+            run_round()
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        return np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(K)]), ev[0].elapsed_time(ev[K]), wall
+
+    if args.schedule == "heap":
+        log(f"sequential heap only: {args.steps} rounds")
+        heap = time_heap(torch, cfg, di, stream, args.steps, timed)
+        log(f"  {heap['us_per_round']:.1f} us/round")
+        print(json.dumps({
+            "metric": METRIC, "value": heap["us_per_round"], "unit": "us/round", "n_gpus": 1, "steps": args.steps,
+            "warmup": 2, "ms_per_step": heap["us_per_round"] / 1e3, "higher_is_better": False, "scaling": "weak",
+            "vs_baseline": None, "dtype": "bf16" if cfg.precision == W.BF16 else "f32", "data": "synthetic",
+            "config": {"workload": cfg.name, "schedule": "sequential-heap", "batch": cfg.batch, "budget": cfg.budget,
+                       "branch": cfg.branch, "candidates": getattr(cfg, "candidates", 0)},
+            "sequential_heap": heap, "roofline": None, "cpu_baseline": None}), flush=True)
+        return 0
+
+    ws = D.alloc_workspace(p, dev)
+    out = D.DeviceTree.alloc(cfg.batch, cfg.budget, dev)
     log(f"warmup {args.warmup}")
     for _ in range(args.warmup):
         D.build_tree(p, di, ws, out)
@@ -218,19 +247,6 @@ def main() -> int:
     for _ in range(2):
         graph.replay()
     torch.cuda.synchronize()
-
-    def timed(run_round, K):
-        """K rounds, an event pair around each; returns (per-round ms, total ms, wall s)."""
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        ev[0].record(stream)
-        for i in range(K):
-            run_round()
-            ev[i + 1].record(stream)
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-        return np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(K)]), ev[0].elapsed_time(ev[K]), wall
 
     # timed region: exactly K graph replays (the value), then K eager calls
     K = args.steps
@@ -323,7 +339,7 @@ def main() -> int:
     # the node-at-a-time baseline DARTree's depth-wise schedule replaces,
     # a few rounds (each is B head evaluations)
     heap = None
-    if cfg.budget <= D.MAX_HEAP_BUDGET:
+    if cfg.budget <= D.MAX_HEAP_BUDGET and not args.no_heap:
         heap_steps = max(3, min(K, int(2e6 / max(us_round * cfg.budget / cfg.depth, 1.0))))
         log(f"sequential heap: {heap_steps} rounds")
         heap = time_heap(torch, cfg, di, stream, heap_steps, timed)

@@ -70,10 +70,12 @@ def _valid_choice(chosen_vals: np.ndarray, unchosen_best: float, what: str, eps:
 
 
 def decode_states(bits_or_f32: np.ndarray, precision: int) -> np.ndarray:
-    if precision == R.BF16:
-        return (np.asarray(bits_or_f32).view(np.uint16).astype(np.uint32) << np.uint32(16)).view(
-            np.float32).astype(np.float64)
-    return np.asarray(bits_or_f32, np.float32).astype(np.float64)
+    # exported buffers may hold slots no kernel wrote (never compared): any bits
+    with np.errstate(invalid="ignore", over="ignore"):
+        if precision == R.BF16:
+            return (np.asarray(bits_or_f32).view(np.uint16).astype(np.uint32) << np.uint32(16)).view(
+                np.float32).astype(np.float64)
+        return np.asarray(bits_or_f32, np.float32).astype(np.float64)
 
 
 def free_running_tol(p) -> float:
