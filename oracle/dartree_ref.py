@@ -56,6 +56,13 @@ until B prefixes have been popped.  Pop order: (s desc, depth asc, parent node
 asc, child rank asc) - depth asc again prefers ancestors, the last two fields
 make the order total.  The popped prefixes are emitted like DARTree's tree.
 
+With the Markov correction head (``head`` = MARKOV; the DSpark-Markov head of
+Sec. 2.2 and Table 3, which models the one-step transition y_{d-1} -> y_d) the
+state of a prefix is the embedding of its last token only,
+r(u_1:d) = rnd(e * U[u_d]) (r_0: the embedding of the last verified token);
+t, a, z and everything after them are unchanged, so the children's
+distribution depends on the path through its last token and depth alone.
+
 Parity status: every function here is pinned by the CPU tests (brute force,
 Lemma 1's heap, the sequential-heap algorithm of Sec. 3.1, special cases and
 library routines).  The head form itself is this oracle's reading of a passage
@@ -71,6 +78,9 @@ import numpy as np
 
 FP32 = 0
 BF16 = 1
+
+RNN = 0      # Elman residual head: the state summarises the whole prefix
+MARKOV = 1   # the state is the last token's embedding (a first-order transition)
 
 
 # ----------------------------------------------------------------------------
@@ -93,12 +103,14 @@ class Params:
     depth_bonus: float
     precision: int
     candidates: int = 0   # K of a shared C_d = TopK(L_d^base, K); 0 = the full vocabulary
+    head: int = RNN       # RNN or MARKOV correction head
 
     @staticmethod
     def of(cfg) -> "Params":
         return Params(cfg.batch, cfg.vocab, cfg.hidden, cfg.depth, cfg.width,
                       cfg.branch, cfg.budget, float(cfg.temperature),
-                      float(cfg.depth_bonus), int(cfg.precision), int(getattr(cfg, "candidates", 0)))
+                      float(cfg.depth_bonus), int(cfg.precision), int(getattr(cfg, "candidates", 0)),
+                      int(getattr(cfg, "head", RNN)))
 
     @property
     def tau(self) -> float:
@@ -224,6 +236,18 @@ def child_states(t_parent: np.ndarray, U_tok: np.ndarray, e: float, precision: i
     return _rounder(precision)(np.tanh(t_parent + e * U_tok))
 
 
+def markov_states(U_tok: np.ndarray, e: float, precision: int) -> np.ndarray:
+    """Markov head: the state of u_1:d is its last token's embedding rnd(e * U[u_d])."""
+    return _rounder(precision)(e * U_tok)
+
+
+def next_states(p: Params, t_parent: np.ndarray, U_tok: np.ndarray) -> np.ndarray:
+    """The state of each kept child under the configured head."""
+    if p.head == MARKOV:
+        return markov_states(U_tok, p.embed_scale, p.precision)
+    return child_states(t_parent, U_tok, p.embed_scale, p.precision)
+
+
 # ----------------------------------------------------------------------------
 # Whole construction
 # ----------------------------------------------------------------------------
@@ -303,7 +327,7 @@ def build_supertree(dec: Decoded, requests=None, choose: Optional[Chooser] = Non
             lvl = Level(token=tok[keep], parent=par[keep], score=sc[keep], lse=lse,
                         cand_ids=cids, cand_logp=clp, logp=lp if keep_logp else None, cset=cset)
             levels.append(lvl)
-            r = child_states(t[lvl.parent], dec.U[lvl.token], e, p.precision)
+            r = next_states(p, t[lvl.parent], dec.U[lvl.token])
             if adopt_states is not None and d < p.depth:
                 r = adopt_states(b, d, r)
             s = lvl.score
@@ -474,7 +498,7 @@ def sequential_heap(dec: Decoded, requests=None, choose_topk: Optional[Callable]
             run.depth.append(d)
             run.score.append(sc)
             if d < p.depth and len(run.token) - 1 < p.budget:   # the last pop's children are never popped
-                r = child_states(t_of[par][None, :], dec.U[v][None, :], e, p.precision)[0]
+                r = next_states(p, t_of[par][None, :], dec.U[v][None, :])[0]
                 if adopt_states is not None:
                     r = adopt_states(b, n, r)
                 expand(n, r)

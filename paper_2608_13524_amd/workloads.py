@@ -54,6 +54,7 @@ class Config:
     precision: int
     seed: int
     candidates: int = 0           # 0: full vocabulary; K > 0: shared C_d = TopK(L_d^base, K)
+    head: int = 0                 # 0: recurrent (Elman) correction head; 1: Markov head
     depth_bonus: float = -0.2
     sigma_w: float = 0.02
     sigma_l: float = 2.0
@@ -106,8 +107,13 @@ CONFIGS["qwen3-4b-shared"] = Config("qwen3-4b-shared", batch=1, vocab=151936, hi
 CONFIGS["qwen3-8b-shared-x4"] = Config("qwen3-8b-shared-x4", batch=4, vocab=151936, hidden=4096,
                                        depth=16, width=12, branch=64, budget=64,
                                        temperature=1.0, precision=BF16, seed=6, candidates=64)
+# The Markov correction head (DSpark-Markov, Table 3: Qwen3-4B, the same
+# DARTree settings): the state is the previous token's embedding only.
+CONFIGS["qwen3-4b-markov"] = Config("qwen3-4b-markov", batch=1, vocab=151936, hidden=2560, depth=16,
+                                    width=12, branch=64, budget=64, temperature=0.0,
+                                    precision=BF16, seed=7, candidates=64, head=1)
 CONFIG_ORDER = ["tiny", "qwen3-4b", "qwen3-4b-wide", "qwen3-8b-x4", "stress-x16",
-                "qwen3-4b-shared", "qwen3-8b-shared-x4"]
+                "qwen3-4b-shared", "qwen3-8b-shared-x4", "qwen3-4b-markov"]
 
 
 def fp32_to_bf16_bits(x: np.ndarray) -> np.ndarray:

@@ -12,6 +12,8 @@ the tree is built by algorithms the paper states separately from Alg. 1:
 * ``marginal_top_b``       - DDTree's optimum for a zeroed correction: top-B
                               prefixes by factorised mass (Sec. 2.3, eq. (4));
 * ``greedy_chain``         - the corrected single chain (W = 1);
+* ``viterbi``              - Markov head: the best full-depth path by dynamic
+                              programming over the previous token;
 * ``canonical_arrays``     - the flattened tree and mask from a set of paths.
 """
 from __future__ import annotations
@@ -54,6 +56,7 @@ class ScalarHead:
         self.h, self.V = cfg.hidden, cfg.vocab
         self.e = float(np.float32(math.sqrt(cfg.hidden)))
         self.tau = cfg.temperature if cfg.temperature > 0 else 1.0
+        self.markov = getattr(cfg, "head", 0) == 1
 
     def _rnd(self, v):
         return _bf16(v) if self.prec == BF16 else v
@@ -70,6 +73,10 @@ class ScalarHead:
         return t, z, logp
 
     def child(self, t, v):
+        """State of a child with token v: tanh(t + e U[v]), or with the Markov
+        head e U[v] alone (the previous token's embedding), rounded."""
+        if self.markov:
+            return [self._rnd(self.e * self.U[v][i]) for i in range(self.h)]
         return [self._rnd(math.tanh(t[i] + self.e * self.U[v][i])) for i in range(self.h)]
 
     def step_over(self, b, d, r, cset):
@@ -241,6 +248,25 @@ def greedy_chain(head: ScalarHead, b, beta):
         scores.append(score)
         state = head.child(t, v)
     return path, scores
+
+
+def viterbi(head: ScalarHead, b, beta):
+    """Markov head: the best full-depth path by dynamic programming over the
+    last token (its score is a sum of one-step transition log-probabilities,
+    log q_d(v | u) of the head run on u's embedding).  Returns (score, path)."""
+    L, V = head.cfg.depth, head.V
+    _, _, lp = head.step(b, 1, head.r0[b])
+    best = {v: ((0.0 + lp[v]) + beta, (v,)) for v in range(V)}
+    for d in range(2, L + 1):
+        nxt = {}
+        for u, (su, pu) in best.items():
+            _, _, lp = head.step(b, d, head.child(None, u))
+            for v in range(V):
+                s = (su + lp[v]) + beta
+                if v not in nxt or s > nxt[v][0]:
+                    nxt[v] = (s, pu + (v,))
+        best = nxt
+    return max(best.values())
 
 
 def canonical_arrays(paths, budget):

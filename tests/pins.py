@@ -451,6 +451,65 @@ def pin_heap_invariants():
             assert set(run.expansions) == want_expanded
 
 
+# ---------------------------------------------------------------------------
+# The Markov correction head (the state is the last token's embedding)
+# ---------------------------------------------------------------------------
+def pin_markov_brute_force():
+    """k = V, no truncation: DARTree's tree and the sequential heap's are the
+    global top-B over every prefix scored along its path by the Markov head
+    (scalar loops)."""
+    for seed, prec, T in ((90, W.FP32, 0.0), (91, W.BF16, 0.7)):
+        cfg = tiny(seed=seed, precision=prec, vocab=4, depth=3, width=64, branch=4, budget=15, temperature=T,
+                   head=R.MARKOV)
+        inp, tree, st = run_oracle(cfg)
+        want = I.brute_force(I.ScalarHead(inp, cfg), 0, cfg.budget, cfg.depth_bonus)
+        _check_against_paths(tree, 0, want, cfg.budget)
+        _, htree, _ = run_heap(cfg, inp)
+        _check_against_paths(htree, 0, want, cfg.budget)
+
+
+def pin_markov_viterbi():
+    """k = V, no truncation, every prefix kept: the best depth-L node is the
+    path dynamic programming over the previous token finds (a first-order
+    chain's optimum needs no path history)."""
+    for seed, prec in ((92, W.FP32), (93, W.BF16)):
+        cfg = tiny(seed=seed, precision=prec, vocab=5, depth=3, width=200, branch=5, budget=200, head=R.MARKOV)
+        inp, tree, st = run_oracle(cfg)
+        score, path = I.viterbi(I.ScalarHead(inp, cfg), 0, cfg.depth_bonus)
+        got = _paths_and_scores(tree, 0)
+        deepest = {p: sc for p, sc in got.items() if len(p) == cfg.depth}
+        best = max(deepest, key=lambda p: deepest[p])
+        assert best == path and abs(deepest[best] - score) < 1e-9, (best, path, deepest[best], score)
+
+
+def pin_markov_property():
+    """Two parents of one depth that end in the same token get the same
+    children's distribution (top-k ids, log q~ and normaliser), whatever
+    their earlier tokens."""
+    cfg = tiny(seed=94, vocab=4, depth=4, width=64, branch=4, budget=10, head=R.MARKOV)
+    inp, tree, st = run_oracle(cfg)
+    pairs = 0
+    for d in range(2, cfg.depth + 1):
+        prev, lvl = st.levels[0][d - 2], st.levels[0][d - 1]
+        by_token = {}
+        for j, tok in enumerate(prev.token):
+            by_token.setdefault(int(tok), []).append(j)
+        for js in by_token.values():
+            for j in js[1:]:
+                assert np.array_equal(lvl.cand_ids[j], lvl.cand_ids[js[0]])
+                assert np.array_equal(lvl.cand_logp[j], lvl.cand_logp[js[0]])
+                assert lvl.lse[j] == lvl.lse[js[0]]
+                pairs += 1
+    assert pairs > 0
+    # with the recurrent head the same pairs differ (the state carries the path)
+    cfg2 = cfg.replace(head=R.RNN)
+    inp2 = W.Inputs(cfg=cfg2, Lb=inp.Lb, H=inp.H, r0=inp.r0, A=inp.A, U=inp.U)
+    _, _, st2 = run_oracle(cfg2, inp2)
+    prev, lvl = st2.levels[0][1], st2.levels[0][2]
+    j0, j1 = [j for j, t in enumerate(prev.token) if t == prev.token[0]][:2]
+    assert not np.array_equal(lvl.cand_logp[j0], lvl.cand_logp[j1])
+
+
 PINS = [
     pin_shared_brute_force, pin_shared_sequential_heap, pin_shared_zeroed_correction,
     pin_shared_full_vocabulary,
@@ -460,4 +519,5 @@ PINS = [
     pin_batch_independence, pin_vocab_permutation,
     pin_heap_brute_force, pin_heap_equals_wide_dartree, pin_heap_scalar, pin_heap_zeroed_correction,
     pin_heap_shared_brute_force, pin_heap_chain, pin_heap_ties_prefer_ancestors, pin_heap_invariants,
+    pin_markov_brute_force, pin_markov_viterbi, pin_markov_property,
 ]

@@ -13,7 +13,7 @@ from tests import pins
 _orig = {name: getattr(R, name) for name in (
     "head_features", "vocab_logits", "log_softmax", "topk_ids", "select_level",
     "child_states", "path_score", "prune", "emit_tree", "rnd_bf16", "candidate_set",
-    "candidate_logits", "heap_entry")}
+    "candidate_logits", "heap_entry", "markov_states", "next_states")}
 
 
 def _head_transposed(r, A, H_d, precision):
@@ -133,7 +133,17 @@ def _heap_min_first(score, depth, parent, rank, token):
     return (score, depth, parent, rank, token)
 
 
+def _markov_no_scale(U_tok, e, precision):
+    return R._rounder(precision)(U_tok)
+
+
+def _next_ignores_head(p, t_parent, U_tok):
+    return R.child_states(t_parent, U_tok, p.embed_scale, p.precision)
+
+
 MUTANTS = {
+    "markov_embedding_unscaled": ("markov_states", _markov_no_scale),
+    "markov_head_ignored": ("next_states", _next_ignores_head),
     "heap_breadth_first": ("heap_entry", _heap_breadth_first),
     "heap_prefers_descendants": ("heap_entry", _heap_prefers_descendants),
     "heap_pops_worst": ("heap_entry", _heap_min_first),
