@@ -227,7 +227,8 @@ def main() -> int:
             "warmup": 2, "ms_per_step": heap["us_per_round"] / 1e3, "higher_is_better": False, "scaling": "weak",
             "vs_baseline": None, "dtype": "bf16" if cfg.precision == W.BF16 else "f32", "data": "synthetic",
             "config": {"workload": cfg.name, "schedule": "sequential-heap", "batch": cfg.batch, "budget": cfg.budget,
-                       "branch": cfg.branch, "candidates": getattr(cfg, "candidates", 0)},
+                       "branch": cfg.branch, "candidates": getattr(cfg, "candidates", 0),
+                       "head": "markov" if getattr(cfg, "head", 0) == 1 else "rnn"},
             "sequential_heap": heap, "roofline": None, "cpu_baseline": None}), flush=True)
         return 0
 
@@ -359,7 +360,8 @@ def main() -> int:
         "config": {"workload": cfg.name, "batch": cfg.batch, "vocab": cfg.vocab, "hidden": cfg.hidden,
                    "depth": cfg.depth, "width": cfg.width, "branch": cfg.branch, "budget": cfg.budget,
                    "temperature": cfg.temperature, "depth_bonus": cfg.depth_bonus,
-                   "candidates": getattr(cfg, "candidates", 0)},
+                   "candidates": getattr(cfg, "candidates", 0),
+                   "head": "markov" if getattr(cfg, "head", 0) == 1 else "rnn"},
         "timing": "HIP graph replay of dartree_build_tree",
         "eager_us_per_round": eager_us,
         "us_per_round_p10": float(np.percentile(per_step_ms, 10) * 1e3),

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define DARTREE_ABI_VERSION 4
+#define DARTREE_ABI_VERSION 5
 
 /* Limits of this implementation (calls beyond them return
  * DARTREE_ERR_UNSUPPORTED). */
@@ -76,6 +76,15 @@ typedef enum dartree_precision {
   DARTREE_BF16 = 1  /* head weights, hidden and states bf16; logits fp32; bf16 MFMA with fp32 accumulation */
 } dartree_precision;
 
+typedef enum dartree_head {
+  DARTREE_HEAD_RNN = 0,    /* recurrent correction: r(u_1:d) = act(tanh(t(u_<d) + e U[u_d])), the
+                              state summarises the whole prefix (Sec. 2.2, the Domino head) */
+  DARTREE_HEAD_MARKOV = 1  /* Markov correction (Sec. 2.2, the DSpark-Markov head of Table 3):
+                              r(u_1:d) = act(e U[u_d]), the last token's embedding only, so the
+                              children's distribution depends on the path through its last token;
+                              prefix_state is then the last verified token's embedding */
+} dartree_head;
+
 /* Scalar arguments of Algorithm 1 (host struct). */
 typedef struct dartree_params {
   int32_t batch;       /* b >= 1 independent requests, each built as its own tree */
@@ -96,6 +105,7 @@ typedef struct dartree_params {
                           scores only C_d and log q~ is normalised over C_d; each
                           node keeps its top-k of C_d, 1 <= k <= K <= V (k = K keeps
                           all of C_d, the paper's default K = 64) */
+  int32_t head;        /* dartree_head: how a child's state is formed (t, a, z are the same) */
 } dartree_params;
 
 /* Device inputs of one round (Algorithm 1, "Require"). */

@@ -91,6 +91,7 @@ dartree_status validate_common(const dartree_params* p) {
   if (p->candidates < 0) return DARTREE_ERR_INVALID_ARG;
   if (p->candidates > 0 && (p->candidates > p->vocab || p->branch > p->candidates)) return DARTREE_ERR_INVALID_ARG;
   if (p->precision != DARTREE_FP32 && p->precision != DARTREE_BF16) return DARTREE_ERR_INVALID_ARG;
+  if (p->head != DARTREE_HEAD_RNN && p->head != DARTREE_HEAD_MARKOV) return DARTREE_ERR_INVALID_ARG;
   if (!isfinite(p->temperature) || p->temperature < 0.f) return DARTREE_ERR_INVALID_ARG;
   if (!isfinite(p->depth_bonus) || p->depth_bonus > 0.f) return DARTREE_ERR_INVALID_ARG;
   if (p->vocab > DARTREE_MAX_VOCAB || p->depth > DARTREE_MAX_DEPTH) return DARTREE_ERR_UNSUPPORTED;
@@ -221,6 +222,7 @@ dartree_status expand_shared(const dartree_params& p, const dartree_inputs& in, 
   la.precision = p.precision;
   la.hidden = int(h);
   la.vocab = int(V);
+  la.markov = p.head == DARTREE_HEAD_MARKOV;
   la.t = t;
   la.U = in.head_U;
   la.e = float(sqrt(double(p.hidden)));
@@ -324,6 +326,7 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   la.precision = p.precision;
   la.hidden = int(h);
   la.vocab = int(V);
+  la.markov = p.head == DARTREE_HEAD_MARKOV;
   la.t = t;
   la.U = in.head_U;
   la.e = e;
@@ -415,6 +418,7 @@ dartree_status build_heap(const dartree_params& p, const dartree_inputs& in, voi
   ha.depth = int(L);
   ha.k = int(k);
   ha.vocab = int(V);
+  ha.markov = p.head == DARTREE_HEAD_MARKOV;
   ha.shared_k = K;
   ha.beta = p.depth_bonus;
   ha.tau = p.temperature > 0.f ? p.temperature : 1.f;

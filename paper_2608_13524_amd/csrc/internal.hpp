@@ -94,6 +94,7 @@ struct LevelArgs {
   int64_t cset_stride;
   int state;                      // 0: no state update
   int precision, hidden, vocab;
+  int markov;                     // state = act(e U[token]) (Markov head), else act(tanh(t + e U[token]))
   const float* t;                 // [rows][hidden]
   const void* U;                  // act [V][hidden]
   float e;
@@ -134,6 +135,7 @@ hipError_t launch_prune_emit(int batch, const LevelShape& shape, int budget,
 // [budget][batch][...] (step i expands slot i).
 struct HeapArgs {
   int batch, budget, depth, k, vocab;
+  int markov;                   // state = act(e U[token]) (Markov head)
   int shared_k;                 // K > 0: the step's row holds logits over C_d in zsh
   float beta, tau, e;
   int precision, hidden;

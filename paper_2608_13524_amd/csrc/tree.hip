@@ -214,15 +214,16 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
         u16x8 r;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          r[j] = f32_to_bf16(tanhf(t0[j] + a.e * bf16_to_f32(u[j])));
-          r[j + 4] = f32_to_bf16(tanhf(t1[j] + a.e * bf16_to_f32(u[j + 4])));
+          const float e0 = a.e * bf16_to_f32(u[j]), e1 = a.e * bf16_to_f32(u[j + 4]);
+          r[j] = f32_to_bf16(a.markov ? e0 : tanhf(t0[j] + e0));
+          r[j + 4] = f32_to_bf16(a.markov ? e1 : tanhf(t1[j] + e1));
         }
         *reinterpret_cast<u16x8*>(rp + x) = r;
       }
     } else {
       const float* up = static_cast<const float*>(a.U) + tok * h;
       float* rp = static_cast<float*>(a.r_out) + c * h;
-      for (int x = threadIdx.x; x < h; x += blockDim.x) rp[x] = tanhf(tp[x] + a.e * up[x]);
+      for (int x = threadIdx.x; x < h; x += blockDim.x) rp[x] = a.markov ? a.e * up[x] : tanhf(tp[x] + a.e * up[x]);
     }
   }
 }

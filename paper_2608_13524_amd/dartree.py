@@ -16,6 +16,8 @@ LIB_PATH = os.path.join(PKG, "libdartree.so")
 
 FP32 = 0
 BF16 = 1
+HEAD_RNN = 0
+HEAD_MARKOV = 1
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 
@@ -44,13 +46,13 @@ class Params(ctypes.Structure):
                 ("depth", ctypes.c_int32), ("width", ctypes.c_int32), ("branch", ctypes.c_int32),
                 ("budget", ctypes.c_int32), ("precision", ctypes.c_int32),
                 ("temperature", ctypes.c_float), ("depth_bonus", ctypes.c_float),
-                ("candidates", ctypes.c_int32)]
+                ("candidates", ctypes.c_int32), ("head", ctypes.c_int32)]
 
     @staticmethod
     def of(cfg) -> "Params":
         return Params(cfg.batch, cfg.vocab, cfg.hidden, cfg.depth, cfg.width, cfg.branch,
                       cfg.budget, cfg.precision, float(cfg.temperature), float(cfg.depth_bonus),
-                      int(getattr(cfg, "candidates", 0)))
+                      int(getattr(cfg, "candidates", 0)), int(getattr(cfg, "head", HEAD_RNN)))
 
     def level_sizes(self) -> list[int]:
         n, out = 1, []

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert D.abi_version() == 4
+    assert D.abi_version() == 5
     for s in range(5):
         assert D.status_string(s)
     assert D.status_string(99) == "unknown status"
@@ -55,6 +55,7 @@ def _p(**kw):
     ("width", 2049, D.ERR_UNSUPPORTED), ("branch", 33, D.ERR_UNSUPPORTED),
     ("budget", 4097, D.ERR_UNSUPPORTED), ("hidden", 2560 + 32, D.ERR_UNSUPPORTED),
     ("width", 1024, D.ERR_UNSUPPORTED),   # 1024 parents x 8 candidates > 4096
+    ("head", 2, D.ERR_INVALID_ARG), ("head", -1, D.ERR_INVALID_ARG),
 ])
 def test_validate_rejects(field, value, code):
     assert D.validate(_p(**{field: value})) == code
@@ -66,6 +67,7 @@ def test_validate_accepts_all_workloads_and_edges():
     assert D.validate(_p(depth_bonus=0.0, temperature=0.0)) == D.OK
     assert D.validate(_p(depth_bonus=-0.0)) == D.OK
     assert D.validate(_p(width=1, branch=1, budget=1)) == D.OK
+    assert D.validate(_p(head=D.HEAD_MARKOV)) == D.OK
     fp = D.Params.of(W.CONFIGS["tiny"])
     fp.hidden = 7                      # any hidden size in fp32 mode
     assert D.validate(fp) == D.OK

@@ -56,6 +56,8 @@ SMALL = {
     "heap-shared-T0.7": small(candidates=16, branch=16, temperature=0.7, seed=73),
     "heap-shared-K200": small(batch=2, candidates=200, branch=64, budget=100, hidden=128, seed=74),
     "heap-shared-fp32": small(precision=W.FP32, hidden=48, candidates=9, branch=9, sigma_w=0.1, seed=75),
+    "heap-markov": small(head=1, seed=79),
+    "heap-markov-shared": small(head=1, candidates=16, branch=8, budget=30, seed=81),
 }
 
 
@@ -104,7 +106,8 @@ def test_heap_zeroed_correction_is_ddtree():
 # Full-size workloads: requests the oracle re-derives, and the budget (the
 # first B pops of a round do not depend on a larger budget).
 FULL = {"tiny": ([0], None), "qwen3-4b": ([0], None), "qwen3-4b-shared": ([0], None),
-        "qwen3-8b-x4": ([1], 64), "qwen3-8b-shared-x4": ([0, 3], None), "stress-x16": ([5], 32)}
+        "qwen3-8b-x4": ([1], 64), "qwen3-8b-shared-x4": ([0, 3], None), "stress-x16": ([5], 32),
+        "qwen3-4b-markov": ([0], None)}
 
 
 @pytest.mark.parametrize("name", list(FULL))

@@ -54,6 +54,10 @@ SMALL = {
     "shared-fp32": small(precision=W.FP32, hidden=48, candidates=9, branch=9, sigma_w=0.1, seed=54),
     "shared-K-eq-V": small(vocab=40, candidates=40, branch=6, width=6, hidden=64, seed=55),
     "shared-k1": small(candidates=8, branch=1, budget=8, seed=56),
+    # the Markov correction head (state = the last token's embedding)
+    "markov-bf16": small(head=1, seed=58),
+    "markov-shared": small(head=1, candidates=16, branch=16, width=12, budget=40, seed=59),
+    "markov-fp32": small(head=1, precision=W.FP32, hidden=48, sigma_w=0.1, seed=80),
 }
 
 
@@ -126,7 +130,8 @@ def test_expand_then_prune_equals_build():
 
 # Full-size workloads: which requests the oracle re-derives.
 FULL_SAMPLE = {"tiny": [0], "qwen3-4b": [0], "qwen3-4b-wide": [0], "qwen3-8b-x4": [0, 3],
-               "stress-x16": [0, 15], "qwen3-4b-shared": [0], "qwen3-8b-shared-x4": [0, 3]}
+               "stress-x16": [0, 15], "qwen3-4b-shared": [0], "qwen3-8b-shared-x4": [0, 3],
+               "qwen3-4b-markov": [0]}
 
 
 def _log_report(name, mode, rep):
