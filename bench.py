@@ -87,6 +87,19 @@ def kernel_work(cfg, kind: str, d: int):
         return 4 * R * V, 0.0
     if kind == "head":
         return act * h * h + act * h * R + 4 * h * R + act * h * R + act * h * b, 2.0 * R * h * h
+    if kind == "select":
+        # the rows' candidates in (segment records, or the logits over C_d),
+        # parent scores, the level and per-row candidates out, and the state
+        # update of the kept children (parent t rows, U rows in, states out)
+        k, nk = cfg.branch, b * sizes[d]
+        if K:
+            rows_in = 4 * R * K + 4 * b * K
+        else:
+            nseg = max(1, min(-(-1024 // R), -(-V // 2048), 64))
+            bucket = next(x for x in (1, 2, 4, 8, 16, 32) if x >= k)
+            rows_in = 4 * R * nseg * ((4 + 2 * bucket + 3) & ~3) if nseg > 1 else 8 * R * k
+        state = nk * (4 * h + 2 * act * h) if d < cfg.depth else 0
+        return rows_in + 4 * R + 12 * nk + R * (4 + 8 * k) + state, 0.0
     return 0, 0.0
 
 
@@ -304,6 +317,9 @@ def main() -> int:
     else:
         roof = {"bound": "hbm", "achieved": bytes_round / t_round / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
+    if roof["frac"] < 0.1:
+        roof["note"] = ("latency-bound: each launch moves little data, so its duration is launch and "
+                        "dependent-load latency, not bandwidth")
     roof["traffic"] = measured_traffic(cfg.name, dom)
     roof["kernel"] = dom
     roof["algorithmic_bytes_per_launch"] = bytes_round / launches
