@@ -63,6 +63,16 @@ r(u_1:d) = rnd(e * U[u_d]) (r_0: the embedding of the last verified token);
 t, a, z and everything after them are unchanged, so the children's
 distribution depends on the path through its last token and depth alone.
 
+The consumer of the emitted tree (Sec. 2.1, Sec. 2.3, Sec. 4.1):
+  * ``acceptance_walk``: verification accepts, from the root, the child whose
+    token equals the target's token at the current position (its greedy
+    prediction at T = 0, its sample at T = 1: exact target-sample matching),
+    and at the first position with no such child emits the target's token as
+    the bonus; tau = accepted + 1 tokens advance per round;
+  * ``tree_attention``: one attention layer over the flattened tree - node
+    i's query attends to every position of the verified context and to the
+    tree nodes j whose bit is set in mask row i (its root-to-node path).
+
 Parity status: every function here is pinned by the CPU tests (brute force,
 Lemma 1's heap, the sequential-heap algorithm of Sec. 3.1, special cases and
 library routines).  The head form itself is this oracle's reading of a passage
@@ -535,3 +545,60 @@ def sequential_heap_tree(dec: Decoded, requests=None) -> tuple[Tree, list]:
     """Sec. 3.1's baseline end to end: B pops per request, emitted trees."""
     runs = sequential_heap(dec, requests)
     return emit_heap(runs, dec.p.budget), runs
+
+
+# ----------------------------------------------------------------------------
+# The consumer: verification of the emitted tree (Sec. 2.1, 2.3, 4.1)
+# ----------------------------------------------------------------------------
+
+def acceptance_walk(tokens: np.ndarray, parents: np.ndarray, num_nodes: int, target: np.ndarray):
+    """The accepted path of one flattened tree and the bonus token.
+
+    ``target[0]`` is the target's token after the verified context and
+    ``target[i + 1]`` its token after node i's path.  From the root, move to
+    the child whose token is the target's token at the current position;
+    stop at the first position without one.  Returns (output indices of the
+    accepted nodes in path order, bonus token).
+    """
+    cur, path = -1, []
+    while True:
+        want = int(target[cur + 1])
+        child = [j for j in range(int(num_nodes)) if int(parents[j]) == cur and int(tokens[j]) == want]
+        if not child:
+            return path, want
+        cur = child[0]
+        path.append(cur)
+
+
+def mask_bit(mask: np.ndarray, i: int, j: int) -> bool:
+    """Bit (i, j) of a packed ancestor-or-self mask [B][ceil(B/64)] (u64)."""
+    return bool((int(mask[i, j // 64]) >> (j % 64)) & 1)
+
+
+def tree_attention(q: np.ndarray, k_ctx: np.ndarray, v_ctx: np.ndarray, k_tree: np.ndarray,
+                   v_tree: np.ndarray, mask: np.ndarray, ctx_len: int, scale: float) -> np.ndarray:
+    """One attention layer over a flattened tree, one request (Sec. 2.3).
+
+    q [B][Hq][D]; k_ctx, v_ctx [n_ctx][Hkv][D] (the first ctx_len positions
+    are the verified context); k_tree, v_tree [B][Hkv][D] (each node's own key
+    and value); mask [B][ceil(B/64)] u64.  Query head h reads key/value head
+    h // (Hq / Hkv).  Node i attends to context positions 0..ctx_len-1 and to
+    the nodes j with mask bit (i, j) set:
+        out[i][h] = sum_j softmax_j(scale q[i][h] . k_j) v_j      (fp64),
+    and a row that sees nothing is zero.
+    """
+    B, Hq, D = q.shape
+    G = Hq // k_ctx.shape[1]
+    out = np.zeros((B, Hq, D))
+    for i in range(B):
+        nodes = [j for j in range(B) if mask_bit(mask, i, j)]
+        for h in range(Hq):
+            kv = h // G
+            keys = np.concatenate([k_ctx[:ctx_len, kv], k_tree[nodes, kv]], axis=0)
+            vals = np.concatenate([v_ctx[:ctx_len, kv], v_tree[nodes, kv]], axis=0)
+            if len(keys) == 0:      # nothing visible (a pad row without context): zero
+                continue
+            s = scale * (keys @ q[i, h])
+            w = np.exp(s - s.max())
+            out[i, h] = (w / w.sum()) @ vals
+    return out

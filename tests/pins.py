@@ -510,6 +510,114 @@ def pin_markov_property():
     assert not np.array_equal(lvl.cand_logp[j0], lvl.cand_logp[j1])
 
 
+# ---------------------------------------------------------------------------
+# The consumer: acceptance walk and tree attention (Sec. 2.1, 2.3, 4.1)
+# ---------------------------------------------------------------------------
+def _walk_targets(tree, b, V, rng, p_match=0.8):
+    """Target tokens that follow a random child of each position with
+    probability p_match (else a random token, possibly absent)."""
+    n = int(tree.num_nodes[b])
+    target = rng.integers(0, V, size=tree.tokens.shape[1] + 1)
+    for pos in range(-1, n):
+        kids = [j for j in range(n) if tree.parents[b][j] == pos]
+        if kids and rng.random() < p_match:
+            target[pos + 1] = tree.tokens[b][rng.choice(kids)]
+    return target
+
+
+def pin_walk_consistent_paths():
+    """The accepted node is the deepest node whose every edge agrees with the
+    target (token of each node = the target's token after its parent), found
+    by checking every node's whole path rather than walking; the bonus is the
+    target's token after it."""
+    rng = np.random.default_rng(100)
+    for seed in (101, 102, 103):
+        cfg = tiny(seed=seed, vocab=6, depth=4, width=5, branch=3, budget=12)
+        inp, tree, st = run_oracle(cfg)
+        for trial in range(20):
+            target = _walk_targets(tree, 0, cfg.vocab, rng)
+            path, bonus = R.acceptance_walk(tree.tokens[0], tree.parents[0], tree.num_nodes[0], target)
+            n = int(tree.num_nodes[0])
+            ok = []
+            for i in range(n):
+                j, good = i, True
+                while j >= 0:
+                    good &= int(tree.tokens[0][j]) == int(target[int(tree.parents[0][j]) + 1])
+                    j = int(tree.parents[0][j])
+                if good:
+                    ok.append(i)
+            deepest = max(ok, key=lambda i: tree.depths[0][i], default=-1)
+            assert (path[-1] if path else -1) == deepest
+            assert len(path) == (int(tree.depths[0][deepest]) if deepest >= 0 else 0)
+            assert bonus == int(target[deepest + 1])
+            assert all(int(tree.parents[0][c]) == (path[k - 1] if k else -1) for k, c in enumerate(path))
+
+
+def pin_walk_special_cases():
+    """No child matches: nothing accepted and the bonus is the target's first
+    token; a fully matching chain is accepted whole (tau = L + 1)."""
+    cfg = tiny(seed=104, vocab=9, depth=5, width=1, branch=3, budget=5)
+    inp, tree, st = run_oracle(cfg)
+    t = np.full(6, 8)
+    t[0] = (int(tree.tokens[0][0]) + 1) % 9
+    assert R.acceptance_walk(tree.tokens[0], tree.parents[0], tree.num_nodes[0], t) == ([], t[0])
+    chain = np.append(tree.tokens[0][:5], 7)
+    path, bonus = R.acceptance_walk(tree.tokens[0], tree.parents[0], tree.num_nodes[0], chain)
+    assert path == [0, 1, 2, 3, 4] and bonus == 7
+
+
+def _attn_inputs(rng, B, n_ctx, Hq, Hkv, D):
+    return (rng.normal(size=(B, Hq, D)), rng.normal(size=(n_ctx, Hkv, D)), rng.normal(size=(n_ctx, Hkv, D)),
+            rng.normal(size=(B, Hkv, D)), rng.normal(size=(B, Hkv, D)))
+
+
+def pin_tree_attention_paths():
+    """Each node's output equals plain softmax attention over the context and
+    the nodes of its own root-to-node path, the path rebuilt from the parent
+    indices (not the mask); pad rows see the context only."""
+    rng = np.random.default_rng(105)
+    cfg = tiny(seed=106, vocab=7, depth=4, width=4, branch=3, budget=14)
+    inp, tree, st = run_oracle(cfg)
+    B, n = cfg.budget, int(tree.num_nodes[0])
+    for Hq, Hkv, ctx_len in ((4, 2, 5), (2, 2, 0), (6, 3, 9)):
+        q, kc, vc, kt, vt = _attn_inputs(rng, B, 9, Hq, Hkv, 8)
+        out = R.tree_attention(q, kc, vc, kt, vt, tree.mask[0], ctx_len, 0.35)
+        for i in range(B):
+            path, j = [], i if i < n else -1
+            while j >= 0:
+                path.append(j)
+                j = int(tree.parents[0][j])
+            for h in range(Hq):
+                kv = h // (Hq // Hkv)
+                keys = np.concatenate([kc[:ctx_len, kv], kt[path, kv]])
+                if len(keys) == 0:
+                    assert np.all(out[i, h] == 0)
+                    continue
+                w = scipy.special.softmax(0.35 * keys @ q[i, h])
+                want = w @ np.concatenate([vc[:ctx_len, kv], vt[path, kv]])
+                assert np.allclose(out[i, h], want, atol=1e-12)
+
+
+def pin_tree_attention_chain_is_causal():
+    """A chain (W = 1) is an ordinary causal sequence after the context:
+    torch's scaled-dot-product attention with a causal mask over
+    [context; chain] gives the same outputs (key/value heads repeated per
+    query group)."""
+    cfg = tiny(seed=107, vocab=9, depth=6, width=1, branch=3, budget=6)
+    inp, tree, st = run_oracle(cfg)
+    rng = np.random.default_rng(108)
+    B, ctx, Hq, Hkv, D = 6, 5, 4, 2, 16
+    q, kc, vc, kt, vt = _attn_inputs(rng, B, ctx, Hq, Hkv, D)
+    out = R.tree_attention(q, kc, vc, kt, vt, tree.mask[0], ctx, 1.0 / np.sqrt(D))
+    K = torch.from_numpy(np.concatenate([kc, kt])).repeat_interleave(Hq // Hkv, dim=1).transpose(0, 1)
+    Vv = torch.from_numpy(np.concatenate([vc, vt])).repeat_interleave(Hq // Hkv, dim=1).transpose(0, 1)
+    Q = torch.from_numpy(q).transpose(0, 1)
+    allowed = torch.ones(B, ctx + B, dtype=torch.bool)
+    allowed[:, ctx:] = torch.tril(torch.ones(B, B, dtype=torch.bool))
+    ref = torch.nn.functional.scaled_dot_product_attention(Q, K, Vv, attn_mask=allowed).transpose(0, 1).numpy()
+    assert np.allclose(out, ref, atol=1e-10)
+
+
 PINS = [
     pin_shared_brute_force, pin_shared_sequential_heap, pin_shared_zeroed_correction,
     pin_shared_full_vocabulary,
@@ -520,4 +628,5 @@ PINS = [
     pin_heap_brute_force, pin_heap_equals_wide_dartree, pin_heap_scalar, pin_heap_zeroed_correction,
     pin_heap_shared_brute_force, pin_heap_chain, pin_heap_ties_prefer_ancestors, pin_heap_invariants,
     pin_markov_brute_force, pin_markov_viterbi, pin_markov_property,
+    pin_walk_consistent_paths, pin_walk_special_cases, pin_tree_attention_paths, pin_tree_attention_chain_is_causal,
 ]

@@ -13,7 +13,8 @@ from tests import pins
 _orig = {name: getattr(R, name) for name in (
     "head_features", "vocab_logits", "log_softmax", "topk_ids", "select_level",
     "child_states", "path_score", "prune", "emit_tree", "rnd_bf16", "candidate_set",
-    "candidate_logits", "heap_entry", "markov_states", "next_states")}
+    "candidate_logits", "heap_entry", "markov_states", "next_states", "acceptance_walk", "tree_attention",
+    "mask_bit")}
 
 
 def _head_transposed(r, A, H_d, precision):
@@ -141,7 +142,42 @@ def _next_ignores_head(p, t_parent, U_tok):
     return R.child_states(t_parent, U_tok, p.embed_scale, p.precision)
 
 
+def _walk_own_target(tokens, parents, num_nodes, target):
+    # reads the target at the child's own index instead of its parent's position
+    cur, path = -1, []
+    while True:
+        kids = [j for j in range(int(num_nodes)) if int(parents[j]) == cur]
+        match = [j for j in kids if int(tokens[j]) == int(target[j + 1])]
+        if not match:
+            return path, int(target[cur + 1])
+        cur = match[0]
+        path.append(cur)
+
+
+def _walk_no_bonus(tokens, parents, num_nodes, target):
+    path, bonus = _orig["acceptance_walk"](tokens, parents, num_nodes, target)
+    return path, int(target[0])
+
+
+def _attn_all_nodes(q, k_ctx, v_ctx, k_tree, v_tree, mask, ctx_len, scale):
+    full = np.full_like(mask, np.uint64(0xFFFFFFFFFFFFFFFF))
+    return _orig["tree_attention"](q, k_ctx, v_ctx, k_tree, v_tree, full, ctx_len, scale)
+
+
+def _attn_no_scale(q, k_ctx, v_ctx, k_tree, v_tree, mask, ctx_len, scale):
+    return _orig["tree_attention"](q, k_ctx, v_ctx, k_tree, v_tree, mask, ctx_len, 1.0)
+
+
+def _mask_bit_transposed(mask, i, j):
+    return bool((int(mask[j, i // 64]) >> (i % 64)) & 1) if j < mask.shape[0] else False
+
+
 MUTANTS = {
+    "walk_reads_child_target": ("acceptance_walk", _walk_own_target),
+    "walk_bonus_always_first": ("acceptance_walk", _walk_no_bonus),
+    "attention_ignores_mask": ("tree_attention", _attn_all_nodes),
+    "attention_unscaled": ("tree_attention", _attn_no_scale),
+    "attention_mask_transposed": ("mask_bit", _mask_bit_transposed),
     "markov_embedding_unscaled": ("markov_states", _markov_no_scale),
     "markov_head_ignored": ("next_states", _next_ignores_head),
     "heap_breadth_first": ("heap_entry", _heap_breadth_first),
