@@ -156,6 +156,52 @@ def time_heap(torch, cfg, di, stream, steps: int, timed) -> dict:
             "timing": "HIP graph replay of dartree_build_tree_heap"}
 
 
+def time_consumer(torch, cfg, out, stream, reps: int = 50) -> dict:
+    """The step after the path on the tree just built: one tree-attention
+    layer of Qwen3-4B's shape over a 2048-position context (the target's
+    verification pass reads the emitted mask) and the acceptance walk, each
+    the mean of `reps` launches bracketed by events."""
+    dev = out.tokens.device
+    s = W.ATTENTION_QWEN3_4B
+    ai = W.make_attention_inputs(cfg.batch, cfg.budget, s["max_ctx"], s["heads_q"], s["heads_kv"], seed=7)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16) if a.dtype == np.uint16 else a).to(dev)
+    q, kc, vc, kt, vt = t(ai.q), t(ai.k_ctx), t(ai.v_ctx), t(ai.k_tree), t(ai.v_tree)
+    p = D.AttnParams(cfg.batch, cfg.budget, s["max_ctx"], s["heads_q"], s["heads_kv"], s["head_dim"],
+                     1.0 / np.sqrt(s["head_dim"]))
+    ws = torch.empty(D.tree_attention_workspace_size(p), dtype=torch.uint8, device=dev)
+    o = torch.empty(cfg.batch, cfg.budget, s["heads_q"], s["head_dim"], dtype=torch.float32, device=dev)
+    target = torch.randint(0, cfg.vocab, (cfg.batch, cfg.budget + 1), dtype=torch.int32, device=dev,
+                           generator=torch.Generator(device=dev).manual_seed(7))
+    acc = torch.empty(cfg.batch, cfg.depth, dtype=torch.int32, device=dev)
+    na = torch.empty(cfg.batch, dtype=torch.int32, device=dev)
+    bonus = torch.empty(cfg.batch, dtype=torch.int32, device=dev)
+
+    def mean_us(fn):
+        fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / reps
+
+    attn_us = mean_us(lambda: D.tree_attention(p, q, kc, vc, kt, vt, out.mask, None, o, ws))
+    walk_us = mean_us(lambda: D.accept_walk(out.tokens, out.parents, out.num_nodes, target, acc, na, bonus))
+    # algorithmic work of the layer: context and tree keys/values once, the
+    # queries once, fp32 outputs written; 4 flop per (query row, key, dim)
+    b, B, n, Hq, Hkv, Dh = cfg.batch, cfg.budget, s["max_ctx"], s["heads_q"], s["heads_kv"], s["head_dim"]
+    nbytes = 2 * 2 * b * (n + B) * Hkv * Dh + 2 * b * B * Hq * Dh + 4 * b * B * Hq * Dh
+    flops = 4.0 * b * B * Hq * (n + B) * Dh
+    return {"tree_attention_us": attn_us, "accept_walk_us": walk_us,
+            "shape": {"heads_q": Hq, "heads_kv": Hkv, "head_dim": Dh, "context": n, "nodes": B},
+            "attention_roofline": {"bound": "hbm", "achieved": nbytes / attn_us / 1e3, "peak": HBM_PEAK_GBS,
+                                   "unit": "GB/s", "frac": nbytes / attn_us / 1e3 / HBM_PEAK_GBS,
+                                   "algorithmic_bytes": nbytes, "flops": flops,
+                                   "note": "latency-bound at one request: 10 MB and 2.2 GFLOP per layer"}}
+
+
 def cpu_baseline(cfg, inputs, budget_s: float = 20.0) -> dict:
     """The oracle (fp64 NumPy) on the host cores, on the first D depths of
     request 0 with D chosen to take ~budget_s; scaled to us per full round."""
@@ -363,6 +409,12 @@ def main() -> int:
         heap["vs_dartree"] = heap["us_per_round"] / us_round
         log(f"  {heap['us_per_round']:.1f} us/round, {heap['vs_dartree']:.2f}x DARTree's round")
 
+    consumer = None
+    if cfg.precision == W.BF16:
+        consumer = time_consumer(torch, cfg, out, stream)
+        log(f"consumer: tree attention {consumer['tree_attention_us']:.1f} us, "
+            f"acceptance walk {consumer['accept_walk_us']:.1f} us")
+
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle on host cores)")
@@ -389,6 +441,7 @@ def main() -> int:
         "projection_mfma_frac": proj_flops / MFMA_BF16_PEAK_TFS,
         "kernels": kernels, "instrumented_us_per_round": instrumented_us,
         "roofline": roof, "lse_topk_roofline": lse_roof, "calibration": cal, "sequential_heap": heap,
+        "consumer": consumer,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define DARTREE_ABI_VERSION 5
+#define DARTREE_ABI_VERSION 6
 
 /* Limits of this implementation (calls beyond them return
  * DARTREE_ERR_UNSUPPORTED). */
@@ -313,6 +313,54 @@ dartree_status dartree_build_tree_heap(const dartree_params* p, const dartree_in
  * dartree_build_tree_heap on `ws` into the caller's buffers (for inspection). */
 dartree_status dartree_export_heap(const dartree_params* p, const void* ws, size_t ws_bytes,
                                    const dartree_heap_trace* dst, hipStream_t stream);
+
+/* ---- the consumer of the emitted tree ----------------------------------------
+ * What the target model does with the tree (Sec. 2.1, Sec. 2.3, Sec. 4.1). */
+
+/* Acceptance walk.  For request q (tree arrays as written by the builds
+ * above: tokens, parents [b][B], num_nodes [b]), target [b][B+1] holds the
+ * target's token after the verified context (index 0) and after the path of
+ * node i (index i + 1): its greedy prediction at T = 0, its sample at T = 1
+ * (exact target-sample matching).  From the root, move to the child whose
+ * token equals the target's token at the current position; stop at the first
+ * position without one.  Writes the output indices of the accepted nodes in
+ * path order to accepted [b][max_len] (-1 after the last), their count to
+ * num_accepted [b] (at most max_len), and the target's token at the last
+ * accepted position to bonus [b]: the round advances num_accepted + 1 tokens.
+ * 1 <= budget <= DARTREE_MAX_SORT; max_len >= 1 (a path has at most L nodes). */
+dartree_status dartree_accept_walk(int32_t batch, int32_t budget, int32_t max_len, const int32_t* tokens,
+                                   const int32_t* parents, const int32_t* num_nodes, const int32_t* target,
+                                   int32_t* accepted, int32_t* num_accepted, int32_t* bonus, hipStream_t stream);
+
+/* Shape of one tree-attention layer (grouped-query attention). */
+typedef struct dartree_attn_params {
+  int32_t batch;     /* b requests */
+  int32_t budget;    /* B tree slots per request (the rows of the emitted tree) */
+  int32_t max_ctx;   /* context positions held per request (>= 0) */
+  int32_t heads_q;   /* query heads, a multiple of heads_kv */
+  int32_t heads_kv;  /* key/value heads; query head h reads key/value head h / (heads_q / heads_kv) */
+  int32_t head_dim;  /* 128 */
+  float scale;       /* softmax scale (> 0), e.g. 1 / sqrt(head_dim) */
+} dartree_attn_params;
+
+dartree_status dartree_tree_attention_workspace_size(const dartree_attn_params* p, size_t* bytes);
+
+/* One attention layer over the flattened trees (Sec. 2.3): the query of
+ * node i attends to the first ctx_len[q] context positions (ctx_len NULL: all
+ * max_ctx) and to the tree nodes j whose bit is set in mask row i (its
+ * ancestors and itself, as emitted):
+ *   out[q][i][h] = sum_j softmax_j(scale q[q][i][h] . k_j) v_j,
+ * and a row that sees nothing is 0.  q: bf16 [b][B][heads_q][128];
+ * k_ctx, v_ctx: bf16 [b][max_ctx][heads_kv][128] (may be NULL if max_ctx = 0);
+ * k_tree, v_tree: bf16 [b][B][heads_kv][128], node i's own key and value;
+ * mask: u64 [b][B][ceil(B/64)]; out: fp32 [b][B][heads_q][128].  bf16
+ * products with fp32 accumulation; the softmax weights are rounded to bf16
+ * for the weighted sum of values.  ws: device, 256-byte aligned, >=
+ * dartree_tree_attention_workspace_size (per-segment partial results). */
+dartree_status dartree_tree_attention(const dartree_attn_params* p, const void* q, const void* k_ctx,
+                                      const void* v_ctx, const void* k_tree, const void* v_tree,
+                                      const uint64_t* mask, const int32_t* ctx_len, float* out, void* ws,
+                                      size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libdartree.so")
-SOURCES = ["api.cpp", "proj.hip", "lse_topk.hip", "tree.hip", "shared.hip", "heap.hip", "calib.hip"]
+SOURCES = ["api.cpp", "proj.hip", "lse_topk.hip", "tree.hip", "shared.hip", "heap.hip", "verify.hip", "calib.hip"]
 ARCH = "gfx950"
 
 FLAGS = [

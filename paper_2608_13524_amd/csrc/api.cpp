@@ -703,6 +703,97 @@ dartree_status dartree_prune_levels(const dartree_params* p, const int32_t* toke
       launch_prune_emit(p->batch, level_shape(*p, s), p->budget, tokens, parents, scores, *out, stream));
 }
 
+// ---------------------------------------------------------------------------
+// The consumer of the emitted tree
+// ---------------------------------------------------------------------------
+dartree_status dartree_accept_walk(int32_t batch, int32_t budget, int32_t max_len, const int32_t* tokens,
+                                   const int32_t* parents, const int32_t* num_nodes, const int32_t* target,
+                                   int32_t* accepted, int32_t* num_accepted, int32_t* bonus, hipStream_t stream) {
+  if (batch < 1 || budget < 1 || max_len < 1) return DARTREE_ERR_INVALID_ARG;
+  if (budget > DARTREE_MAX_SORT) return DARTREE_ERR_UNSUPPORTED;
+  if (!tokens || !parents || !num_nodes || !target || !accepted || !num_accepted || !bonus)
+    return DARTREE_ERR_INVALID_ARG;
+  return hip_status(launch_accept_walk(batch, budget, max_len, tokens, parents, num_nodes, target, accepted,
+                                       num_accepted, bonus, stream));
+}
+
+namespace {
+dartree_status check_attn(const dartree_attn_params* p) {
+  if (!p) return DARTREE_ERR_INVALID_ARG;
+  if (p->batch < 1 || p->budget < 1 || p->max_ctx < 0 || p->heads_q < 1 || p->heads_kv < 1 || p->head_dim < 1)
+    return DARTREE_ERR_INVALID_ARG;
+  if (p->heads_q % p->heads_kv != 0 || !isfinite(p->scale) || p->scale <= 0.f) return DARTREE_ERR_INVALID_ARG;
+  if (p->head_dim != 128 || p->budget > DARTREE_MAX_SORT) return DARTREE_ERR_UNSUPPORTED;
+  if (int64_t(p->batch) * p->budget * p->heads_q > (int64_t(1) << 30)) return DARTREE_ERR_UNSUPPORTED;
+  return DARTREE_OK;
+}
+
+struct AttnLayout {
+  int nseg_ctx, rows_pad;
+  size_t part_o, part_ml, total;
+};
+
+AttnLayout attn_layout_of(const dartree_attn_params& p) {
+  AttnLayout l{};
+  const int seg = attention_segment_len();
+  l.nseg_ctx = (p.max_ctx + seg - 1) / seg;
+  const int rows = p.budget * (p.heads_q / p.heads_kv);
+  l.rows_pad = (rows + 63) / 64 * 64;
+  const size_t slots = size_t(l.nseg_ctx + 1) * p.batch * p.heads_kv * l.rows_pad;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { const size_t at = o; o = align_up(o + bytes); return at; };
+  l.part_o = take(slots * 128 * 4);
+  l.part_ml = take(slots * 2 * 4);
+  l.total = o;
+  return l;
+}
+}  // namespace
+
+dartree_status dartree_tree_attention_workspace_size(const dartree_attn_params* p, size_t* bytes) {
+  if (!bytes) return DARTREE_ERR_INVALID_ARG;
+  const dartree_status v = check_attn(p);
+  if (v != DARTREE_OK) return v;
+  *bytes = attn_layout_of(*p).total;
+  return DARTREE_OK;
+}
+
+dartree_status dartree_tree_attention(const dartree_attn_params* p, const void* q, const void* k_ctx,
+                                      const void* v_ctx, const void* k_tree, const void* v_tree,
+                                      const uint64_t* mask, const int32_t* ctx_len, float* out, void* ws,
+                                      size_t ws_bytes, hipStream_t stream) {
+  dartree_status v = check_attn(p);
+  if (v != DARTREE_OK) return v;
+  if (!q || !k_tree || !v_tree || !mask || !out) return DARTREE_ERR_INVALID_ARG;
+  if (p->max_ctx > 0 && (!k_ctx || !v_ctx)) return DARTREE_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k_tree) || !aligned16(v_tree) || (k_ctx && !aligned16(k_ctx)) ||
+      (v_ctx && !aligned16(v_ctx)) || !aligned16(out))
+    return DARTREE_ERR_INVALID_ARG;
+  const AttnLayout l = attn_layout_of(*p);
+  if (!ws || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0 || ws_bytes < l.total) return DARTREE_ERR_WORKSPACE;
+  AttnArgs a{};
+  a.batch = p->batch;
+  a.budget = p->budget;
+  a.max_ctx = p->max_ctx;
+  a.heads_q = p->heads_q;
+  a.heads_kv = p->heads_kv;
+  a.group = p->heads_q / p->heads_kv;
+  a.nseg_ctx = l.nseg_ctx;
+  a.seg_len = attention_segment_len();
+  a.rows_pad = l.rows_pad;
+  a.scale_log2 = p->scale * 1.4426950408889634f;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_ctx = static_cast<const uint16_t*>(k_ctx);
+  a.v_ctx = static_cast<const uint16_t*>(v_ctx);
+  a.k_tree = static_cast<const uint16_t*>(k_tree);
+  a.v_tree = static_cast<const uint16_t*>(v_tree);
+  a.mask = mask;
+  a.ctx_len = ctx_len;
+  a.part_o = at<float>(ws, l.part_o);
+  a.part_ml = at<float>(ws, l.part_ml);
+  a.out = out;
+  return hip_status(launch_tree_attention(a, stream));
+}
+
 dartree_status dartree_heap_workspace_size(const dartree_params* p, size_t* bytes) {
   if (!bytes) return DARTREE_ERR_INVALID_ARG;
   const dartree_status v = validate_heap(p);

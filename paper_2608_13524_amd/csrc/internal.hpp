@@ -161,6 +161,33 @@ struct HeapArgs {
   void* r_store;                // act [budget + 1][batch][hidden]: r of slot i
 };
 hipError_t launch_heap_step(const HeapArgs& a, hipStream_t s);
+
+// The consumer of the emitted tree: the acceptance walk, and one tree-attention
+// layer (head_dim 128) in key segments merged by a second kernel.  Partial
+// results per segment s, request q, key/value head h and query row r (r =
+// node * group + query head within the group) live at index
+// ((s * batch + q) * heads_kv + h) * rows_pad + r of part_o ([..][128]) and
+// part_ml ([..][2]: running max in log2 units, sum).
+hipError_t launch_accept_walk(int batch, int budget, int max_len, const int32_t* tokens, const int32_t* parents,
+                              const int32_t* num_nodes, const int32_t* target, int32_t* accepted,
+                              int32_t* n_accepted, int32_t* bonus, hipStream_t s);
+struct AttnArgs {
+  int batch, budget, max_ctx, heads_q, heads_kv, group;
+  int nseg_ctx, seg_len, rows_pad;
+  float scale_log2;             // softmax scale * log2(e)
+  const uint16_t* q;            // bf16 [batch][budget][heads_q][128]
+  const uint16_t* k_ctx;        // bf16 [batch][max_ctx][heads_kv][128]
+  const uint16_t* v_ctx;
+  const uint16_t* k_tree;       // bf16 [batch][budget][heads_kv][128]
+  const uint16_t* v_tree;
+  const uint64_t* mask;         // [batch][budget][ceil(budget / 64)]
+  const int32_t* ctx_len;       // [batch] or NULL (max_ctx)
+  float* part_o;
+  float* part_ml;
+  float* out;                   // fp32 [batch][budget][heads_q][128]
+};
+int attention_segment_len();
+hipError_t launch_tree_attention(const AttnArgs& a, hipStream_t s);
 hipError_t launch_heap_emit(const HeapArgs& a, const dartree_tree& out, hipStream_t s);
 
 }  // namespace dartree

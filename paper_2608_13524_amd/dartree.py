@@ -36,6 +36,7 @@ SYMBOLS = [
     "dartree_lse_topk_workspace_size", "dartree_lse_topk", "dartree_select_topw",
     "dartree_prune_levels", "dartree_candidate_sets_workspace_size", "dartree_candidate_sets",
     "dartree_heap_workspace_size", "dartree_build_tree_heap", "dartree_export_heap",
+    "dartree_accept_walk", "dartree_tree_attention_workspace_size", "dartree_tree_attention",
     "dartree_calib_read", "dartree_calib_copy", "dartree_calib_mfma",
 ]
 CALIB_SINK_FLOATS = 4096
@@ -86,6 +87,12 @@ class HeapTraceC(ctypes.Structure):
                 ("csets", ctypes.c_void_p)]
 
 
+class AttnParams(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("budget", ctypes.c_int32), ("max_ctx", ctypes.c_int32),
+                ("heads_q", ctypes.c_int32), ("heads_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("scale", ctypes.c_float)]
+
+
 class DartreeError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
@@ -130,6 +137,9 @@ def lib() -> ctypes.CDLL:
     L.dartree_heap_workspace_size.argtypes = [P, ctypes.POINTER(sz)]
     L.dartree_build_tree_heap.argtypes = [P, ctypes.POINTER(InputsC), vp, sz, ctypes.POINTER(TreeC), vp]
     L.dartree_export_heap.argtypes = [P, vp, sz, ctypes.POINTER(HeapTraceC), vp]
+    L.dartree_accept_walk.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.dartree_tree_attention_workspace_size.argtypes = [ctypes.POINTER(AttnParams), ctypes.POINTER(sz)]
+    L.dartree_tree_attention.argtypes = [ctypes.POINTER(AttnParams), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.dartree_calib_read.argtypes = [vp, sz, vp, vp]
     L.dartree_calib_copy.argtypes = [vp, vp, sz, vp]
     L.dartree_calib_mfma.argtypes = [i32, i32, vp, vp]
@@ -450,3 +460,28 @@ def candidate_sets_workspace_size(rows: int, vocab: int, K: int) -> int:
     _check(lib().dartree_candidate_sets_workspace_size(rows, vocab, K, ctypes.byref(n)),
            "dartree_candidate_sets_workspace_size")
     return n.value
+
+
+# ---------------------------------------------------------------------------
+# The consumer of the emitted tree
+# ---------------------------------------------------------------------------
+def accept_walk(tokens, parents, num_nodes, target, accepted, num_accepted, bonus, stream=None) -> None:
+    """tokens, parents [b][B] and num_nodes [b] of emitted trees, target [b][B+1];
+    outputs accepted [b][max_len], num_accepted [b], bonus [b] (int32 device)."""
+    batch, budget = tokens.shape
+    _check(lib().dartree_accept_walk(batch, budget, accepted.shape[1], _ptr(tokens), _ptr(parents), _ptr(num_nodes),
+                                     _ptr(target), _ptr(accepted), _ptr(num_accepted), _ptr(bonus),
+                                     _stream(stream)), "dartree_accept_walk")
+
+
+def tree_attention_workspace_size(p: AttnParams) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().dartree_tree_attention_workspace_size(ctypes.byref(p), ctypes.byref(n)),
+           "dartree_tree_attention_workspace_size")
+    return n.value
+
+
+def tree_attention(p: AttnParams, q, k_ctx, v_ctx, k_tree, v_tree, mask, ctx_len, out, ws, stream=None) -> None:
+    _check(lib().dartree_tree_attention(ctypes.byref(p), _ptr(q), _ptr(k_ctx), _ptr(v_ctx), _ptr(k_tree),
+                                        _ptr(v_tree), _ptr(mask), _ptr(ctx_len), _ptr(out), _ptr(ws),
+                                        0 if ws is None else ws.numel(), _stream(stream)), "dartree_tree_attention")

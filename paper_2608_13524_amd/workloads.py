@@ -222,3 +222,42 @@ def make_inputs(cfg: Config, requests: Optional[list[int]] = None,
     r0 = np.stack([p[2] for p in parts])
     sub = cfg.replace(batch=len(requests))
     return Inputs(cfg=sub, Lb=Lb, H=H, r0=r0, A=A, U=U)
+
+
+# ---------------------------------------------------------------------------
+# The consumer of the emitted tree: one tree-attention layer's inputs
+# ---------------------------------------------------------------------------
+@dataclasses.dataclass
+class AttentionInputs:
+    """bf16 bit patterns (uint16) of one attention layer over a flattened tree:
+    q [b][B][Hq][D], k_ctx / v_ctx [b][max_ctx][Hkv][D], k_tree / v_tree
+    [b][B][Hkv][D]; ctx_len int32 [b]."""
+
+    q: np.ndarray
+    k_ctx: np.ndarray
+    v_ctx: np.ndarray
+    k_tree: np.ndarray
+    v_tree: np.ndarray
+    ctx_len: np.ndarray
+
+
+# Qwen3-4B's attention shape (32 query heads, 8 key/value heads, head size
+# 128) over a 2048-position verified context: the layer the paper's target
+# runs on every verified tree.
+ATTENTION_QWEN3_4B = dict(heads_q=32, heads_kv=8, head_dim=128, max_ctx=2048)
+
+
+def make_attention_inputs(batch: int, budget: int, max_ctx: int, heads_q: int, heads_kv: int,
+                          head_dim: int = 128, seed: int = 0, ctx_len=None) -> AttentionInputs:
+    """Unit-normal queries, keys and values rounded to bf16, one stream per
+    tensor (SeedSequence([seed, 3, tensor]))."""
+    def draw(t, shape):
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 3, t])))
+        return fp32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+
+    lens = np.full(batch, max_ctx, np.int32) if ctx_len is None else np.asarray(ctx_len, np.int32)
+    return AttentionInputs(q=draw(0, (batch, budget, heads_q, head_dim)),
+                           k_ctx=draw(1, (batch, max_ctx, heads_kv, head_dim)),
+                           v_ctx=draw(2, (batch, max_ctx, heads_kv, head_dim)),
+                           k_tree=draw(3, (batch, budget, heads_kv, head_dim)),
+                           v_tree=draw(4, (batch, budget, heads_kv, head_dim)), ctx_len=lens)

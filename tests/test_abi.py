@@ -22,7 +22,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     syms = declared_symbols()
-    assert len(syms) == 23, syms
+    assert len(syms) == 26, syms
     lib = D.lib()
     for s in syms:
         assert hasattr(lib, s), s
@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert D.abi_version() == 5
+    assert D.abi_version() == 6
     for s in range(5):
         assert D.status_string(s)
     assert D.status_string(99) == "unknown status"
@@ -217,3 +217,31 @@ def test_sequential_heap_validation_and_rejects():
                                        None) == D.ERR_INVALID_ARG
     assert lib.dartree_export_heap(byref(p), FAKE, n, None, None) == D.ERR_INVALID_ARG
     assert lib.dartree_export_heap(byref(p), FAKE, n - 1, byref(D.HeapTraceC()), None) == D.ERR_WORKSPACE
+
+
+def test_consumer_rejects_bad_arguments():
+    lib = D.lib()
+    F = ctypes.c_void_p(FAKE)
+    args = [F] * 7
+    assert lib.dartree_accept_walk(0, 8, 4, *args, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_accept_walk(1, 8, 0, *args, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_accept_walk(1, 4097, 4, *args, None) == D.ERR_UNSUPPORTED
+    assert lib.dartree_accept_walk(1, 8, 4, F, F, F, None, F, F, F, None) == D.ERR_INVALID_ARG
+    p = D.AttnParams(batch=1, budget=64, max_ctx=2048, heads_q=32, heads_kv=8, head_dim=128, scale=0.0884)
+    n = D.tree_attention_workspace_size(p)
+    assert n >= 9 * 8 * 256 * 128 * 4          # one partial row per segment, kv head and query row
+    for field, value, code in (("head_dim", 64, D.ERR_UNSUPPORTED), ("heads_q", 30, D.ERR_INVALID_ARG),
+                               ("scale", 0.0, D.ERR_INVALID_ARG), ("budget", 0, D.ERR_INVALID_ARG),
+                               ("max_ctx", -1, D.ERR_INVALID_ARG), ("budget", 4097, D.ERR_UNSUPPORTED)):
+        bad = D.AttnParams(1, 64, 2048, 32, 8, 128, 0.0884)
+        setattr(bad, field, value)
+        with pytest.raises(D.DartreeError) as e:
+            D.tree_attention_workspace_size(bad)
+        assert e.value.status == code, field
+    call = lambda ws, nbytes, q=F, kc=F: lib.dartree_tree_attention(ctypes.byref(p), q, kc, F, F, F, F, None, F, ws,
+                                                                    nbytes, None)
+    assert call(F, n - 1) == D.ERR_WORKSPACE
+    assert call(ctypes.c_void_p(FAKE + 16), n) == D.ERR_WORKSPACE
+    assert call(F, n, q=None) == D.ERR_INVALID_ARG
+    assert call(F, n, kc=None) == D.ERR_INVALID_ARG                 # context expected
+    assert call(F, n, q=ctypes.c_void_p(FAKE + 2)) == D.ERR_INVALID_ARG
