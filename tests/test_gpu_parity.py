@@ -54,6 +54,9 @@ SMALL = {
     "shared-fp32": small(precision=W.FP32, hidden=48, candidates=9, branch=9, sigma_w=0.1, seed=54),
     "shared-K-eq-V": small(vocab=40, candidates=40, branch=6, width=6, hidden=64, seed=55),
     "shared-k1": small(candidates=8, branch=1, budget=8, seed=56),
+    "shared-K64-two-row-blocks": small(batch=2, candidates=64, branch=8, width=80, budget=120, vocab=3001,
+                                       hidden=128, seed=58),   # 80 rows x 64 candidates
+
     # the Markov correction head (state = the last token's embedding)
     "markov-bf16": small(head=1, seed=58),
     "markov-shared": small(head=1, candidates=16, branch=16, width=12, budget=40, seed=59),
