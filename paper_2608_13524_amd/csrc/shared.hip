@@ -204,6 +204,14 @@ __global__ __launch_bounds__(1024) void shared_logits_bf16(int np, int K, int hi
   }
   // node-row tiles this block needs (block-uniform)
   const int ntile = min(kRowTiles, (np - 64 * rb + 15) / 16);
+  // wave 0 adds L^base at its lanes' four candidates: fetch them now, while
+  // the products run, rather than after the reduction
+  float lbv[4] = {0.f, 0.f, 0.f, 0.f};
+  if (wave == 0) {
+    const float* lbq = lb + g * lb_stride;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) lbv[i] = lbq[set[min(16 * cb + 4 * kg + i, K - 1)]];
+  }
   f32x4 acc[kRowTiles];
 #pragma unroll
   for (int t = 0; t < kRowTiles; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -221,7 +229,6 @@ __global__ __launch_bounds__(1024) void shared_logits_bf16(int np, int K, int hi
   for (int t = 0; t < kRowTiles; ++t) red[wave][t][lane] = acc[t];
   __syncthreads();
   if (wave != 0) return;
-  const float* lbq = lb + g * lb_stride;
   // lane holds D[candidate 4 kg + i][node row r16] of each tile; waves summed in order
 #pragma unroll
   for (int t = 0; t < kRowTiles; ++t) {
@@ -234,7 +241,7 @@ __global__ __launch_bounds__(1024) void shared_logits_bf16(int np, int K, int hi
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int cc = 16 * cb + 4 * kg + i;
-      if (cc < K) z[(int64_t(q) * np + j) * K + cc] = v[i] + lbq[set[cc]];
+      if (cc < K) z[(int64_t(q) * np + j) * K + cc] = v[i] + lbv[i];
     }
   }
 }

@@ -47,10 +47,13 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
   __shared__ uint64_t keys[kSortMax];
   __shared__ float c_logp[kSortMax];
   __shared__ int32_t c_ids[kSortMax];
+  __shared__ float ps[kSortMax];   // parent scores (n_parent <= n_parent k <= kSortMax), fetched early
   const int q = blockIdx.x / S, sl = blockIdx.x - q * S;
   const int np = a.n_parent, k = a.k;
   int n = np * k;
   const int64_t rbase = int64_t(q) * np;
+  for (int j = threadIdx.x; j < np; j += blockDim.x)
+    ps[j] = a.parent_score ? a.parent_score[int64_t(q) * a.parent_stride + j] : 0.f;
   if (a.shared_k > 0) {
     // shared candidate set: row j's K corrected logits over C_d -> log q~
     // normalised over C_d, and its k best by (z desc, id asc), ranked by
@@ -127,8 +130,7 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
   }
   __syncthreads();
   auto score_at = [&](int j, int r) {   // s of row j's candidate r, as in the keys below
-    const float sp = a.parent_score ? a.parent_score[int64_t(q) * a.parent_stride + j] : 0.f;
-    return (sp + c_logp[j * k + r]) + a.beta;
+    return (ps[j] + c_logp[j * k + r]) + a.beta;
   };
   // With rows in rank order, a row's candidates from position n_keep on have
   // scores <= its candidate n_keep's; if that is strictly below its candidate
