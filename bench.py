@@ -160,7 +160,7 @@ def time_consumer(torch, cfg, out, stream, reps: int = 50) -> dict:
     """The step after the path on the tree just built: one tree-attention
     layer of Qwen3-4B's shape over a 2048-position context (the target's
     verification pass reads the emitted mask) and the acceptance walk, each
-    the mean of `reps` launches bracketed by events."""
+    the mean of `reps` launches replayed from a HIP graph."""
     dev = out.tokens.device
     s = W.ATTENTION_QWEN3_4B
     ai = W.make_attention_inputs(cfg.batch, cfg.budget, s["max_ctx"], s["heads_q"], s["heads_kv"], seed=7)
@@ -177,12 +177,19 @@ def time_consumer(torch, cfg, out, stream, reps: int = 50) -> dict:
     bonus = torch.empty(cfg.batch, dtype=torch.int32, device=dev)
 
     def mean_us(fn):
+        # `reps` launches captured in one HIP graph and replayed, so the host's
+        # launch rate does not starve the device between these short kernels
         fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                fn()
+        g.replay()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         a.record(stream)
-        for _ in range(reps):
-            fn()
+        g.replay()
         b.record(stream)
         torch.cuda.synchronize()
         return a.elapsed_time(b) * 1e3 / reps

@@ -336,7 +336,7 @@ dartree_status dartree_accept_walk(int32_t batch, int32_t budget, int32_t max_le
 typedef struct dartree_attn_params {
   int32_t batch;     /* b requests */
   int32_t budget;    /* B tree slots per request (the rows of the emitted tree) */
-  int32_t max_ctx;   /* context positions held per request (>= 0) */
+  int32_t max_ctx;   /* context positions held per request, 0 .. 261888 (1023 segments of 256) */
   int32_t heads_q;   /* query heads, a multiple of heads_kv */
   int32_t heads_kv;  /* key/value heads; query head h reads key/value head h / (heads_q / heads_kv) */
   int32_t head_dim;  /* 128 */

@@ -725,6 +725,8 @@ dartree_status check_attn(const dartree_attn_params* p) {
   if (p->heads_q % p->heads_kv != 0 || !isfinite(p->scale) || p->scale <= 0.f) return DARTREE_ERR_INVALID_ARG;
   if (p->head_dim != 128 || p->budget > DARTREE_MAX_SORT) return DARTREE_ERR_UNSUPPORTED;
   if (int64_t(p->batch) * p->budget * p->heads_q > (int64_t(1) << 30)) return DARTREE_ERR_UNSUPPORTED;
+  const int64_t segs = (int64_t(p->max_ctx) + attention_segment_len() - 1) / attention_segment_len() + 1;
+  if (segs > attention_max_segments()) return DARTREE_ERR_UNSUPPORTED;
   return DARTREE_OK;
 }
 

@@ -187,6 +187,7 @@ struct AttnArgs {
   float* out;                   // fp32 [batch][budget][heads_q][128]
 };
 int attention_segment_len();
+int attention_max_segments();   // limit of context segments + 1
 hipError_t launch_tree_attention(const AttnArgs& a, hipStream_t s);
 hipError_t launch_heap_emit(const HeapArgs& a, const dartree_tree& out, hipStream_t s);
 

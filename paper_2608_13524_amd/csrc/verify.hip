@@ -119,26 +119,40 @@ __global__ __launch_bounds__(256) void tree_attention_part(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < kD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int kb = k0; kb < k1; kb += kKeys) {
-    // stage K [key][dim] (a wave covers 4 whole rows) and V^T [dim][key] (a
-    // wave covers 64 keys of one 8-dim slice, so its 2-byte stores spread over
-    // the banks); keys past k1 are zero, never read from memory
-    typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
-    __syncthreads();
-    for (int c = threadIdx.x; c < kKeys * kD / 8; c += 256) {
-      const int key = c / (kD / 8), d8 = (c % (kD / 8)) * 8;
-      u16x8 kv = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-      if (kb + key < k1) kv = *reinterpret_cast<const u16x8*>(kbase + (int64_t(kb + key) * a.heads_kv + kvh) * kD + d8);
-      *reinterpret_cast<u16x8*>(&Ks[key][d8]) = kv;
-    }
-    for (int c = threadIdx.x; c < kKeys * kD / 8; c += 256) {
-      const int key = c % kKeys, d8 = (c / kKeys) * 8;
-      u16x8 vv = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-      if (kb + key < k1) vv = *reinterpret_cast<const u16x8*>(vbase + (int64_t(kb + key) * a.heads_kv + kvh) * kD + d8);
+  // this thread's share of a 64-key step: 4 chunks of K (a wave covers 4
+  // whole rows) and 4 of V (a wave covers 64 keys of one 8-dim slice, so the
+  // transposed 2-byte stores spread over the banks); keys past k1 are zero,
+  // never read from memory.  The next step's share is loaded while the
+  // current one is multiplied.
+  typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+  constexpr int kChunks = kKeys * kD / 8 / 256;
+  u16x8 kn[kChunks], vn[kChunks];
+  auto load_step = [&](int kb) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[d8 + e][key] = vv[e];
+    for (int i = 0; i < kChunks; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      const int kk = c / (kD / 8), kd = (c % (kD / 8)) * 8;
+      const int vk = c % kKeys, vd = (c / kKeys) * 8;
+      kn[i] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+      vn[i] = kn[i];
+      if (kb + kk < k1) kn[i] = *reinterpret_cast<const u16x8*>(kbase + (int64_t(kb + kk) * a.heads_kv + kvh) * kD + kd);
+      if (kb + vk < k1) vn[i] = *reinterpret_cast<const u16x8*>(vbase + (int64_t(kb + vk) * a.heads_kv + kvh) * kD + vd);
+    }
+  };
+  if (k0 < k1) load_step(k0);
+
+  for (int kb = k0; kb < k1; kb += kKeys) {
+    __syncthreads();   // every wave is done with the previous step's tiles
+#pragma unroll
+    for (int i = 0; i < kChunks; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      *reinterpret_cast<u16x8*>(&Ks[c / (kD / 8)][(c % (kD / 8)) * 8]) = kn[i];
+      const int vk = c % kKeys, vd = (c / kKeys) * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Vt[vd + e][vk] = vn[i][e];
     }
     __syncthreads();
+    if (kb + kKeys < k1) load_step(kb + kKeys);
 
     // S[key][query] for the 4 key tiles of 16
     f32x4 s[4];
@@ -216,37 +230,50 @@ __global__ __launch_bounds__(256) void tree_attention_part(AttnArgs a) {
   for (int dt = 0; dt < kD / 16; ++dt) *reinterpret_cast<f32x4*>(op + dt * 16 + g * 4) = o[dt];
 }
 
-// grid: batch * budget * Hq, block kD: merge the segments of one query row.
-__global__ __launch_bounds__(kD) void tree_attention_merge(AttnArgs a) {
+// grid: batch * budget * ceil(heads_q / 8), block 1024: merge the segments
+// of 8 query heads of one node, one (head, dim) output per thread.  The
+// per-head segment weights w_s = exp2(m_s - M) / L go to LDS first; then
+// every output sums its segments' partial rows with independent loads.
+constexpr int kMergeHeads = 8;
+constexpr int kMergeThreads = kMergeHeads * kD;
+constexpr int kMaxSegments = 1024;   // limit of nseg = context segments + 1 (checked on the host)
+__global__ __launch_bounds__(kMergeThreads) void tree_attention_merge(AttnArgs a) {
+  __shared__ float w[kMaxSegments * kMergeHeads];   // [nseg][kMergeHeads]
   const int nseg = a.nseg_ctx + 1;
-  int bid = blockIdx.x;
-  const int head = bid % a.heads_q;
-  bid /= a.heads_q;
-  const int node = bid % a.budget;
-  const int q = bid / a.budget;
-  const int kvh = head / a.group, row = node * a.group + head % a.group;
-  float M = -INFINITY;
-  for (int s = 0; s < nseg; ++s) {
-    const int64_t pr = ((int64_t(s) * a.batch + q) * a.heads_kv + kvh) * a.rows_pad + row;
-    M = fmaxf(M, a.part_ml[pr * 2]);
-  }
-  float L = 0.f, acc = 0.f;
-  if (M != -INFINITY) {
-    for (int s = 0; s < nseg; ++s) {
-      const int64_t pr = ((int64_t(s) * a.batch + q) * a.heads_kv + kvh) * a.rows_pad + row;
-      const float m = a.part_ml[pr * 2];
-      if (m == -INFINITY) continue;
-      const float w = __builtin_amdgcn_exp2f(m - M);
-      L += w * a.part_ml[pr * 2 + 1];
-      acc += w * a.part_o[pr * kD + threadIdx.x];
+  const int nhg = (a.heads_q + kMergeHeads - 1) / kMergeHeads;
+  const int hg = blockIdx.x % nhg, node = (blockIdx.x / nhg) % a.budget, q = blockIdx.x / nhg / a.budget;
+  auto part = [&](int s, int head) {
+    const int kvh = head / a.group, row = node * a.group + head % a.group;
+    return ((int64_t(s) * a.batch + q) * a.heads_kv + kvh) * a.rows_pad + row;
+  };
+  if (threadIdx.x < kMergeHeads) {
+    const int head = hg * kMergeHeads + threadIdx.x;
+    if (head < a.heads_q) {
+      float M = -INFINITY;
+      for (int s = 0; s < nseg; ++s) M = fmaxf(M, a.part_ml[part(s, head) * 2]);
+      float L = 0.f;
+      for (int s = 0; s < nseg; ++s) {
+        const float m = a.part_ml[part(s, head) * 2];
+        const float ws = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - M);
+        w[s * kMergeHeads + threadIdx.x] = ws;
+        L += ws * a.part_ml[part(s, head) * 2 + 1];
+      }
+      const float inv = L > 0.f ? 1.f / L : 0.f;   // a row that sees nothing is zero
+      for (int s = 0; s < nseg; ++s) w[s * kMergeHeads + threadIdx.x] *= inv;
     }
   }
-  a.out[((int64_t(q) * a.budget + node) * a.heads_q + head) * kD + threadIdx.x] = L > 0.f ? acc / L : 0.f;
+  __syncthreads();
+  const int hl = threadIdx.x / kD, d = threadIdx.x % kD, head = hg * kMergeHeads + hl;
+  if (head >= a.heads_q) return;
+  float acc = 0.f;
+  for (int s = 0; s < nseg; ++s) acc += w[s * kMergeHeads + hl] * a.part_o[part(s, head) * kD + d];
+  a.out[((int64_t(q) * a.budget + node) * a.heads_q + head) * kD + d] = acc;
 }
 
 }  // namespace
 
 int attention_segment_len() { return 4 * kKeys; }
+int attention_max_segments() { return kMaxSegments; }
 
 hipError_t launch_accept_walk(int batch, int budget, int max_len, const int32_t* tokens, const int32_t* parents,
                               const int32_t* num_nodes, const int32_t* target, int32_t* accepted,
@@ -265,7 +292,8 @@ hipError_t launch_tree_attention(const AttnArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(tree_attention_part, dim3(parts), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(tree_attention_merge, dim3(unsigned(a.batch) * a.budget * a.heads_q), dim3(kD), 0, s, a);
+  const unsigned nhg = unsigned((a.heads_q + kMergeHeads - 1) / kMergeHeads);
+  hipLaunchKernelGGL(tree_attention_merge, dim3(unsigned(a.batch) * a.budget * nhg), dim3(kMergeThreads), 0, s, a);
   return hipGetLastError();
 }
 

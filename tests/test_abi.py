@@ -230,9 +230,12 @@ def test_consumer_rejects_bad_arguments():
     p = D.AttnParams(batch=1, budget=64, max_ctx=2048, heads_q=32, heads_kv=8, head_dim=128, scale=0.0884)
     n = D.tree_attention_workspace_size(p)
     assert n >= 9 * 8 * 256 * 128 * 4          # one partial row per segment, kv head and query row
+    edge = D.AttnParams(1, 64, 1023 * 256, 4, 1, 128, 0.0884)
+    assert D.tree_attention_workspace_size(edge) > 0   # 1023 context segments + the tree: the limit
     for field, value, code in (("head_dim", 64, D.ERR_UNSUPPORTED), ("heads_q", 30, D.ERR_INVALID_ARG),
                                ("scale", 0.0, D.ERR_INVALID_ARG), ("budget", 0, D.ERR_INVALID_ARG),
-                               ("max_ctx", -1, D.ERR_INVALID_ARG), ("budget", 4097, D.ERR_UNSUPPORTED)):
+                               ("max_ctx", -1, D.ERR_INVALID_ARG), ("budget", 4097, D.ERR_UNSUPPORTED),
+                               ("max_ctx", 1023 * 256 + 1, D.ERR_UNSUPPORTED)):
         bad = D.AttnParams(1, 64, 2048, 32, 8, 128, 0.0884)
         setattr(bad, field, value)
         with pytest.raises(D.DartreeError) as e:
