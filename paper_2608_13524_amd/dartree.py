@@ -21,6 +21,8 @@ HEAD_MARKOV = 1
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 
+ABI_VERSION = 6   # DARTREE_ABI_VERSION of include/dartree.h this binding follows
+
 MAX_VOCAB = 1 << 20
 MAX_DEPTH = 64
 MAX_WIDTH = 2048

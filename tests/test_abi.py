@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert D.abi_version() == 6
+    assert D.abi_version() == D.ABI_VERSION == 6
     for s in range(5):
         assert D.status_string(s)
     assert D.status_string(99) == "unknown status"
