@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define DARTREE_ABI_VERSION 6
+#define DARTREE_ABI_VERSION 7
 
 /* Limits of this implementation (calls beyond them return
  * DARTREE_ERR_UNSUPPORTED). */
@@ -218,15 +218,26 @@ dartree_status dartree_export_states(const dartree_params* p, const void* ws, si
  * The kernels of one depth, exposed for callers that assemble their own loop
  * (and for testing each step on injected inputs). */
 
+/* Bytes of device scratch dartree_project needs for this shape (host only;
+ * 0 for shapes that never split a tile along K). */
+dartree_status dartree_project_workspace_size(int32_t precision, int32_t rows, int32_t vocab, int32_t hidden,
+                                              size_t* bytes);
+
 /* Corrected logits (Algorithm 1, "correct all prefixes ... in parallel"):
  * z[m][v] = bias[m / rows_per_group][v] + sum_i x[m][i] U[v][i]
  * for m < rows, v < vocab.  x: act [rows][hidden]; U: act [vocab][hidden];
  * bias: fp32 rows of length vocab, row g at bias + g * bias_stride (elements);
- * z: fp32 [rows][vocab].  precision as in dartree_params. */
+ * z: fp32 [rows][vocab].  precision as in dartree_params.
+ * ws/ws_bytes: device scratch of dartree_project_workspace_size bytes
+ * (256-byte aligned; may be NULL when that size is 0, else
+ * DARTREE_ERR_WORKSPACE).  With bf16 and >= 512 rows the output tiles of a
+ * last partial wave over the compute units are split along K and their
+ * partial sums added in a fixed order, so the result is deterministic for a
+ * given device (the split depends on its number of compute units). */
 dartree_status dartree_project(int32_t precision, int32_t rows, int32_t vocab, int32_t hidden,
                                int32_t rows_per_group, const void* x, const void* U,
                                const float* bias, int64_t bias_stride, float* z,
-                               hipStream_t stream);
+                               void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Row-wise log-softmax normaliser and top-k of z / tau (tau = T if T > 0 else 1):
  * lse[m] = log sum_v exp(z[m][v] / tau); cand_ids[m][0..k) are the k best ids

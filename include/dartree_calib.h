@@ -8,7 +8,9 @@
  *     which reads every row of U once per depth),
  *   - a plain device-to-device copy (also the known-size reference that
  *     converts hardware byte counters into bytes),
- *   - a register-only loop of bf16 matrix-core instructions.
+ *   - a register-only loop of bf16 matrix-core instructions on pseudo-random
+ *     operands (the sustained matrix-core rate depends on the operand bits:
+ *     power limits the clock, and random operands draw the most).
  * They compute nothing of the method.  Conventions as in dartree.h: caller-
  * owned device memory, work enqueued on `stream`, arguments validated before
  * anything is enqueued (DARTREE_ERR_INVALID_ARG otherwise).

@@ -49,17 +49,25 @@ Shape shape_of(const dartree_params& p) {
 //   state: act [2][R][h]   t: f32 [R][h]   a: act [R][h]   z: f32 [R][V]
 //   k3: the row-split partials of the largest depth
 //   cset: i32 [b][L][K] shared candidate sets and their chunk winners (K > 0)
+//   split: partial sums of the projection tiles split along K (the head and
+//          the logits of one depth run one after the other and share it)
 struct Layout {
-  size_t lvl_tok, lvl_par, lvl_score, lse, cand_logp, cand_ids, state0, state1, t, a, z, k3, cset, cset_scratch, total;
+  size_t lvl_tok, lvl_par, lvl_score, lse, cand_logp, cand_ids, state0, state1, t, a, z, k3, cset, cset_scratch,
+      split, split_bytes, total;
 };
 
 Layout layout_of(const dartree_params& p, const Shape& s) {
   const size_t L = p.depth, b = p.batch, W = p.width, k = p.branch, h = p.hidden, V = p.vocab;
   const size_t R = b * W;
   const size_t K = size_t(p.candidates);
-  size_t k3 = 0;
+  size_t k3 = 0, split = 0;
   if (K == 0)
     for (int d = 1; d <= p.depth; ++d) k3 = std::max(k3, lse_topk_scratch_bytes(int64_t(b) * s.n[d - 1], V, int(k)));
+  for (int d = 1; d <= p.depth; ++d) {
+    const int64_t rows = int64_t(b) * s.n[d - 1];
+    split = std::max(split, proj_split_bytes(p.precision, EPI_HEAD, rows, int64_t(h), int64_t(h)));
+    if (K == 0) split = std::max(split, proj_split_bytes(p.precision, EPI_LOGITS, rows, int64_t(V), int64_t(h)));
+  }
   Layout l{};
   size_t o = 0;
   auto take = [&](size_t bytes) { const size_t at = o; o = align_up(o + bytes); return at; };
@@ -77,6 +85,8 @@ Layout layout_of(const dartree_params& p, const Shape& s) {
   l.k3 = take(k3);
   l.cset = take(b * L * K * 4);
   l.cset_scratch = take(K > 0 ? candidate_sets_scratch_bytes(int64_t(b) * L, V, int(K)) : 0);
+  l.split = take(split);
+  l.split_bytes = split;
   l.total = o;
   return l;
 }
@@ -270,6 +280,7 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   head.bias_stride = L * h;
   head.out = t;
   head.act_out = a;
+  head.split = l.split_bytes ? at<float>(ws, l.split) : nullptr;
   tm.mark(tb + DARTREE_KERNEL_HEAD, 0);
   hipError_t err = launch_project(head, st);
   tm.mark(tb + DARTREE_KERNEL_HEAD, 1);
@@ -290,6 +301,7 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   lg.bias_f32 = in.drafter_logits + size_t(d - 1) * V;
   lg.bias_stride = L * V;
   lg.out = z;
+  lg.split = l.split_bytes ? at<float>(ws, l.split) : nullptr;
   tm.mark(tb + DARTREE_KERNEL_LOGITS, 0);
   err = launch_project(lg, st);
   tm.mark(tb + DARTREE_KERNEL_LOGITS, 1);
@@ -605,13 +617,25 @@ dartree_status dartree_export_states(const dartree_params* p, const void* ws, si
   return hip_status(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, stream));
 }
 
+dartree_status dartree_project_workspace_size(int32_t precision, int32_t rows, int32_t vocab, int32_t hidden,
+                                              size_t* bytes) {
+  if (!bytes) return DARTREE_ERR_INVALID_ARG;
+  if (precision != DARTREE_FP32 && precision != DARTREE_BF16) return DARTREE_ERR_INVALID_ARG;
+  if (rows < 1 || vocab < 1 || hidden < 1) return DARTREE_ERR_INVALID_ARG;
+  *bytes = proj_split_bytes(precision, EPI_LOGITS, rows, vocab, hidden);
+  return DARTREE_OK;
+}
+
 dartree_status dartree_project(int32_t precision, int32_t rows, int32_t vocab, int32_t hidden, int32_t rows_per_group,
                                const void* x, const void* U, const float* bias, int64_t bias_stride, float* z,
-                               hipStream_t stream) {
+                               void* ws, size_t ws_bytes, hipStream_t stream) {
   if (precision != DARTREE_FP32 && precision != DARTREE_BF16) return DARTREE_ERR_INVALID_ARG;
   if (rows < 1 || vocab < 1 || hidden < 1 || rows_per_group < 1 || bias_stride < 0) return DARTREE_ERR_INVALID_ARG;
   if (!x || !U || !bias || !z || !aligned16(x) || !aligned16(U) || !aligned16(z)) return DARTREE_ERR_INVALID_ARG;
   if (precision == DARTREE_BF16 && hidden % 64 != 0) return DARTREE_ERR_UNSUPPORTED;
+  const size_t need = proj_split_bytes(precision, EPI_LOGITS, rows, vocab, hidden);
+  if (need > 0 && (!ws || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0 || ws_bytes < need))
+    return DARTREE_ERR_WORKSPACE;
   ProjArgs a{};
   a.precision = precision;
   a.epilogue = EPI_LOGITS;
@@ -624,6 +648,7 @@ dartree_status dartree_project(int32_t precision, int32_t rows, int32_t vocab, i
   a.bias_f32 = bias;
   a.bias_stride = bias_stride;
   a.out = z;
+  a.split = need > 0 ? static_cast<float*>(ws) : nullptr;
   return hip_status(launch_project(a, stream));
 }
 

@@ -53,11 +53,28 @@ __global__ __launch_bounds__(kThreads) void calib_copy(f32x4* __restrict__ dst, 
 }
 
 // Register-only bf16 MFMA loop: an 8 x 8 grid of independent accumulators
-// per wave (64 products per round), one wave per SIMD.
-__device__ __forceinline__ bf16x8 calib_operand(int lane, int shift, int mul, float unit) {
+// per wave (64 products per round), one wave per SIMD.  The operands are
+// pseudo-random bf16 values (random sign, exponent 2^-8 .. 2^-1, random
+// mantissa), like the activations and weights the projection multiplies: the
+// matrix cores' power, and with it the clock the chip sustains, grows with the
+// number of operand bits that toggle, and operands with few mantissa bits set
+// run about a fifth faster than random ones.
+__device__ __forceinline__ uint32_t calib_mix(uint32_t h) {
+  h ^= h >> 15;
+  h *= 0x2C1B3C6Du;
+  h ^= h >> 12;
+  h *= 0x297A2D39u;
+  h ^= h >> 15;
+  return h;
+}
+__device__ __forceinline__ bf16x8 calib_operand(int lane, int slot) {
   bf16x8 v;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) v[j] = __bf16(float((lane * mul + j + shift) & 7) * unit);
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t h = calib_mix(uint32_t((slot * 64 + lane) * 8 + j) * 0x9E3779B1u + 0x3C6EF372u);
+    const uint32_t bits = ((h >> 31) << 15) | ((119u + (h >> 8) % 8u) << 7) | (h & 0x7Fu);
+    v[j] = __builtin_bit_cast(__bf16, uint16_t(bits));
+  }
   return v;
 }
 
@@ -66,8 +83,8 @@ __global__ __launch_bounds__(kThreads) void calib_mfma(int iters, float* sink) {
   bf16x8 a[8], b[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    a[i] = calib_operand(lane, i, 1, 0.125f);
-    b[i] = calib_operand(lane, i, 3, 0.0625f);
+    a[i] = calib_operand(lane, i);
+    b[i] = calib_operand(lane, 8 + i);
   }
   f32x4 c[8][8];
 #pragma unroll

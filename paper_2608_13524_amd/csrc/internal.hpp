@@ -57,8 +57,12 @@ struct ProjArgs {
   const int32_t* group_index;  // optional device [M / rows_per_group]: bias row of each group
   float* out;            // fp32 [M][N]
   void* act_out;         // EPI_HEAD: act [M][N]
+  float* split;          // optional device scratch of proj_split_bytes(...) bytes: partial sums of
+                         // tiles split along K (without it no tile is split)
 };
 hipError_t launch_project(const ProjArgs& a, hipStream_t s);
+// Scratch the product of this shape can use to split tiles along K (0 if none).
+size_t proj_split_bytes(int precision, int epilogue, int64_t M, int64_t N, int64_t K);
 
 // Row-wise online log-sum-exp and top-k (K3).  Rows are split into
 // lse_topk_segments(rows, vocab) segments; with more than one, each segment

@@ -10,13 +10,18 @@
 //    weight matrix (U is 0.78-1.56 GB per depth, far beyond the caches), so
 //    every weight element is read once from HBM with coalesced non-temporal
 //    loads and staged through LDS into MFMA operand layout.
-//  * proj_bf16_big: many rows (>= 512) against the vocabulary.  256x256 tiles,
+//  * proj_bf16_big: many rows (>= 512) against the vocabulary, and the head at
+//    >= 512 rows when its tiles are too few to fill the chip.  256x256 tiles,
 //    8 waves in two groups alternating LDS reads and MFMAs, buffer loads
-//    straight to swizzled LDS, XCD-aware tile order.
+//    straight to swizzled LDS, XCD-aware tile order; the tiles of a last
+//    partial wave are split along K into pieces whose partial sums a fix-up
+//    kernel adds in piece order.
 //  * proj_bf16_tiled: other many-row products (the head, or a few hundred
 //    rows).  128x128 output tiles, 64-deep K steps staged through
 //    double-buffered, padded LDS tiles shared by 4 waves (64x64 each).
 // fp32 path: plain FMA loop (small problems only).
+#include <algorithm>
+
 #include "internal.hpp"
 
 namespace dartree {
@@ -314,49 +319,103 @@ __global__ __launch_bounds__(256) void proj_bf16_tiled(KArgs a) {
 // alternate between a memory phase (reading the operand fragments of one
 // 64-deep K step from LDS) and a compute phase (the 64 MFMAs of that step),
 // one phase apart, so each SIMD always has one wave issuing MFMAs; a barrier
-// ends every phase.  Group 0 moves the K steps into double-buffered LDS with
-// buffer loads straight to LDS (XOR-swizzled rows: conflict-free for the
-// MFMA-layout reads): step s + 1 at the start of its memory phase for step s,
-// into the buffer of step s - 1, which both groups have finished reading.
-// Every wave executes the same number of barriers (2 nk + 2).  The ragged
+// ends every phase.  Group 0 moves the K steps into LDS with buffer loads
+// straight to LDS (XOR-swizzled rows: conflict-free for the MFMA-layout
+// reads).  The weight rows stream from HBM and get three LDS stages: step
+// s + 2 is issued at the start of the memory phase for step s, into the stage
+// of step s - 1, which both groups have finished reading, so each load has two
+// steps to land.  The node rows (cache-resident: every weight tile reuses
+// them) get two stages and are issued one step ahead.  3 x 32 KB + 2 x 32 KB
+// fill the 160 KB of LDS.  Every wave executes the same number of barriers
+// (2 nk + 2).  The ragged
 // last tile along M or N is shifted back to end at the matrix edge, so every
 // loaded row exists; that block stores only the rows the previous tile did
 // not cover.  Tiles are ordered so that the blocks of one XCD (blocks are
 // dealt to the 8 XCDs round-robin) cover the M-tiles of one weight tile,
 // which then stays in that XCD's L2.
+//
+// One block per CU fits (160 KB of LDS), so T tiles run in ceil(T / CUs)
+// waves and a last partial wave of r tiles leaves the other CUs idle.  Those
+// r tiles are split along K into S = min(CUs / r, steps / 4) pieces: block
+// (tile, piece) multiplies its contiguous range of K steps and stores the raw
+// 256x256 fp32 partial sum; proj_big_fixup then adds the S partials of every
+// element in piece order (deterministic) and applies the epilogue.
 // ---------------------------------------------------------------------------
 constexpr int GBM = 256, GBN = 256, GBK = 64;
 #define LDS_AS __attribute__((address_space(3)))
 
 __device__ __forceinline__ int swz16(int r) { return (r ^ (r >> 3)) & 7; }  // r in 0..15
 
-__global__ __launch_bounds__(512) void proj_bf16_big(KArgs a, int vec) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2][(GBN + GBM) * GBK];  // [buf][W rows | X rows]
+// Tiles [0, full) whole; tiles [full, full + rem) in `pieces` K pieces whose
+// partial sums go to split[(r * pieces + piece) * 256 * 256 ..] (row-major
+// 256 x 256 fp32 relative to the tile's loaded origin).
+struct BigPlan {
+  int full, rem, pieces;
+  float* split;
+};
+
+// Output origin (m0, n0) of tile t (N-tile major, M-tile minor) and the origin
+// (ml, nl) of the rows it loads: the ragged last tile is shifted back to end
+// at the matrix edge (M, N >= 256).
+struct BigTile {
+  int m0, n0, ml, nl;
+};
+__device__ __forceinline__ BigTile big_tile(int M, int N, int t) {
+  const int ntm = (M + GBM - 1) / GBM;
+  BigTile b;
+  b.n0 = (t / ntm) * GBN;
+  b.m0 = (t % ntm) * GBM;
+  b.nl = min(b.n0, N - GBN);
+  b.ml = min(b.m0, M - GBM);
+  return b;
+}
+
+// Work item of block b among n: XCD x (b % 8) gets the contiguous run
+// [x q8, (x + 1) q8), q8 = n / 8, so its blocks share operand rows in its L2.
+__device__ __forceinline__ int xcd_order(int b, int n) {
+  const int q8 = n / 8;
+  return b < 8 * q8 ? (b % 8) * q8 + b / 8 : b;
+}
+
+template <int EPI>
+__global__ __launch_bounds__(512) void proj_bf16_big(KArgs a, int vec, BigPlan pl) {
+  constexpr int kStage = GBN * GBK;  // elements of one 256-row, 64-deep stage
+  __shared__ __attribute__((aligned(16))) uint16_t smem[5 * kStage];  // W stages 0..2, X stages 0..1
   const int lane = threadIdx.x & 63, r16 = lane & 15, kg = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int grp = wave >> 2, q = wave & 3;
   const int M = a.M, N = a.N, K = a.K;
-  const int ntm = (M + GBM - 1) / GBM, ntn = (N + GBN - 1) / GBN, T = ntm * ntn;
-  int t = blockIdx.x;
-  const int q8 = T / 8;
-  if (t < 8 * q8) t = (t % 8) * q8 + t / 8;
-  const int n0 = (t / ntm) * GBN, m0 = (t % ntm) * GBM;
-  const int nl = min(n0, N - GBN), ml = min(m0, M - GBM);  // loaded tile origin (M, N >= 256)
+  const int nk_all = K / GBK;
+  int t, ks = 0, nk = nk_all, slot = -1;  // K steps [ks, ks + nk); slot >= 0: a piece of a split tile
+  if (int(blockIdx.x) < pl.full) {
+    t = xcd_order(blockIdx.x, pl.full);
+  } else {
+    // pieces ordered piece-major, so the M-tiles of one weight tile at one
+    // piece are consecutive items (and land on one XCD)
+    const int item = xcd_order(int(blockIdx.x) - pl.full, pl.rem * pl.pieces);
+    const int piece = item / pl.rem, r = item % pl.rem;
+    t = pl.full + r;
+    ks = piece * nk_all / pl.pieces;
+    nk = (piece + 1) * nk_all / pl.pieces - ks;
+    slot = r * pl.pieces + piece;
+  }
+  const BigTile tl = big_tile(M, N, t);
+  const int m0 = tl.m0, n0 = tl.n0, ml = tl.ml, nl = tl.nl;
   const uint16_t* X = static_cast<const uint16_t*>(a.x);
   const uint16_t* Wt = static_cast<const uint16_t*>(a.w);
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(Wt + int64_t(nl) * K), (short)0, GBN * K * 2, 0x00020000);
   const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(X + int64_t(ml) * K), (short)0, GBM * K * 2, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rs = q < 2 ? rw : rx;
-  // group 0 wave q moves stage rows [128 q, +128) (weight rows for q < 2, node
-  // rows otherwise), 8 rows per load: lane / 8 is the row, LDS chunk lane % 8
-  // holds global chunk (lane % 8) ^ swizzle(row)
+  const bool wload = q < 2;
+  const __amdgpu_buffer_rsrc_t rs = wload ? rw : rx;
+  // group 0 wave q moves rows [128 (q % 2), +128) of the weight stage (q < 2)
+  // or of the node stage, 8 rows per load: lane / 8 is the row, LDS chunk
+  // lane % 8 holds global chunk (lane % 8) ^ swizzle(row)
   const int lrow = lane >> 3, lcp = lane & 7;
   const unsigned vo0 = unsigned(lrow * K * 2 + ((lcp ^ swz16(lrow)) * 16));
   const unsigned vo1 = unsigned(lrow * K * 2 + ((lcp ^ swz16(8 + lrow)) * 16));
   const int sw = swz16(r16);
-  const int nk = K / GBK;
 
   f32x4 acc[4][8];
 #pragma unroll
@@ -364,28 +423,30 @@ __global__ __launch_bounds__(512) void proj_bf16_big(KArgs a, int vec) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto dma = [&](int buf, int kt) {
-    LDS_AS uint16_t* base = (LDS_AS uint16_t*)smem[buf] + 128 * q * GBK;  // generic -> LDS address space
+  auto dma = [&](int kt) {
+    const int stage = wload ? kt % 3 : 3 + (kt & 1);
+    LDS_AS uint16_t* base = (LDS_AS uint16_t*)smem + stage * kStage + 128 * (q & 1) * GBK;  // generic -> LDS
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const unsigned so = unsigned((128 * (q & 1) + 8 * i) * K * 2 + kt * GBK * 2);
+      const unsigned so = unsigned((128 * (q & 1) + 8 * i) * K * 2 + (ks + kt) * GBK * 2);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (LDS_AS void*)(base + 8 * i * GBK), 16, (i & 1) ? vo1 : vo0, so, 0,
                                                0);
     }
   };
   bf16x8 A[2][4], B[2][8];
-  auto fetch = [&](int buf) {
-    const LDS_AS uint16_t* S = (const LDS_AS uint16_t*)smem[buf];
+  auto fetch = [&](int st) {
+    const LDS_AS uint16_t* Sw = (const LDS_AS uint16_t*)smem + (st % 3) * kStage;
+    const LDS_AS uint16_t* Sx = (const LDS_AS uint16_t*)smem + (3 + (st & 1)) * kStage;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int c = ((4 * h + kg) ^ sw) * 8;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        A[h][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const LDS_AS u32x4*>(S + (64 * q + 16 * i + r16) * GBK + c));
+        A[h][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const LDS_AS u32x4*>(Sw + (64 * q + 16 * i + r16) * GBK + c));
 #pragma unroll
       for (int j = 0; j < 8; ++j)
         B[h][j] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const LDS_AS u32x4*>(S + GBN * GBK + (128 * grp + 16 * j + r16) * GBK + c));
+            bf16x8, *reinterpret_cast<const LDS_AS u32x4*>(Sx + (128 * grp + 16 * j + r16) * GBK + c));
     }
   };
   auto compute = [&]() {
@@ -404,32 +465,37 @@ __global__ __launch_bounds__(512) void proj_bf16_big(KArgs a, int vec) {
   auto wait_loads = [] { __builtin_amdgcn_s_waitcnt(0x0F70); };      // vmcnt(0)
 
   if (grp == 0) {
-    dma(0, 0);
-    if (nk > 1) {
-      dma(1, 1);
-      __builtin_amdgcn_s_waitcnt(0x4F70);  // vmcnt(16): step 0 landed, step 1 in flight
-    } else {
-      wait_loads();
-    }
+    // weights: steps 0..2 into their three stages, nodes: steps 0..1; wait for
+    // step 0 with the later ones (16 loads each) still in flight
+    const int ahead = min(wload ? 2 : 1, nk - 1);
+    for (int kt = 0; kt <= ahead; ++kt) dma(kt);
+    if (ahead == 2) __builtin_amdgcn_s_waitcnt(0x8F70);       // vmcnt(32)
+    else if (ahead == 1) __builtin_amdgcn_s_waitcnt(0x4F70);  // vmcnt(16)
+    else wait_loads();
   }
   barrier();  // step 0 in LDS
   if (grp == 0) {
     for (int st = 0; st < nk; ++st) {
-      if (st >= 1 && st + 1 < nk) dma((st + 1) & 1, st + 1);
-      fetch(st & 1);
+      if (st >= 1) {
+        const int kt = st + (wload ? 2 : 1);
+        if (kt < nk) dma(kt);
+      }
+      fetch(st);
       wait_lds_reads();
       barrier();  // end of phase 2 st
       __builtin_amdgcn_sched_barrier(0);
       compute();
       __builtin_amdgcn_sched_barrier(0);
-      if (st + 1 < nk) wait_loads();  // this wave's share of step st + 1 landed
-      barrier();                      // end of phase 2 st + 1
+      // this wave's share of step st + 1 landed (a weight wave may keep step st + 2 in flight)
+      if (wload && st + 2 < nk) __builtin_amdgcn_s_waitcnt(0x4F70);  // vmcnt(16)
+      else if (st + 1 < nk) wait_loads();
+      barrier();  // end of phase 2 st + 1
     }
     barrier();  // phase 2 nk: group 1 multiplies the last step
   } else {
     barrier();  // phase 0: group 0 reads step 0
     for (int st = 0; st < nk; ++st) {
-      fetch(st & 1);
+      fetch(st);
       wait_lds_reads();
       barrier();  // end of phase 2 st + 1
       __builtin_amdgcn_sched_barrier(0);
@@ -440,6 +506,15 @@ __global__ __launch_bounds__(512) void proj_bf16_big(KArgs a, int vec) {
   }
 
   // lane holds D[n = 4 kg + e][m = r16] of each 16x16 sub-tile
+  if (slot >= 0) {
+    float* P = pl.split + size_t(slot) * (GBM * GBN);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        *reinterpret_cast<f32x4*>(P + (128 * grp + 16 * j + r16) * GBN + 64 * q + 16 * i + 4 * kg) = acc[i][j];
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -448,13 +523,40 @@ __global__ __launch_bounds__(512) void proj_bf16_big(KArgs a, int vec) {
       const int n = nl + 64 * q + 16 * i + 4 * kg;
       if (m < m0) continue;
       if (n >= n0) {
-        emit4<EPI_LOGITS>(a, m, n, acc[i][j], vec != 0);
+        emit4<EPI>(a, m, n, acc[i][j], vec != 0);
       } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          if (n + e >= n0) emit<EPI_LOGITS, true>(a, m, n + e, acc[i][j][e]);
+          if (n + e >= n0) emit<EPI, true>(a, m, n + e, acc[i][j][e]);
       }
     }
+}
+
+// The split tiles: 16 blocks per tile, each 16 rows x 256 columns; every
+// thread sums the pieces of 4 float4s in piece order and applies the epilogue.
+template <int EPI>
+__global__ __launch_bounds__(256) void proj_big_fixup(KArgs a, int vec, BigPlan pl) {
+  const int r = blockIdx.x / 16, row0 = (blockIdx.x % 16) * 16;
+  const BigTile tl = big_tile(a.M, a.N, pl.full + r);
+  const float* P = pl.split + size_t(r) * pl.pieces * (GBM * GBN);
+  const int c4 = threadIdx.x & 63;
+  const int n = tl.nl + 4 * c4;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int row = row0 + (threadIdx.x >> 6) + 4 * u;
+    const int m = tl.ml + row;
+    if (m < tl.m0) continue;
+    const size_t e = size_t(row) * GBN + 4 * c4;
+    f32x4 v = *reinterpret_cast<const f32x4*>(P + e);
+    for (int pc = 1; pc < pl.pieces; ++pc) v += *reinterpret_cast<const f32x4*>(P + size_t(pc) * (GBM * GBN) + e);
+    if (n >= tl.n0) {
+      emit4<EPI>(a, m, n, v, vec != 0);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (n + k >= tl.n0) emit<EPI, true>(a, m, n + k, v[k]);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -504,7 +606,60 @@ hipError_t launch_stream_nt(const KArgs& k, int epi, hipStream_t s) {
   return launch_stream<MT, 1, 8, 2>(k, epi, s);
 }
 
+// Split plan limits: at most kSplitMaxBlocks pieces (one 256 KB partial each),
+// and at least kMinPieceSteps 64-deep K steps per piece.
+constexpr int kSplitMaxBlocks = 256;
+constexpr int kMinPieceSteps = 4;
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return kSplitMaxBlocks;
+  if (dev < 64 && cached[dev] > 0) return cached[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    n = kSplitMaxBlocks;
+  if (dev < 64) cached[dev] = n;
+  return n;
+}
+
+// Shapes the 256x256-tile kernel takes: the vocabulary at >= 512 rows, and
+// (only when split) the head at >= 512 rows.
+bool big_logits(const KArgs& k) { return k.M >= 2 * GBM && k.N >= 64 * GBN; }
+bool big_head_candidate(const KArgs& k) { return k.M >= 2 * GBM && k.N >= GBN && k.K >= 2 * kMinPieceSteps * GBK; }
+
+BigPlan big_plan(const KArgs& k, float* split) {
+  const int T = ((k.M + GBM - 1) / GBM) * ((k.N + GBN - 1) / GBN);
+  BigPlan pl{T, 0, 1, nullptr};
+  if (!split) return pl;
+  const int ncu = std::min(device_cus(), kSplitMaxBlocks);
+  const int rem = T % ncu;
+  if (rem == 0) return pl;
+  const int pieces = std::min(ncu / rem, (k.K / GBK) / kMinPieceSteps);
+  if (pieces < 2) return pl;
+  return BigPlan{T - rem, rem, pieces, split};
+}
+
+template <int EPI>
+hipError_t launch_big(const KArgs& k, const BigPlan& pl, hipStream_t s) {
+  const int vec = epilogue_vec_ok(k, EPI);
+  hipLaunchKernelGGL((proj_bf16_big<EPI>), dim3(pl.full + pl.rem * pl.pieces), dim3(512), 0, s, k, vec, pl);
+  if (pl.rem > 0) hipLaunchKernelGGL((proj_big_fixup<EPI>), dim3(pl.rem * 16), dim3(256), 0, s, k, vec, pl);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+size_t proj_split_bytes(int precision, int epilogue, int64_t M, int64_t N, int64_t K) {
+  if (precision != DARTREE_BF16 || M <= 0 || N <= 0 || K <= 0 || M > INT32_MAX || N > INT32_MAX) return 0;
+  KArgs k{};
+  k.M = int(M);
+  k.N = int(N);
+  k.K = int(K);
+  const bool big = epilogue == EPI_LOGITS ? big_logits(k) : big_head_candidate(k);
+  return big ? size_t(kSplitMaxBlocks) * GBM * GBN * sizeof(float) : 0;
+}
 
 hipError_t launch_project(const ProjArgs& p, hipStream_t s) {
   KArgs k;
@@ -533,10 +688,10 @@ hipError_t launch_project(const ProjArgs& p, hipStream_t s) {
   if (k.M <= 32) return launch_stream_nt<2>(k, p.epilogue, s);
   if (k.M <= 48) return launch_stream_nt<3>(k, p.epilogue, s);
   if (k.M <= 64) return launch_stream_nt<4>(k, p.epilogue, s);
-  if (p.epilogue == EPI_LOGITS && k.M >= 2 * GBM && k.N >= 64 * GBN) {
-    const int tiles = ((k.M + GBM - 1) / GBM) * ((k.N + GBN - 1) / GBN);
-    hipLaunchKernelGGL(proj_bf16_big, dim3(tiles), dim3(512), 0, s, k, int(epilogue_vec_ok(k, EPI_LOGITS)));
-    return hipGetLastError();
+  if (p.epilogue == EPI_LOGITS && big_logits(k)) return launch_big<EPI_LOGITS>(k, big_plan(k, p.split), s);
+  if (p.epilogue == EPI_HEAD && big_head_candidate(k)) {
+    const BigPlan pl = big_plan(k, p.split);
+    if (pl.rem > 0) return launch_big<EPI_HEAD>(k, pl, s);
   }
   const dim3 grid((k.M + TBM - 1) / TBM, (k.N + TBN - 1) / TBN);
   if (p.epilogue == EPI_LOGITS) hipLaunchKernelGGL((proj_bf16_tiled<EPI_LOGITS>), grid, dim3(256), 0, s, k);

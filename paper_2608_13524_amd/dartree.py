@@ -21,7 +21,7 @@ HEAD_MARKOV = 1
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 
-ABI_VERSION = 6   # DARTREE_ABI_VERSION of include/dartree.h this binding follows
+ABI_VERSION = 7   # DARTREE_ABI_VERSION of include/dartree.h this binding follows
 
 MAX_VOCAB = 1 << 20
 MAX_DEPTH = 64
@@ -35,6 +35,7 @@ SYMBOLS = [
     "dartree_abi_version", "dartree_status_string", "dartree_validate",
     "dartree_workspace_size", "dartree_expand_depth", "dartree_prune",
     "dartree_build_tree", "dartree_build_tree_timed", "dartree_export_supertree", "dartree_export_states", "dartree_project",
+    "dartree_project_workspace_size",
     "dartree_lse_topk_workspace_size", "dartree_lse_topk", "dartree_select_topw",
     "dartree_prune_levels", "dartree_candidate_sets_workspace_size", "dartree_candidate_sets",
     "dartree_heap_workspace_size", "dartree_build_tree_heap", "dartree_export_heap",
@@ -129,7 +130,8 @@ def lib() -> ctypes.CDLL:
                                            ctypes.POINTER(vp), vp]
     L.dartree_export_supertree.argtypes = [P, vp, sz, ctypes.POINTER(SupertreeC), vp]
     L.dartree_export_states.argtypes = [P, vp, sz, i32, vp, vp]
-    L.dartree_project.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, i64, vp, vp]
+    L.dartree_project.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, i64, vp, vp, sz, vp]
+    L.dartree_project_workspace_size.argtypes = [i32, i32, i32, i32, ctypes.POINTER(sz)]
     L.dartree_lse_topk_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(sz)]
     L.dartree_lse_topk.argtypes = [vp, i32, i32, i32, f32, vp, vp, vp, vp, sz, vp]
     L.dartree_select_topw.argtypes = [i32, i32, i32, i32, f32, vp, vp, vp, vp, vp, vp, vp]
@@ -402,11 +404,19 @@ def export_states(p: Params, ws, d: int, dst, stream=None) -> None:
            "dartree_export_states")
 
 
-def project(precision: int, x, U, bias, bias_stride: int, z, rows_per_group: int, stream=None) -> None:
+def project_workspace_size(precision: int, rows: int, vocab: int, hidden: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().dartree_project_workspace_size(precision, rows, vocab, hidden, ctypes.byref(n)),
+           "dartree_project_workspace_size")
+    return n.value
+
+
+def project(precision: int, x, U, bias, bias_stride: int, z, rows_per_group: int, ws=None, stream=None) -> None:
     rows, hidden = x.shape
     vocab = U.shape[0]
     _check(lib().dartree_project(precision, rows, vocab, hidden, rows_per_group, _ptr(x), _ptr(U), _ptr(bias),
-                                 bias_stride, _ptr(z), _stream(stream)), "dartree_project")
+                                 bias_stride, _ptr(z), _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)),
+           "dartree_project")
 
 
 def lse_topk(z, k: int, temperature: float, lse, cand_logp, cand_ids, ws=None, stream=None) -> None:

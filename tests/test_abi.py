@@ -22,7 +22,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     syms = declared_symbols()
-    assert len(syms) == 26, syms
+    assert len(syms) == 27, syms
     lib = D.lib()
     for s in syms:
         assert hasattr(lib, s), s
@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert D.abi_version() == D.ABI_VERSION == 6
+    assert D.abi_version() == D.ABI_VERSION == 7
     for s in range(5):
         assert D.status_string(s)
     assert D.status_string(99) == "unknown status"
@@ -119,9 +119,19 @@ def test_entry_points_reject_before_any_launch():
     assert lib.dartree_export_states(byref(p), FAKE, need, 0, FAKE, None) == D.ERR_INVALID_ARG
     assert lib.dartree_export_states(byref(p), FAKE, need - 1, 3, FAKE, None) == D.ERR_WORKSPACE
     # single-step calls
-    assert lib.dartree_project(1, 8, 100, 65, 8, FAKE, FAKE, FAKE, 100, FAKE, None) == D.ERR_UNSUPPORTED
-    assert lib.dartree_project(1, 0, 100, 64, 8, FAKE, FAKE, FAKE, 100, FAKE, None) == D.ERR_INVALID_ARG
-    assert lib.dartree_project(1, 8, 100, 64, 8, FAKE + 2, FAKE, FAKE, 100, FAKE, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_project(1, 8, 100, 65, 8, FAKE, FAKE, FAKE, 100, FAKE, None, 0, None) == D.ERR_UNSUPPORTED
+    assert lib.dartree_project(1, 0, 100, 64, 8, FAKE, FAKE, FAKE, 100, FAKE, None, 0, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_project(1, 8, 100, 64, 8, FAKE + 2, FAKE, FAKE, 100, FAKE, None, 0, None) == D.ERR_INVALID_ARG
+    # split scratch: none for few rows or fp32, 64 MB for the 256x256-tile kernel's shapes
+    assert D.project_workspace_size(D.BF16, 64, 151936, 2560) == 0
+    assert D.project_workspace_size(D.FP32, 1024, 151936, 2560) == 0
+    split = D.project_workspace_size(D.BF16, 1024, 151936, 5120)
+    assert split == 256 * 256 * 256 * 4
+    assert lib.dartree_project(1, 1024, 151936, 5120, 64, FAKE, FAKE, FAKE, 0, FAKE, None, 0, None) == D.ERR_WORKSPACE
+    assert lib.dartree_project(1, 1024, 151936, 5120, 64, FAKE, FAKE, FAKE, 0, FAKE, FAKE, split - 1,
+                               None) == D.ERR_WORKSPACE
+    assert lib.dartree_project(1, 1024, 151936, 5120, 64, FAKE, FAKE, FAKE, 0, FAKE, FAKE + 16, split,
+                               None) == D.ERR_WORKSPACE
     assert lib.dartree_lse_topk(FAKE, 4, 100, 101, 1.0, FAKE, FAKE, FAKE, None, 0, None) == D.ERR_INVALID_ARG
     assert lib.dartree_lse_topk(FAKE, 4, 100, 4, -1.0, FAKE, FAKE, FAKE, None, 0, None) == D.ERR_INVALID_ARG
     big = D.lse_topk_workspace_size(1, 151936, 8)

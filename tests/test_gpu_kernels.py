@@ -75,6 +75,11 @@ def test_lse_topk(rows, vocab, k, T, dist):
     (200, 3000, 256, 50),
     # >= 512 rows against >= 16384 columns: the 256x256-tile kernel, ragged in both
     (512, 16400, 256, 64), (600, 16390, 128, 75), (1024, 20000, 512, 64),
+    # one and three 64-deep K steps: every depth of the load pipeline's prologue
+    (512, 16384, 64, 64), (520, 16500, 192, 13),
+    # a last partial wave of tiles split along K (on 256 CUs: 60 tiles in 4
+    # pieces; 69 tiles in 3 pieces, ragged in M and N)
+    (1024, 20000, 1024, 64), (1030, 16400, 768, 103),
 ])
 def test_project_bf16_within_error_bound(rows, vocab, hidden, group):
     rng = np.random.default_rng(rows + vocab + hidden)
@@ -84,8 +89,17 @@ def test_project_bf16_within_error_bound(rows, vocab, hidden, group):
     bias = rng.normal(0, 2, size=(groups, vocab + 3)).astype(np.float32)  # stride vocab + 3
     dev = device()
     z = torch.empty(rows, vocab, dtype=torch.float32, device=dev)
-    say(f"project bf16 rows={rows} vocab={vocab} hidden={hidden} group={group}")
-    D.project(D.BF16, to_dev(x), to_dev(U), to_dev(bias), vocab + 3, z, group)
+    nws = D.project_workspace_size(D.BF16, rows, vocab, hidden)
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev) if nws else None
+    say(f"project bf16 rows={rows} vocab={vocab} hidden={hidden} group={group} ws={nws}")
+    xd, Ud, bd = to_dev(x), to_dev(U), to_dev(bias)
+    D.project(D.BF16, xd, Ud, bd, vocab + 3, z, group, ws)
+    if ws is not None:  # deterministic: a second call (stale scratch) gives the same bits
+        z2 = torch.empty_like(z)
+        ws.fill_(0x7F)
+        D.project(D.BF16, xd, Ud, bd, vocab + 3, z2, group, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(z, z2)
     torch.cuda.synchronize()
     z = z.cpu().numpy().astype(np.float64)
     xf = W.bf16_bits_to_fp32(x).astype(np.float64)

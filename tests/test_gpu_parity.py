@@ -41,6 +41,11 @@ SMALL = {
     "bf16-B1": small(budget=1, seed=39),
     "bf16-k12": small(branch=12, width=20, budget=50, seed=47),       # top-k bucket 16, row segments merged
     "bf16-k20": small(branch=20, width=24, budget=70, seed=48),       # top-k bucket 32
+    # >= 512 parent rows: the head's 256x256 tiles split along K (512 rows: 4 tiles in 2 pieces each)
+    "bf16-head-split": small(batch=8, width=64, branch=8, depth=4, budget=120, vocab=4099, hidden=512, seed=42),
+    # 1024 rows x 16400 vocabulary: 260 logit tiles, the 4 past one wave of 256 CUs split in 2 pieces
+    "bf16-logits-split": small(batch=16, width=64, branch=8, depth=4, budget=100, vocab=16400, hidden=512,
+                               seed=43),
     "fp32-small": small(precision=W.FP32, hidden=48, sigma_w=0.1, seed=40),
     "fp32-tiny-vocab": small(precision=W.FP32, vocab=7, hidden=5, branch=3, width=5, budget=12, seed=41),
     # shared candidate sets C_d = TopK(L_d^base, K)
