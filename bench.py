@@ -168,7 +168,8 @@ def time_consumer(torch, cfg, out, stream, reps: int = 50) -> dict:
     q, kc, vc, kt, vt = t(ai.q), t(ai.k_ctx), t(ai.v_ctx), t(ai.k_tree), t(ai.v_tree)
     p = D.AttnParams(cfg.batch, cfg.budget, s["max_ctx"], s["heads_q"], s["heads_kv"], s["head_dim"],
                      1.0 / np.sqrt(s["head_dim"]))
-    ws = torch.empty(D.tree_attention_workspace_size(p), dtype=torch.uint8, device=dev)
+    nws = D.tree_attention_workspace_size(p)
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev) if nws else None
     o = torch.empty(cfg.batch, cfg.budget, s["heads_q"], s["head_dim"], dtype=torch.float32, device=dev)
     target = torch.randint(0, cfg.vocab, (cfg.batch, cfg.budget + 1), dtype=torch.int32, device=dev,
                            generator=torch.Generator(device=dev).manual_seed(7))

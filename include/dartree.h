@@ -354,6 +354,11 @@ typedef struct dartree_attn_params {
   float scale;       /* softmax scale (> 0), e.g. 1 / sqrt(head_dim) */
 } dartree_attn_params;
 
+/* Bytes of device workspace for dartree_tree_attention (host only).  With
+ * fewer than 512 (request, key/value head, 64-query-row tile) blocks the
+ * context is split into segments of 256 positions whose partial results are
+ * merged (the workspace holds them); with 512 or more every block covers all
+ * keys and the size is 0. */
 dartree_status dartree_tree_attention_workspace_size(const dartree_attn_params* p, size_t* bytes);
 
 /* One attention layer over the flattened trees (Sec. 2.3): the query of
@@ -367,7 +372,8 @@ dartree_status dartree_tree_attention_workspace_size(const dartree_attn_params* 
  * mask: u64 [b][B][ceil(B/64)]; out: fp32 [b][B][heads_q][128].  bf16
  * products with fp32 accumulation; the softmax weights are rounded to bf16
  * for the weighted sum of values.  ws: device, 256-byte aligned, >=
- * dartree_tree_attention_workspace_size (per-segment partial results). */
+ * dartree_tree_attention_workspace_size (per-segment partial results; may be
+ * NULL when that size is 0). */
 dartree_status dartree_tree_attention(const dartree_attn_params* p, const void* q, const void* k_ctx,
                                       const void* v_ctx, const void* k_tree, const void* v_tree,
                                       const uint64_t* mask, const int32_t* ctx_len, float* out, void* ws,

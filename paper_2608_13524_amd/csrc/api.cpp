@@ -766,7 +766,8 @@ AttnLayout attn_layout_of(const dartree_attn_params& p) {
   l.nseg_ctx = (p.max_ctx + seg - 1) / seg;
   const int rows = p.budget * (p.heads_q / p.heads_kv);
   l.rows_pad = (rows + 63) / 64 * 64;
-  const size_t slots = size_t(l.nseg_ctx + 1) * p.batch * p.heads_kv * l.rows_pad;
+  const bool fused = attention_fused(p.batch, p.budget, p.heads_q, p.heads_kv);
+  const size_t slots = fused ? 0 : size_t(l.nseg_ctx + 1) * p.batch * p.heads_kv * l.rows_pad;
   size_t o = 0;
   auto take = [&](size_t bytes) { const size_t at = o; o = align_up(o + bytes); return at; };
   l.part_o = take(slots * 128 * 4);
@@ -796,7 +797,8 @@ dartree_status dartree_tree_attention(const dartree_attn_params* p, const void* 
       (v_ctx && !aligned16(v_ctx)) || !aligned16(out))
     return DARTREE_ERR_INVALID_ARG;
   const AttnLayout l = attn_layout_of(*p);
-  if (!ws || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0 || ws_bytes < l.total) return DARTREE_ERR_WORKSPACE;
+  if (l.total > 0 && (!ws || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0 || ws_bytes < l.total))
+    return DARTREE_ERR_WORKSPACE;
   AttnArgs a{};
   a.batch = p->batch;
   a.budget = p->budget;
@@ -815,8 +817,8 @@ dartree_status dartree_tree_attention(const dartree_attn_params* p, const void* 
   a.v_tree = static_cast<const uint16_t*>(v_tree);
   a.mask = mask;
   a.ctx_len = ctx_len;
-  a.part_o = at<float>(ws, l.part_o);
-  a.part_ml = at<float>(ws, l.part_ml);
+  a.part_o = l.total > 0 ? at<float>(ws, l.part_o) : nullptr;
+  a.part_ml = l.total > 0 ? at<float>(ws, l.part_ml) : nullptr;
   a.out = out;
   return hip_status(launch_tree_attention(a, stream));
 }

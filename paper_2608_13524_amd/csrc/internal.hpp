@@ -192,6 +192,9 @@ struct AttnArgs {
 };
 int attention_segment_len();
 int attention_max_segments();   // limit of context segments + 1
+// true when one block per (request, key/value head, 64-row tile) covers all
+// keys (enough blocks for the chip): no partial results, no merge
+bool attention_fused(int batch, int budget, int heads_q, int heads_kv);
 hipError_t launch_tree_attention(const AttnArgs& a, hipStream_t s);
 hipError_t launch_heap_emit(const HeapArgs& a, const dartree_tree& out, hipStream_t s);
 

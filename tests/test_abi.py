@@ -242,6 +242,9 @@ def test_consumer_rejects_bad_arguments():
     assert n >= 9 * 8 * 256 * 128 * 4          # one partial row per segment, kv head and query row
     edge = D.AttnParams(1, 64, 1023 * 256, 4, 1, 128, 0.0884)
     assert D.tree_attention_workspace_size(edge) > 0   # 1023 context segments + the tree: the limit
+    # >= 512 (request, kv head, 64-row tile) blocks: every block covers all keys, no workspace
+    assert D.tree_attention_workspace_size(D.AttnParams(16, 64, 2048, 32, 8, 128, 0.0884)) == 0   # 16*8*4
+    assert D.tree_attention_workspace_size(D.AttnParams(15, 64, 2048, 32, 8, 128, 0.0884)) > 0    # 480
     for field, value, code in (("head_dim", 64, D.ERR_UNSUPPORTED), ("heads_q", 30, D.ERR_INVALID_ARG),
                                ("scale", 0.0, D.ERR_INVALID_ARG), ("budget", 0, D.ERR_INVALID_ARG),
                                ("max_ctx", -1, D.ERR_INVALID_ARG), ("budget", 4097, D.ERR_UNSUPPORTED),

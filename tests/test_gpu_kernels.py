@@ -272,20 +272,38 @@ def test_calibration_kernels():
     sink.zero_()
     D.calib_mfma(3, 5, sink)
     torch.cuda.synchronize()
-    # accumulator (i, j) adds the tile a_i b_j^T every round: 4 waves, 5 rounds
-    lane = torch.arange(64)
+    # accumulator (i, j) adds the tile a_i b_j^T every round: 4 waves, 5 rounds.
+    # The operands are pseudo-random bf16 values: element e of lane l of slot
+    # s (a_i: slot i, b_j: slot 8 + j) comes from an integer hash of
+    # (s * 64 + l) * 8 + e, regenerated here from the same published steps.
+    M32 = 0xFFFFFFFF
 
-    def operand(shift, mul, unit):                 # lane l holds row l % 16, k-group l // 16
-        vals = torch.stack([((lane * mul + e + shift) & 7).float() * unit for e in range(8)], 1)
-        M = torch.zeros(16, 32)
+    def mix(h):
+        h ^= h >> 15
+        h = (h * 0x2C1B3C6D) & M32
+        h ^= h >> 12
+        h = (h * 0x297A2D39) & M32
+        h ^= h >> 15
+        return h
+
+    def operand(slot):                             # lane l holds row l % 16, k-group l // 16
+        M = np.zeros((16, 32))
         for l in range(64):
-            M[l % 16, 8 * (l // 16):8 * (l // 16) + 8] = vals[l]
+            for e in range(8):
+                h = mix((((slot * 64 + l) * 8 + e) * 0x9E3779B1 + 0x3C6EF372) & M32)
+                bits = ((h >> 31) << 15) | ((119 + (h >> 8) % 8) << 7) | (h & 0x7F)
+                M[l % 16, 8 * (l // 16) + e] = W.bf16_bits_to_fp32(np.array([bits], np.uint16))[0]
         return M
 
-    tile = sum(float((operand(i, 1, 0.125) @ operand(j, 3, 0.0625).T).sum()) for i in range(8) for j in range(8))
-    want = 4 * 5 * tile
-    got = sink[:3].cpu()
-    assert torch.allclose(got, torch.full((3,), want), rtol=1e-6), (got, want)
+    A = [operand(i) for i in range(8)]
+    B = [operand(8 + j) for j in range(8)]
+    want = 4 * 5 * sum(float((A[i] @ B[j].T).sum()) for i in range(8) for j in range(8))
+    # fp32 accumulation: every product passes through at most ~30 roundings at
+    # 2^-24 (5 rounds of 32-term sums, the lane, wave and block reductions)
+    scale = 4 * 5 * sum(float((np.abs(A[i]) @ np.abs(B[j]).T).sum()) for i in range(8) for j in range(8))
+    got = sink[:3].cpu().double().numpy()
+    assert np.all(np.abs(got - want) <= 2e-6 * scale), (got, want, scale)
+    assert got[0] == got[1] == got[2]
 
 
 @pytest.mark.parametrize("rows,vocab,K,dist", [

@@ -76,7 +76,8 @@ def run_attention(ai: W.AttentionInputs, mask, budget, heads_q, heads_kv, scale,
     dev = device()
     b, max_ctx = ai.k_ctx.shape[0], ai.k_ctx.shape[1]
     p = D.AttnParams(b, budget, max_ctx, heads_q, heads_kv, 128, scale)
-    ws = torch.empty(max(D.tree_attention_workspace_size(p), 1), dtype=torch.uint8, device=dev)
+    nws = D.tree_attention_workspace_size(p)
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev) if nws else None
     out = torch.full((b, budget, heads_q, 128), float("nan"), dtype=torch.float32, device=dev)
     kc = to_dev(ai.k_ctx) if max_ctx else None
     vc = to_dev(ai.v_ctx) if max_ctx else None
@@ -117,6 +118,9 @@ ATTN = {
     "single-node": (2, 1, 70, [70, 1], 8, 8),
     "empty-context-row": (2, 12, 256, [0, 256], 16, 4),
     "tree-only-pads": (1, 140, 0, [0], 4, 2),      # rows 125.. are pad slots that see nothing: zero
+    # >= 512 (request, kv head, row tile) blocks: one block covers all keys, no merge
+    "fused-ragged": (8, 130, 300, [300, 0, 17, 256, 299, 1, 64, 200], 32, 8),   # 8 x 8 x 9 tiles
+    "fused-tree-only": (16, 200, 0, [0] * 16, 16, 2),                          # 16 x 2 x 25 tiles
 }
 
 
