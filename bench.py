@@ -202,12 +202,20 @@ def time_consumer(torch, cfg, out, stream, reps: int = 50) -> dict:
     b, B, n, Hq, Hkv, Dh = cfg.batch, cfg.budget, s["max_ctx"], s["heads_q"], s["heads_kv"], s["head_dim"]
     nbytes = 2 * 2 * b * (n + B) * Hkv * Dh + 2 * b * B * Hq * Dh + 4 * b * B * Hq * Dh
     flops = 4.0 * b * B * Hq * (n + B) * Dh
+    # the bound by arithmetic intensity against the spec balance (2.5 PFLOP/s / 8 TB/s = 312 flop/B)
+    if flops / nbytes > MFMA_BF16_PEAK_TFS * 1e12 / (HBM_PEAK_GBS * 1e9):
+        roof = {"bound": "mfma", "achieved": flops / attn_us / 1e6, "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": flops / attn_us / 1e6 / MFMA_BF16_PEAK_TFS}
+    else:
+        roof = {"bound": "hbm", "achieved": nbytes / attn_us / 1e3, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": nbytes / attn_us / 1e3 / HBM_PEAK_GBS}
+    roof.update({"algorithmic_bytes": nbytes, "flops": flops})
+    if nbytes < 64e6:
+        roof["note"] = (f"latency-bound: {nbytes / 1e6:.0f} MB and {flops / 1e9:.1f} GFLOP per layer "
+                        f"({b} request(s) x {B} nodes)")
     return {"tree_attention_us": attn_us, "accept_walk_us": walk_us,
             "shape": {"heads_q": Hq, "heads_kv": Hkv, "head_dim": Dh, "context": n, "nodes": B},
-            "attention_roofline": {"bound": "hbm", "achieved": nbytes / attn_us / 1e3, "peak": HBM_PEAK_GBS,
-                                   "unit": "GB/s", "frac": nbytes / attn_us / 1e3 / HBM_PEAK_GBS,
-                                   "algorithmic_bytes": nbytes, "flops": flops,
-                                   "note": "latency-bound at one request: 10 MB and 2.2 GFLOP per layer"}}
+            "attention_roofline": roof}
 
 
 def cpu_baseline(cfg, inputs, budget_s: float = 20.0) -> dict:

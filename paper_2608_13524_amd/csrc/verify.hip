@@ -19,12 +19,14 @@
 //    row l % 16 and keys 4 (l / 16) + i of every 16-key tile, which is exactly
 //    the B operand layout of the P V product when the keys of each 32-key
 //    chunk are taken in the order {4g..4g+3, 16+4g..16+4g+3} for lane group
-//    g = l / 16; V is staged transposed in LDS and read in that same order, so
-//    P never leaves the registers.
+//    g = l / 16; V is transposed in registers (4 keys x 8 dims per thread)
+//    and stored to LDS with its keys already in that order, so one 16-byte
+//    read gives a lane its V operand and P never leaves the registers.
 #include "internal.hpp"
 
 namespace dartree {
 namespace {
+
 
 __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -74,26 +76,42 @@ __global__ __launch_bounds__(64) void accept_walk(int budget, int max_len, const
 // ---------------------------------------------------------------------------
 constexpr int kD = 128;
 constexpr int kKeys = 64;                  // keys per block step
-constexpr int kRows = 64;                  // query rows per block (4 waves x 16)
 constexpr int kKS = kD + 8;                // padded LDS row of K (bf16)
+constexpr int kRows = 64;                  // query rows per block (4 waves x 16)
 constexpr int kVS = kKeys + 8;             // padded LDS row of V^T (bf16)
 // With at least this many (request, key/value head, row tile) blocks (two
 // per CU on 256 CUs) every block covers all keys: no segment split, no merge.
 constexpr int kFusedMinBlocks = 512;
 
+// Position of key group kg4 (keys 4 kg4 .. 4 kg4 + 3 of a 64-key step) in a
+// V^T row: 32-key chunk c = kg4 / 8, lane group g = kg4 % 4, half
+// (kg4 / 4) % 2; the chunk holds, per lane group, its 4 keys of the first
+// 16-key tile and then its 4 of the second.
+__device__ __forceinline__ int vt_pos(int kg4) { return (kg4 >> 3) * 32 + (kg4 & 3) * 8 + ((kg4 >> 2) & 1) * 4; }
+
+// Blocks are dealt to the 8 XCDs round-robin: give XCD x the contiguous run
+// of work items [x n / 8, (x + 1) n / 8) so that the row tiles of one
+// (request, key/value head), which read the same keys and values, share its L2.
+__device__ __forceinline__ int attn_xcd_order(int b, int n) {
+  const int q8 = n / 8;
+  return b < 8 * q8 ? (b % 8) * q8 + b / 8 : b;
+}
+
 // grid: batch * Hkv * row tiles * segments (FUSED: batch * Hkv * row tiles).
-// Segment s < nseg_ctx covers context keys [s * seg_len, +seg_len) (clipped to
-// the request's length); segment nseg_ctx covers the tree's B keys under the
-// mask.  FUSED: one block covers the context keys [0, ctx_len) and then the
-// tree keys.
-template <bool FUSED>
-__global__ __launch_bounds__(256) void tree_attention_part(AttnArgs a) {
+// A block has 4 waves, each with RG groups of 16 query rows (a row tile is
+// 64 RG rows).  Segment s < nseg_ctx covers context keys [s * seg_len,
+// +seg_len) (clipped to the request's length); segment nseg_ctx covers the
+// tree's B keys under the mask.  FUSED: one block covers the context keys
+// [0, ctx_len) and then the tree keys.
+template <bool FUSED, int RG>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void tree_attention_part(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t Ks[kKeys][kKS];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[kD][kVS];
+  constexpr int kTileRows = kRows * RG;
   const int nseg = FUSED ? 1 : a.nseg_ctx + 1;
   const int rows = a.budget * a.group;
-  const int ntile = (rows + kRows - 1) / kRows;
-  int bid = blockIdx.x;
+  const int ntile = (rows + kTileRows - 1) / kTileRows;
+  int bid = FUSED ? attn_xcd_order(blockIdx.x, gridDim.x) : int(blockIdx.x);
   const int seg = bid % nseg;
   bid /= nseg;
   const int rt = bid % ntile;
@@ -105,46 +123,69 @@ __global__ __launch_bounds__(256) void tree_attention_part(AttnArgs a) {
   const int clen = a.ctx_len ? min(max(a.ctx_len[q], 0), a.max_ctx) : a.max_ctx;
   const int words = (a.budget + 63) / 64;
 
-  // this lane's query row (rows past the end are computed on the last row, never stored)
-  const int row = rt * kRows + wave * 16 + r16;
-  const int rowc = min(row, rows - 1);
-  const int node = rowc / a.group, head = kvh * a.group + rowc % a.group;
-  const uint16_t* qp = a.q + ((int64_t(q) * a.budget + node) * a.heads_q + head) * kD + g * 8;
-  bf16x8 qf[kD / 32];
+  // this lane's query rows (rows past the end are computed on the last row, never stored)
+  int row[RG], node[RG], head[RG];
+  bf16x8 qf[RG][kD / 32];
+  const uint64_t* mrow[RG];
 #pragma unroll
-  for (int ks = 0; ks < kD / 32; ++ks) qf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const f32x4*>(qp + ks * 32));
-  const uint64_t* mrow = a.mask + (int64_t(q) * a.budget + node) * words;
-
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4 o[kD / 16];
+  for (int rg = 0; rg < RG; ++rg) {
+    row[rg] = rt * kTileRows + (wave * RG + rg) * 16 + r16;
+    const int rowc = min(row[rg], rows - 1);
+    node[rg] = rowc / a.group;
+    head[rg] = kvh * a.group + rowc % a.group;
+    const uint16_t* qp = a.q + ((int64_t(q) * a.budget + node[rg]) * a.heads_q + head[rg]) * kD + g * 8;
 #pragma unroll
-  for (int dt = 0; dt < kD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int ks = 0; ks < kD / 32; ++ks)
+      qf[rg][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const f32x4*>(qp + ks * 32));
+    mrow[rg] = a.mask + (int64_t(q) * a.budget + node[rg]) * words;
+  }
 
+  float m_run[RG], l_run[RG];
+  f32x4 o[RG][kD / 16];
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg) {
+    m_run[rg] = -INFINITY;
+    l_run[rg] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < kD / 16; ++dt) o[rg][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+  typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+  // this thread's share of a 64-key step: 4 chunks of K (chunk c = tid + 256 i:
+  // key c / 16, dims 8 (c % 16)), and of V the 8 dims 8 (tid / 16) of the 4
+  // keys 4 (tid % 16) .. +3.  They are read with buffer loads whose range ends
+  // at the step's last valid key (k1), so keys past it read as zero with no
+  // per-lane test; the byte offsets within a step are fixed per thread.  The
+  // next step's share is loaded while the current one is multiplied.
+  const int vkg = threadIdx.x & 15, vdc = threadIdx.x >> 4;
+  constexpr int kChunks = kKeys * kD / 8 / 256;
+  const int key_bytes = a.heads_kv * kD * 2;
+  int koff[kChunks], voff[4];
+#pragma unroll
+  for (int i = 0; i < kChunks; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    koff[i] = (c / (kD / 8)) * key_bytes + kvh * kD * 2 + (c % (kD / 8)) * 16;
+    voff[i] = (4 * vkg + i) * key_bytes + kvh * kD * 2 + 16 * vdc;
+  }
   // keys [k0, k1) of one source (the context, or the tree under the mask)
   auto sweep = [&](const bool tree, const int k0, const int k1) {
     const uint16_t* kbase = tree ? a.k_tree + int64_t(q) * a.budget * a.heads_kv * kD
                                  : a.k_ctx + int64_t(q) * a.max_ctx * a.heads_kv * kD;
     const uint16_t* vbase = tree ? a.v_tree + int64_t(q) * a.budget * a.heads_kv * kD
                                  : a.v_ctx + int64_t(q) * a.max_ctx * a.heads_kv * kD;
-    // this thread's share of a 64-key step: 4 chunks of K (a wave covers 4
-    // whole rows) and 4 of V (a wave covers 64 keys of one 8-dim slice, so the
-    // transposed 2-byte stores spread over the banks); keys past k1 are zero,
-    // never read from memory.  The next step's share is loaded while the
-    // current one is multiplied.
-    typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
-    constexpr int kChunks = kKeys * kD / 8 / 256;
-    u16x8 kn[kChunks], vn[kChunks];
+    u16x8 kn[kChunks], vn[4];
     auto load_step = [&](int kb) {
+      const int bytes = min(k1 - kb, kKeys) * key_bytes;
+      const int64_t first = int64_t(kb) * a.heads_kv * kD;
+      const __amdgpu_buffer_rsrc_t rk =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(kbase + first), (short)0, bytes, 0x00020000);
+      const __amdgpu_buffer_rsrc_t rv =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(vbase + first), (short)0, bytes, 0x00020000);
 #pragma unroll
-      for (int i = 0; i < kChunks; ++i) {
-        const int c = threadIdx.x + 256 * i;
-        const int kk = c / (kD / 8), kd = (c % (kD / 8)) * 8;
-        const int vk = c % kKeys, vd = (c / kKeys) * 8;
-        kn[i] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-        vn[i] = kn[i];
-        if (kb + kk < k1) kn[i] = *reinterpret_cast<const u16x8*>(kbase + (int64_t(kb + kk) * a.heads_kv + kvh) * kD + kd);
-        if (kb + vk < k1) vn[i] = *reinterpret_cast<const u16x8*>(vbase + (int64_t(kb + vk) * a.heads_kv + kvh) * kD + vd);
-      }
+      for (int i = 0; i < kChunks; ++i) kn[i] = __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, koff[i], 0, 0));
+#pragma unroll
+      for (int i = 0; i < 4; ++i) vn[i] = __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(rv, voff[i], 0, 0));
     };
     if (k0 < k1) load_step(k0);
 
@@ -154,107 +195,135 @@ __global__ __launch_bounds__(256) void tree_attention_part(AttnArgs a) {
       for (int i = 0; i < kChunks; ++i) {
         const int c = threadIdx.x + 256 * i;
         *reinterpret_cast<u16x8*>(&Ks[c / (kD / 8)][(c % (kD / 8)) * 8]) = kn[i];
-        const int vk = c % kKeys, vd = (c / kKeys) * 8;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) Vt[vd + e][vk] = vn[i][e];
       }
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        *reinterpret_cast<u16x4*>(&Vt[8 * vdc + e][vt_pos(vkg)]) = u16x4{vn[0][e], vn[1][e], vn[2][e], vn[3][e]};
       __syncthreads();
       if (kb + kKeys < k1) load_step(kb + kKeys);
 
-      // S[key][query] for the 4 key tiles of 16
-      f32x4 s[4];
+      // S[key][query] for the 4 key tiles of 16, every row group
+      f32x4 s[RG][4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        s[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg) s[rg][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < kD / 32; ++ks) {
           const bf16x8 kf =
               __builtin_bit_cast(bf16x8, *reinterpret_cast<const f32x4*>(&Ks[t * 16 + r16][ks * 32 + g * 8]));
-          s[t] = mfma16(kf, qf[ks], s[t]);
+#pragma unroll
+          for (int rg = 0; rg < RG; ++rg) s[rg][t] = mfma16(kf, qf[rg][ks], s[rg][t]);
         }
       }
-      // visibility, scale (log2 domain) and the block's row maximum
-      const uint64_t mw = tree ? mrow[kb / 64] : 0ull;
-      float bmax = -INFINITY;
+      // visibility: a context step wholly inside [k0, k1) needs no test
+      if (tree || kb + kKeys > k1) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
+        for (int rg = 0; rg < RG; ++rg) {
+          const uint64_t mw = tree ? mrow[rg][kb / 64] : ~0ull;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int kl = t * 16 + g * 4 + i;   // key within the 64-key step
-          const bool ok = kb + kl < k1 && (!tree || ((mw >> kl) & 1ull));
-          s[t][i] = ok ? s[t][i] * a.scale_log2 : -INFINITY;
-          bmax = fmaxf(bmax, s[t][i]);
+          for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int kl = t * 16 + g * 4 + i;   // key within the 64-key step
+              if (!(kb + kl < k1 && ((mw >> kl) & 1ull))) s[rg][t][i] = -INFINITY;
+            }
         }
-      bmax = fmaxf(bmax, __shfl_xor(bmax, 16));
-      bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
-      // a row that has seen no visible key keeps m = -inf, l = 0, o = 0; the
+      }
+      // online softmax on the unscaled scores (scale > 0 keeps the order);
+      // p = exp2(scale log2(e) (s - m)).  The running maximum m moves only when
+      // a row's new maximum exceeds it by more than 8 / (scale log2(e)), so
+      // p <= 2^8 and the rescaling of l and O is skipped for most steps.  A
+      // row that has seen no visible key keeps m = -inf, l = 0, O = 0; the
       // arithmetic handles it (exp2(-inf) = 0), so control flow stays uniform
-      // around the matrix-core instructions
-      const float m_new = fmaxf(m_run, bmax);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-      float psum = 0.f;
+      // around the matrix-core instructions.
+      const float c2 = a.scale_log2;
+      bf16x8 pb[RG][2];
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
+      for (int rg = 0; rg < RG; ++rg) {
+        float bmax = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          s[t][i] = __builtin_amdgcn_exp2f(s[t][i] - m_use);
-          psum += s[t][i];
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) bmax = fmaxf(bmax, s[rg][t][i]);
+        bmax = fmaxf(bmax, __shfl_xor(bmax, 16));
+        bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
+        const bool grow = bmax * c2 > m_run[rg] * c2 + 8.f;
+        if (__any(grow)) {
+          const float m_new = grow ? bmax : m_run[rg];
+          const float alpha = __builtin_amdgcn_exp2f((m_run[rg] - (m_new == -INFINITY ? 0.f : m_new)) * c2);
+          l_run[rg] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < kD / 16; ++dt) o[rg][dt] *= alpha;
+          m_run[rg] = m_new;
         }
-      psum += __shfl_xor(psum, 16);
-      psum += __shfl_xor(psum, 32);
-      l_run = l_run * alpha + psum;
-      m_run = m_new;
+        const float nmc = -(m_run[rg] == -INFINITY ? 0.f : m_run[rg]) * c2;
+        float psum = 0.f;
 #pragma unroll
-      for (int dt = 0; dt < kD / 16; ++dt) o[dt] *= alpha;
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            s[rg][t][i] = __builtin_amdgcn_exp2f(fmaf(s[rg][t][i], c2, nmc));
+            psum += s[rg][t][i];
+          }
+        psum += __shfl_xor(psum, 16);
+        psum += __shfl_xor(psum, 32);
+        l_run[rg] += psum;
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            pb[rg][c][i] = __bf16(s[rg][2 * c][i]);
+            pb[rg][c][4 + i] = __bf16(s[rg][2 * c + 1][i]);
+          }
+      }
       // O[dim][query] += V^T[dim][key] P[query][key] over the two 32-key chunks
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        bf16x8 pb;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          pb[i] = __bf16(s[2 * c][i]);
-          pb[4 + i] = __bf16(s[2 * c + 1][i]);
-        }
+      for (int c = 0; c < 2; ++c)
 #pragma unroll
         for (int dt = 0; dt < kD / 16; ++dt) {
-          typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
-          const u16x4 lo = *reinterpret_cast<const u16x4*>(&Vt[dt * 16 + r16][c * 32 + g * 4]);
-          const u16x4 hi = *reinterpret_cast<const u16x4*>(&Vt[dt * 16 + r16][c * 32 + 16 + g * 4]);
-          const u16x8 vv = u16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          o[dt] = mfma16(__builtin_bit_cast(bf16x8, vv), pb, o[dt]);
+          const bf16x8 vv =
+              __builtin_bit_cast(bf16x8, *reinterpret_cast<const f32x4*>(&Vt[dt * 16 + r16][c * 32 + g * 8]));
+#pragma unroll
+          for (int rg = 0; rg < RG; ++rg) o[rg][dt] = mfma16(vv, pb[rg][c], o[rg][dt]);
         }
-      }
     }
   };
 
   if (FUSED) {
     sweep(false, 0, clen);
     sweep(true, 0, a.budget);
-    if (row >= rows) return;
-    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;   // a row that sees nothing is zero
-    float* op = a.out + ((int64_t(q) * a.budget + node) * a.heads_q + head) * kD;
 #pragma unroll
-    for (int dt = 0; dt < kD / 16; ++dt) *reinterpret_cast<f32x4*>(op + dt * 16 + g * 4) = o[dt] * inv;
+    for (int rg = 0; rg < RG; ++rg) {
+      if (row[rg] >= rows) continue;
+      const float inv = l_run[rg] > 0.f ? 1.f / l_run[rg] : 0.f;   // a row that sees nothing is zero
+      float* op = a.out + ((int64_t(q) * a.budget + node[rg]) * a.heads_q + head[rg]) * kD;
+#pragma unroll
+      for (int dt = 0; dt < kD / 16; ++dt) *reinterpret_cast<f32x4*>(op + dt * 16 + g * 4) = o[rg][dt] * inv;
+    }
     return;
   }
   const bool tree = seg == a.nseg_ctx;
   if (tree) sweep(true, 0, a.budget);
   else sweep(false, seg * a.seg_len, min(clen, seg * a.seg_len + a.seg_len));
-  if (row >= rows) return;
-  const int64_t pr = ((int64_t(seg) * a.batch + q) * a.heads_kv + kvh) * a.rows_pad + row;
-  if (g == 0) {
-    a.part_ml[pr * 2] = m_run;
-    a.part_ml[pr * 2 + 1] = l_run;
-  }
-  float* op = a.part_o + pr * kD;
 #pragma unroll
-  for (int dt = 0; dt < kD / 16; ++dt) *reinterpret_cast<f32x4*>(op + dt * 16 + g * 4) = o[dt];
+  for (int rg = 0; rg < RG; ++rg) {
+    if (row[rg] >= rows) continue;
+    const int64_t pr = ((int64_t(seg) * a.batch + q) * a.heads_kv + kvh) * a.rows_pad + row[rg];
+    if (g == 0) {
+      a.part_ml[pr * 2] = m_run[rg];
+      a.part_ml[pr * 2 + 1] = l_run[rg];
+    }
+    float* op = a.part_o + pr * kD;
+#pragma unroll
+    for (int dt = 0; dt < kD / 16; ++dt) *reinterpret_cast<f32x4*>(op + dt * 16 + g * 4) = o[rg][dt];
+  }
 }
 
 // grid: batch * budget * ceil(heads_q / 8), block 1024: merge the segments
 // of 8 query heads of one node, one (head, dim) output per thread.  The
-// per-head segment weights w_s = exp2(m_s - M) / L go to LDS first; then
+// per-head segment weights w_s = exp2(scale log2(e) (m_s - M)) / L (m_s the
+// segment's unscaled row maximum, M their maximum) go to LDS first; then
 // every output sums its segments' partial rows with independent loads.
 constexpr int kMergeHeads = 8;
 constexpr int kMergeThreads = kMergeHeads * kD;
@@ -275,8 +344,8 @@ __global__ __launch_bounds__(kMergeThreads) void tree_attention_merge(AttnArgs a
       for (int s = 0; s < nseg; ++s) M = fmaxf(M, a.part_ml[part(s, head) * 2]);
       float L = 0.f;
       for (int s = 0; s < nseg; ++s) {
-        const float m = a.part_ml[part(s, head) * 2];
-        const float ws = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - M);
+        const float m = a.part_ml[part(s, head) * 2];   // unscaled row maximum of segment s
+        const float ws = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m - M) * a.scale_log2);
         w[s * kMergeHeads + threadIdx.x] = ws;
         L += ws * a.part_ml[part(s, head) * 2 + 1];
       }
@@ -315,11 +384,13 @@ hipError_t launch_tree_attention(const AttnArgs& a, hipStream_t s) {
   const int rows = a.budget * a.group;
   const int ntile = (rows + kRows - 1) / kRows;
   if (attention_fused(a.batch, a.budget, a.heads_q, a.heads_kv)) {
-    hipLaunchKernelGGL(tree_attention_part<true>, dim3(unsigned(a.batch) * a.heads_kv * ntile), dim3(256), 0, s, a);
+    const int ntile2 = (rows + 2 * kRows - 1) / (2 * kRows);   // 128-row tiles
+    hipLaunchKernelGGL((tree_attention_part<true, 2>), dim3(unsigned(a.batch) * a.heads_kv * ntile2), dim3(256), 0, s,
+                       a);
     return hipGetLastError();
   }
   const unsigned parts = unsigned(a.batch) * a.heads_kv * ntile * (a.nseg_ctx + 1);
-  hipLaunchKernelGGL(tree_attention_part<false>, dim3(parts), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((tree_attention_part<false, 1>), dim3(parts), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const unsigned nhg = unsigned((a.heads_q + kMergeHeads - 1) / kMergeHeads);
