@@ -17,6 +17,8 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import re
+import subprocess
 import sys
 import time
 
@@ -218,6 +220,26 @@ def time_consumer(torch, cfg, out, stream, reps: int = 50) -> dict:
             "attention_roofline": roof}
 
 
+def gpu_env(torch) -> dict:
+    """Device, HIP runtime and the shader clock (rocm-smi, sampled right after
+    the timed replays; null when the tool is unavailable)."""
+    props = torch.cuda.get_device_properties(0)
+    env = {"device": torch.cuda.get_device_name(0), "arch": getattr(props, "gcnArchName", None),
+           "compute_units": props.multi_processor_count, "hip": torch.version.hip, "sclk_mhz": None}
+    try:
+        res = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True, timeout=15)
+        data = json.loads(res.stdout) if res.returncode == 0 else {}
+        for card in data.values():
+            for key, val in card.items():   # e.g. "sclk clock speed:": "(2400Mhz)"
+                m = re.search(r"(\d+)\s*mhz", str(val), re.I)
+                if key.lower().startswith("sclk") and m:
+                    env["sclk_mhz"] = int(m.group(1))
+            break
+    except (OSError, ValueError, subprocess.SubprocessError):
+        pass
+    return env
+
+
 def cpu_baseline(cfg, inputs, budget_s: float = 20.0) -> dict:
     """The oracle (fp64 NumPy) on the host cores, on the first D depths of
     request 0 with D chosen to take ~budget_s; scaled to us per full round."""
@@ -249,7 +271,9 @@ def cpu_baseline(cfg, inputs, budget_s: float = 20.0) -> dict:
         t = (t * reps + run(depth)) / (reps + 1)
         reps += 1
     scale = sum(rows) / sum(rows[:depth]) * cfg.batch
+    blas = ",".join(sorted({i.get("internal_api", "?") for i in info if i.get("user_api") == "blas"})) or None
     return {"value": t * scale * 1e6, "unit": "us/round", "cores": int(threads), "kind": "oracle",
+            "blas": blas, "host_cpus_available": len(os.sched_getaffinity(0)),
             "sample": f"request 0, depths 1..{depth} of {cfg.depth} (mean of {reps} run(s), {t:.2f} s each), "
                       f"scaled by parent rows to the full round of {cfg.batch} request(s)"}
 
@@ -328,6 +352,7 @@ def main() -> int:
     K = args.steps
     per_step_ms, total_ms, wall = timed(graph.replay, K)
     us_round = total_ms * 1e3 / K
+    env = gpu_env(torch)
     log(f"timed {K} graph replays: {us_round:.1f} us/round (wall {wall * 1e3 / K:.1f} ms/round)")
     eager_ms, eager_total, _ = timed(lambda: D.build_tree(p, di, ws, out), K)
     eager_us = eager_total * 1e3 / K
@@ -457,7 +482,7 @@ def main() -> int:
         "projection_mfma_frac": proj_flops / MFMA_BF16_PEAK_TFS,
         "kernels": kernels, "instrumented_us_per_round": instrumented_us,
         "roofline": roof, "lse_topk_roofline": lse_roof, "calibration": cal, "sequential_heap": heap,
-        "consumer": consumer,
+        "consumer": consumer, "env": env,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
