@@ -239,6 +239,9 @@ __global__ __launch_bounds__(1024) void prune_emit(LevelShape shape, int budget,
   __shared__ uint64_t keys[kSortMax];
   __shared__ int32_t out_idx[kSortMax];   // per supertree node: output index, -1 if pruned
   __shared__ int32_t par_out[kSortMax];   // per output index: parent's output index
+  // per supertree node, staged once: token, parent slot, score
+  __shared__ int32_t s_tok[kSortMax], s_par[kSortMax];
+  __shared__ float s_score[kSortMax];
   __shared__ uint32_t rank_key[DARTREE_MAX_WIDTH];
   __shared__ int32_t kept_at_depth;
 
@@ -249,22 +252,27 @@ __global__ __launch_bounds__(1024) void prune_emit(LevelShape shape, int budget,
   const int words = (budget + 63) / 64;
   const int npad = next_pow2(total);
   auto lvl_index = [&](int d, int slot) { return (int64_t(d - 1) * batch + q) * W + slot; };
-  // supertree node index of the parent of level entry li at depth d >= 2
-  // (slots outside S_{d-1} are clamped: malformed levels cannot index out of bounds)
-  auto parent_node = [&](int d, int64_t li) {
-    const int ps = min(max(lvl_par[li], 0), shape.n[d - 2] - 1);
+  // supertree node index of the parent of node g at depth d >= 2 (slots
+  // outside S_{d-1} are clamped: malformed levels cannot index out of bounds)
+  auto parent_node = [&](int d, int g) {
+    const int ps = min(max(s_par[g], 0), shape.n[d - 2] - 1);
     return shape.off[d - 2] + ps;
   };
 
-  // 1. top-B of the supertree
+  // 0. stage the levels in LDS (one pass of independent loads) and build the
+  // 1. top-B keys of the supertree
   for (int g = threadIdx.x; g < npad; g += blockDim.x) {
     uint64_t key = ~0ull;
     if (g < total) {
       int d = 1;
       while (g >= shape.off[d]) ++d;
       const int slot = g - shape.off[d - 1];
-      key = (uint64_t(score_desc_key(lvl_score[lvl_index(d, slot)])) << 32) |
-            (uint32_t(d) << 16) | uint32_t(slot);
+      const int64_t li = lvl_index(d, slot);
+      const float sc = lvl_score[li];
+      s_tok[g] = lvl_tok[li];
+      s_par[g] = lvl_par[li];
+      s_score[g] = sc;
+      key = (uint64_t(score_desc_key(sc)) << 32) | (uint32_t(d) << 16) | uint32_t(slot);
     }
     keys[g] = key;
     if (g < total) out_idx[g] = -1;
@@ -288,9 +296,8 @@ __global__ __launch_bounds__(1024) void prune_emit(LevelShape shape, int budget,
     for (int i = threadIdx.x; i < nd; i += blockDim.x) {
       uint32_t rk = ~0u;
       if (out_idx[od + i] >= 0) {
-        const int64_t li = lvl_index(d, i);
-        const uint32_t pidx = d == 1 ? 0u : uint32_t(out_idx[parent_node(d, li)]);
-        rk = (pidx << 20) | (uint32_t(lvl_tok[li]) & 0xFFFFFu);
+        const uint32_t pidx = d == 1 ? 0u : uint32_t(out_idx[parent_node(d, od + i)]);
+        rk = (pidx << 20) | (uint32_t(s_tok[od + i]) & 0xFFFFFu);
       }
       rank_key[i] = rk;
     }
@@ -301,8 +308,7 @@ __global__ __launch_bounds__(1024) void prune_emit(LevelShape shape, int budget,
       int r = 0;
       for (int j = 0; j < nd; ++j) r += (rank_key[j] < mine) | ((rank_key[j] == mine) & (j < i));
       out_idx[od + i] = base + r;
-      const int64_t li = lvl_index(d, i);
-      par_out[base + r] = d == 1 ? -1 : out_idx[parent_node(d, li)];
+      par_out[base + r] = d == 1 ? -1 : out_idx[parent_node(d, od + i)];
       atomicAdd(&kept_at_depth, 1);
     }
     __syncthreads();
@@ -325,11 +331,10 @@ __global__ __launch_bounds__(1024) void prune_emit(LevelShape shape, int budget,
     for (int i = threadIdx.x; i < nd; i += blockDim.x) {
       const int o = out_idx[od + i];
       if (o < 0) continue;
-      const int64_t li = lvl_index(d, i);
-      out.tokens[ob + o] = lvl_tok[li];
+      out.tokens[ob + o] = s_tok[od + i];
       out.parents[ob + o] = par_out[o];
       out.depths[ob + o] = d;
-      out.scores[ob + o] = lvl_score[li];
+      out.scores[ob + o] = s_score[od + i];
     }
   }
   // 4. ancestor-or-self mask, one 64-bit word per thread
