@@ -135,8 +135,8 @@ def calibrate(torch, dev, U, stream, reps: int = 5) -> dict:
 
 
 def time_heap(torch, cfg, di, stream, steps: int, timed) -> dict:
-    """The node-at-a-time baseline (Sec. 3.1, "Seq. Correction w. Heap" of
-    Table 2) on the same inputs: one round is B pops, each after a head,
+    """The node-at-a-time baseline (Sec. 3.1, the sequential correction with a
+    heap of Table 2) on the same inputs: one round is B pops, each after a head,
     logits and softmax pass on the popped prefix, captured in a HIP graph."""
     p = D.Params.of(cfg)
     dev = di.U.device
@@ -290,8 +290,9 @@ def main() -> int:
                     help="heap: time only the sequential-heap baseline (for a kernel trace of it alone)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: requests are independent trees and this build has no "
-              "multi-GPU path (sharding is described in DESIGN.md).", file=sys.stderr)
+        print("bench.py runs on one GPU only (--gpus 1): the library builds trees on one device. Requests "
+              "are independent trees, so several GPUs would each take their own requests with no exchange.",
+              file=sys.stderr)
         return 2
 
     import torch

@@ -108,7 +108,7 @@ typedef struct dartree_params {
   int32_t head;        /* dartree_head: how a child's state is formed (t, a, z are the same) */
 } dartree_params;
 
-/* Device inputs of one round (Algorithm 1, "Require"). */
+/* Device inputs of one round (the inputs Algorithm 1 takes). */
 typedef struct dartree_inputs {
   const float* drafter_logits; /* L^base: fp32 [b][L][V] */
   const void* drafter_hidden;  /* H: act [b][L][h] */
@@ -223,7 +223,7 @@ dartree_status dartree_export_states(const dartree_params* p, const void* ws, si
 dartree_status dartree_project_workspace_size(int32_t precision, int32_t rows, int32_t vocab, int32_t hidden,
                                               size_t* bytes);
 
-/* Corrected logits (Algorithm 1, "correct all prefixes ... in parallel"):
+/* Corrected logits (Algorithm 1, every prefix of a depth corrected in one batch):
  * z[m][v] = bias[m / rows_per_group][v] + sum_i x[m][i] U[v][i]
  * for m < rows, v < vocab.  x: act [rows][hidden]; U: act [vocab][hidden];
  * bias: fp32 rows of length vocab, row g at bias + g * bias_stride (elements);
@@ -258,7 +258,7 @@ dartree_status dartree_candidate_sets_workspace_size(int32_t rows, int32_t vocab
 dartree_status dartree_candidate_sets(const float* logits, int32_t rows, int32_t vocab, int32_t K, int32_t* ids,
                                       void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Segmented top-W (Algorithm 1, "retain the global top-W child prefixes"):
+/* Segmented top-W (Algorithm 1, the W best children of each request kept):
  * for each request q < batch, candidates (j, i) for parent j < n_parent and
  * rank i < k score s = (parent_score[q][j] + cand_logp[q*n_parent + j][i]) + beta
  * (parent_score may be NULL: every parent scores 0, the root); the first n_keep

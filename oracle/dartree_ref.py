@@ -3,9 +3,8 @@
 TEST INFRASTRUCTURE ONLY (see the package docstring): nothing on the product
 path may import, call or link this module.
 
-What it computes (paper: Sec. 3.2 "Depth-Wise Parallel Supertree Construction",
-Algorithm 1 "DARTree Construction", Sec. 3.3 "Deferred Best-First Pruning",
-eq. (5) and Lemma 1), for each request independently:
+What it computes (paper: Sec. 3.2, Algorithm 1, Sec. 3.3, eq. (5) and
+Lemma 1), for each request independently:
 
   root level S_0 = {empty prefix}, state r_0, score 0              (Alg. 1, init)
   for d = 1 .. L:                                                 (Alg. 1, depth loop)
@@ -27,13 +26,14 @@ id asc) for each request and depth, the head scores only C_d
 C_d, i.e. the tokens outside C_d take z = -inf; the rest is unchanged (the
 per-parent cap k <= K, k = K keeping every token of C_d as in Alg. 1).
   emit T in canonical breadth-first order with parent indices and the
-  ancestor-or-self tree-attention mask (Sec. 2.3 "Tree Verification").
+  ancestor-or-self tree-attention mask (Sec. 2.3).
 
-Readings where the paper is silent (each is listed in the design doc):
-  * the head form g and the state update (Alg. 1 gives only g(H_d, r(u_<d)) and
-    "r(u_1:d) from r(u_<d) and u_d"): the Elman residual head above;
+Readings where the paper is silent:
+  * the head form g and the state update (Alg. 1 gives only the signature
+    g(H_d, r(u_<d)) and says that a child's state follows from its parent's
+    state and its token): the Elman residual head above;
   * the candidate set is the per-parent top-k of the full-vocabulary corrected
-    logits (the "Full" vocabulary variant of Appendix D) with branching cap k,
+    logits (the full-vocabulary variant of Appendix D) with branching cap k,
     or, with ``candidates`` = K, the shared C_d above with q~ normalised over
     C_d (Alg. 1 writes q~_d(C_d | u_<d) = g_{C_d}(...) without stating the
     normaliser; normalising over C_d keeps log q~ <= 0, which Lemma 1 needs);
@@ -41,14 +41,15 @@ Readings where the paper is silent (each is listed in the design doc):
   * rounding points: with bf16 inputs, a and r are rounded to bf16 (through
     fp32, nearest-even) because they are operands of bf16 matrix products;
     everything else is fp64 here.  With fp32 inputs nothing is rounded;
-  * n_d = min(W, n_{d-1} * k); "global" top-W is per request;
+  * n_d = min(W, n_{d-1} * k); the top-W that Alg. 1 calls global is taken
+    per request;
   * tie-breaks: top-k (z desc, id asc); top-W (s desc, parent slot asc, id asc);
-    top-B (s desc, depth asc, slot asc) - "depth asc" is Lemma 1's "ancestors
-    are preferred under ties";
+    top-B (s desc, depth asc, slot asc) - depth ascending is Lemma 1's tie
+    rule, under which a prefix wins a tie with its extensions;
   * the root is not a node of T and does not count toward B.
 
-The node-at-a-time baseline DARTree replaces (Sec. 3.1, "Seq. Correction w.
-Heap" of Table 2) is ``sequential_heap``: a max-heap over candidate prefixes;
+The node-at-a-time baseline DARTree replaces (Sec. 3.1, the sequential
+correction with a heap of Table 2) is ``sequential_heap``: a max-heap over candidate prefixes;
 the head is run on the root and its k best children are pushed; each pop adds
 the best prefix to the tree, runs the head on it under its own token history
 (state from its parent's t and its token) and pushes its k best children,

@@ -9,7 +9,7 @@
 //     across lanes, the winning lane shifting its list;
 //   * rows are split into segments when there are too few rows to fill the
 //     chip; a second kernel merges the per-segment partials in segment order.
-// Ties: ids ascend along every thread's traversal, so "strictly greater"
+// Ties: ids ascend along every thread's traversal, so a strictly-greater test
 // keeps the lower id first; every merge compares (value desc, id asc).
 #include <float.h>
 

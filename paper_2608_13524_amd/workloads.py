@@ -6,8 +6,8 @@ weights). It holds none of the method's arithmetic; both the HIP path and the
 CPU oracle consume what it produces.
 
 Inputs stand in for the drafter outputs of the paper's workload (a DFlash-style
-block drafter with a gamma=16 block over the Qwen3 vocabulary, Sec. 4.1 "Baselines
-and Implementation"); trained drafters and benchmark prompts are not available,
+block drafter with a gamma=16 block over the Qwen3 vocabulary, Sec. 4.1); trained
+drafters and benchmark prompts are not available,
 so every tensor is drawn from a fixed distribution:
 
 * weights ``A`` [h][h] and ``U`` [V][h] ~ N(0, sigma_w^2)

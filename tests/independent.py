@@ -6,7 +6,7 @@ the tree is built by algorithms the paper states separately from Alg. 1:
 
 * ``heap_best_first``      - best-first max-heap over a materialised prefix tree
                               (Lemma 1 and its proof, Appendix C);
-* ``sequential_heap``      - "Sequential Correction w. Heap": pop the best prefix,
+* ``sequential_heap``      - the sequential correction with a heap: pop the best prefix,
                               run the head on it, push its children (Sec. 3.1);
 * ``brute_force``          - global top-B over every prefix of length <= L;
 * ``marginal_top_b``       - DDTree's optimum for a zeroed correction: top-B
