@@ -597,11 +597,17 @@ hipError_t launch_stream(const KArgs& k, int epi, hipStream_t s) {
 
 template <int MT>
 hipError_t launch_stream_nt(const KArgs& k, int epi, hipStream_t s) {
-  // Long weight matrices (the vocabulary): 32-row blocks, 8 waves over K.
+  // Long weight matrices (the vocabulary): 32-row blocks, 8 waves over K at
+  // 16 node rows; from 17 node rows on, 128-row blocks and 4 waves over K, so
+  // that every node-row operand a wave loads serves 8 weight tiles (measured
+  // at 32 and 64 rows: 1.36x and 1.47x the 32-row blocks' stream rate).
   // Short ones (A, h rows): 16-row blocks, 16 waves over K (8 when the node
   // rows need more registers), so that even h = 2560 rows give enough waves
   // to keep HBM busy.
-  if (k.N >= 32 * 2048) return launch_stream<MT, 2, 8, 2>(k, epi, s);
+  if (k.N >= 32 * 2048) {
+    if constexpr (MT >= 2) return launch_stream<MT, 8, 4, 1>(k, epi, s);
+    return launch_stream<MT, 2, 8, 2>(k, epi, s);
+  }
   if constexpr (MT <= 2) return launch_stream<MT, 1, 16, 2>(k, epi, s);
   return launch_stream<MT, 1, 8, 2>(k, epi, s);
 }

@@ -73,6 +73,9 @@ def test_lse_topk(rows, vocab, k, T, dist):
     (1, 4099, 2560, 1), (8, 4099, 2560, 8), (13, 5000, 512, 5), (16, 151936, 2560, 8),
     (33, 3001, 1024, 11), (64, 4099, 4096, 16), (100, 4099, 512, 25), (128, 4103, 1024, 64),
     (200, 3000, 256, 50),
+    # 17..64 rows against a long vocabulary: 128-row blocks, 4 waves over K
+    # (ragged: the last block runs past the vocabulary)
+    (20, 65600, 320, 4), (33, 70000, 256, 11), (64, 66000, 512, 16),
     # >= 512 rows against >= 16384 columns: the 256x256-tile kernel, ragged in both
     (512, 16400, 256, 64), (600, 16390, 128, 75), (1024, 20000, 512, 64),
     # one and three 64-deep K steps: every depth of the load pipeline's prologue
