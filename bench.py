@@ -18,7 +18,6 @@ import argparse
 import json
 import os
 import re
-import subprocess
 import sys
 import time
 
@@ -42,9 +41,10 @@ def log(msg: str) -> None:
 
 
 def measured_traffic(workload: str, kernel: str):
-    """HBM bytes per launch from the committed counter summary of this
-    workload and kernel, or None if there is none or the kernel's source has
-    changed since the counters were taken."""
+    """The committed counter summary of this workload and kernel (HBM bytes
+    per launch, over the round and at the steady-state depths), or None if
+    there is none or the kernel's source has changed since the counters were
+    taken."""
     import hashlib
     import re
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
@@ -59,7 +59,7 @@ def measured_traffic(workload: str, kernel: str):
     src = os.path.join(ROOT, rec["source"])
     if not os.path.exists(src) or hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
         return None
-    return float(rec["traffic_bytes_per_launch"])
+    return rec
 
 
 def kernel_work(cfg, kind: str, d: int):
@@ -221,21 +221,20 @@ def time_consumer(torch, cfg, out, stream, reps: int = 50) -> dict:
 
 
 def gpu_env(torch) -> dict:
-    """Device, HIP runtime and the shader clock (rocm-smi, sampled right after
-    the timed replays; null when the tool is unavailable)."""
+    """Device, HIP runtime and the shader clock, read from the device's
+    pp_dpm_sclk file in sysfs (the level marked current), sampled right after
+    the timed replays; null where the file is not readable."""
     props = torch.cuda.get_device_properties(0)
     env = {"device": torch.cuda.get_device_name(0), "arch": getattr(props, "gcnArchName", None),
            "compute_units": props.multi_processor_count, "hip": torch.version.hip, "sclk_mhz": None}
     try:
-        res = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True, text=True, timeout=15)
-        data = json.loads(res.stdout) if res.returncode == 0 else {}
-        for card in data.values():
-            for key, val in card.items():   # e.g. "sclk clock speed:": "(2400Mhz)"
-                m = re.search(r"(\d+)\s*mhz", str(val), re.I)
-                if key.lower().startswith("sclk") and m:
+        pci = f"{props.pci_domain_id:04x}:{props.pci_bus_id:02x}:{props.pci_device_id:02x}.0"
+        with open(f"/sys/bus/pci/devices/{pci}/pp_dpm_sclk") as f:
+            for line in f:                  # e.g. "1: 2400Mhz *"
+                m = re.search(r"(\d+)\s*mhz\s*\*", line, re.I)
+                if m:
                     env["sclk_mhz"] = int(m.group(1))
-            break
-    except (OSError, ValueError, subprocess.SubprocessError):
+    except (OSError, AttributeError, ValueError):
         pass
     return env
 
@@ -375,13 +374,24 @@ def main() -> int:
     torch.cuda.synchronize()
     dur = {name: [] for name in D.KERNEL_NAMES + ["prune"]}
     work = {name: [0.0, 0.0] for name in D.KERNEL_NAMES + ["prune"]}
+    # the steady-state depths: those with the most parent rows (every depth
+    # after the level sizes stop growing)
+    sizes = [1] + cfg.level_sizes()
+    steady = [d for d in range(1, cfg.depth + 1) if sizes[d - 1] == max(sizes[:cfg.depth])]
+    steady_t = {name: 0.0 for name in D.KERNEL_NAMES}
+    steady_w = {name: [0.0, 0.0] for name in D.KERNEL_NAMES}
     for i in range(K):
         for d in range(1, cfg.depth + 1):
             for c, name in enumerate(D.KERNEL_NAMES):
                 j = (d - 1) * nk + c
-                dur[name].append(kev[i][2 * j].elapsed_time(kev[i][2 * j + 1]) * 1e3)
+                t_ = kev[i][2 * j].elapsed_time(kev[i][2 * j + 1]) * 1e3
+                dur[name].append(t_)
+                b_, f_ = kernel_work(cfg, name, d)
+                if d in steady:
+                    steady_t[name] += t_
+                    steady_w[name][0] += b_
+                    steady_w[name][1] += f_
                 if i == 0:
-                    b_, f_ = kernel_work(cfg, name, d)
                     work[name][0] += b_
                     work[name][1] += f_
         j = cfg.depth * nk
@@ -408,21 +418,45 @@ def main() -> int:
     if roof["frac"] < 0.1:
         roof["note"] = ("latency-bound: each launch moves little data, so its duration is launch and "
                         "dependent-load latency, not bandwidth")
-    roof["traffic"] = measured_traffic(cfg.name, dom)
+    traffic = measured_traffic(cfg.name, dom)
+    roof["traffic"] = float(traffic["traffic_bytes_per_launch"]) if traffic else None
     roof["kernel"] = dom
     roof["algorithmic_bytes_per_launch"] = bytes_round / launches
     roof["algorithmic_flops_per_launch"] = flops_round / launches
     roof["avg_launch_us"] = kernels[dom]["avg_us_per_launch"]
+
+    def steady_state(name, bound):
+        t_ = steady_t[name] * 1e-6
+        if t_ <= 0:
+            return None
+        b_, f_ = steady_w[name]
+        ach = f_ / t_ / 1e12 if bound == "mfma" else b_ / t_ / 1e9
+        peak = MFMA_BF16_PEAK_TFS if bound == "mfma" else HBM_PEAK_GBS
+        n = len(steady) * K
+        return {"depths": [steady[0], steady[-1]], "rows": cfg.batch * sizes[steady[0] - 1],
+                "avg_launch_us": steady_t[name] / n, "algorithmic_bytes_per_launch": b_ / n,
+                "algorithmic_flops_per_launch": f_ / n, "achieved": ach, "frac": ach / peak}
+
+    if dom in steady_t:
+        roof["steady_state"] = steady_state(dom, roof["bound"])
+        if roof["steady_state"]:
+            roof["steady_state"]["traffic"] = (float(traffic.get("steady_traffic_bytes_per_launch",
+                                                                 traffic["traffic_bytes_per_launch"]))
+                                               if traffic else None)
     # second roofline of the per-row softmax/top-k pass (HBM); with a shared
     # candidate set this slot is the candidate-set pass over L^base at d = 1
-    lb, _ = work["lse_topk"]
-    lse_t = kernels["lse_topk"]["us_per_round"] * 1e-6
-    lse_roof = {"bound": "hbm", "achieved": lb / lse_t / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": lb / lse_t / 1e9 / HBM_PEAK_GBS,
-                "note": ("candidate sets TopK(L^base, K) of every depth, built once per round"
-                         if getattr(cfg, "candidates", 0) else
-                         "z is written by the projection just before; below ~256 MB it can be served "
-                         "from the Infinity Cache rather than HBM")}
+    # (over the depths that launch it)
+    lse_d = [d for d in range(1, cfg.depth + 1) if kernel_work(cfg, "lse_topk", d)[0] > 0]
+    lse_roof = None
+    if lse_d:
+        lb = sum(kernel_work(cfg, "lse_topk", d)[0] for d in lse_d)
+        lse_t = sum(dur["lse_topk"][i * cfg.depth + d - 1] for i in range(K) for d in lse_d) / K * 1e-6
+        lse_roof = {"bound": "hbm", "achieved": lb / lse_t / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": lb / lse_t / 1e9 / HBM_PEAK_GBS, "depths": lse_d,
+                    "note": ("candidate sets TopK(L^base, K) of every depth, built once per round"
+                             if getattr(cfg, "candidates", 0) else
+                             "z is written by the projection just before; below ~256 MB it can be served "
+                             "from the Infinity Cache rather than HBM")}
     proj_flops = work["logits"][1] / (kernels["logits"]["us_per_round"] * 1e-6) / 1e12
 
     # achievable ceilings measured in this job: stream U once (the projection's
@@ -433,8 +467,16 @@ def main() -> int:
     meas = cal["mfma_TFs"] if roof["bound"] == "mfma" else cal["read_GBs"]
     roof["measured_peak"] = meas
     roof["frac_of_measured"] = roof["achieved"] / meas
-    lse_roof["measured_peak"] = cal["read_GBs"]
-    lse_roof["frac_of_measured"] = lse_roof["achieved"] / cal["read_GBs"]
+    if lse_roof:
+        lse_roof["measured_peak"] = cal["read_GBs"]
+        lse_roof["frac_of_measured"] = lse_roof["achieved"] / cal["read_GBs"]
+        if not getattr(cfg, "candidates", 0) and steady_w["lse_topk"][0] > 0:
+            lse_roof["steady_state"] = steady_state("lse_topk", "hbm")
+            if lse_roof["steady_state"]:
+                lse_roof["steady_state"]["frac_of_measured"] = (lse_roof["steady_state"]["achieved"] /
+                                                                cal["read_GBs"])
+    if roof.get("steady_state"):
+        roof["steady_state"]["frac_of_measured"] = roof["steady_state"]["achieved"] / meas
 
     sizes = [1] + cfg.level_sizes()
     nodes = cfg.batch * sum(sizes[d - 1] * cfg.branch for d in range(1, cfg.depth + 1))
