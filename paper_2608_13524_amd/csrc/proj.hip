@@ -48,12 +48,14 @@ __device__ __forceinline__ int64_t bias_base(const KArgs& a, int m) {
   return int64_t(a.group_index ? a.group_index[g] : g) * a.bias_stride;
 }
 
-template <int EPI, bool BF16>
+// NTS: logits stored with non-temporal stores (outputs far beyond the caches).
+template <int EPI, bool BF16, bool NTS = false>
 __device__ __forceinline__ void emit(const KArgs& a, int m, int n, float acc) {
   const int64_t bb = bias_base(a, m);
   const int64_t o = int64_t(m) * a.N + n;
   if constexpr (EPI == EPI_LOGITS) {
-    a.out[o] = acc + a.bias_f32[bb + n];
+    if constexpr (NTS) __builtin_nontemporal_store(acc + a.bias_f32[bb + n], a.out + o);
+    else a.out[o] = acc + a.bias_f32[bb + n];
   } else {
     a.out[o] = acc;
     float hb;
@@ -100,14 +102,15 @@ __device__ __forceinline__ u32x4 ld_stream(const uint16_t* p) {
 __device__ __forceinline__ u32x4 ld_cached(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ int lds_swizzle(int row) { return (row ^ (row >> 3)) & 7; }
 
-template <int EPI>
+template <int EPI, bool NTS = false>
 __device__ __forceinline__ void emit4(const KArgs& a, int m, int n, f32x4 v, bool vec) {
   const int64_t bb = bias_base(a, m);
   const int64_t o = int64_t(m) * a.N + n;
   if (vec && n + 3 < a.N) {
     if constexpr (EPI == EPI_LOGITS) {
       const f32x4 b = *reinterpret_cast<const f32x4*>(a.bias_f32 + bb + n);
-      *reinterpret_cast<f32x4*>(a.out + o) = v + b;
+      if constexpr (NTS) __builtin_nontemporal_store(v + b, reinterpret_cast<f32x4*>(a.out + o));
+      else *reinterpret_cast<f32x4*>(a.out + o) = v + b;
     } else {
       typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
       const u16x4 hb = *reinterpret_cast<const u16x4*>(static_cast<const uint16_t*>(a.bias_act) + bb + n);
@@ -121,7 +124,7 @@ __device__ __forceinline__ void emit4(const KArgs& a, int m, int n, f32x4 v, boo
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
-    if (n + i < a.N) emit<EPI, true>(a, m, n + i, v[i]);
+    if (n + i < a.N) emit<EPI, true, NTS>(a, m, n + i, v[i]);
 }
 
 template <int MT, int NT, int KW, int D, int EPI>
@@ -426,7 +429,9 @@ __global__ __launch_bounds__(512) void proj_bf16_big(KArgs a, int vec, BigPlan p
   const unsigned vo1 = unsigned(lrow * K * 2 + ((lcp ^ swz16(8 + lrow)) * 16));
   const int sw = swz16(r32 & 15);
 
-  // wave tile: weight rows 64 q + 32 i + (0..31) x node rows 128 grp + 32 j + (0..31)
+  // wave tile: weight rows 64 q + 32 i + (0..31) x node rows 128 grp + 32 j +
+  // (0..31); each MFMA takes the node rows as its first operand, so that it
+  // produces out[m][n] with n = the lane (see the epilogue)
   f32x16 acc[2][4];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -470,7 +475,7 @@ __global__ __launch_bounds__(512) void proj_bf16_big(KArgs a, int vec, BigPlan p
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(A[sub][i], B[sub][j], acc[i][j]);
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(B[sub][j], A[sub][i], acc[i][j]);
   };
   // A bare barrier: the workgroup fence of __syncthreads would also wait for
   // the loads still in flight for the next step.  The waits that the data
@@ -520,8 +525,14 @@ __global__ __launch_bounds__(512) void proj_bf16_big(KArgs a, int vec, BigPlan p
     }
   }
 
-  // elements 4 t .. 4 t + 3 of acc[i][j] are the node row m = 128 grp + 32 j
-  // + l % 32 at the 4 consecutive weight rows n = 64 q + 32 i + 8 t + 4 (l / 32)
+  // element v of acc[i][j] in lane l is out[m][n] at node row m = 128 grp +
+  // 32 j + 8 (v / 4) + 4 (l / 32) + v % 4 and weight row n = 64 q + 32 i +
+  // l % 32: the 32 lanes of a half-wave hold 32 consecutive n of one m, so
+  // every store instruction writes whole 128-byte lines.  The logits, far
+  // beyond the caches and read back right away by the softmax pass, are
+  // stored non-temporally (whole lines written around the caches read back
+  // at the rate of data not written recently).
+  (void)vec;
   if (slot >= 0) {
     float* P = pl.split + size_t(slot) * (GBM * GBN);
 #pragma unroll
@@ -529,30 +540,50 @@ __global__ __launch_bounds__(512) void proj_bf16_big(KArgs a, int vec, BigPlan p
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
-          *reinterpret_cast<f32x4*>(P + (128 * grp + 32 * j + r32) * GBN + 64 * q + 32 * i + 8 * t + 4 * kh) =
-              f32x4{acc[i][j][4 * t], acc[i][j][4 * t + 1], acc[i][j][4 * t + 2], acc[i][j][4 * t + 3]};
+        for (int v = 0; v < 16; ++v)
+          P[(128 * grp + 32 * j + 8 * (v >> 2) + 4 * kh + (v & 3)) * GBN + 64 * q + 32 * i + r32] = acc[i][j][v];
     return;
   }
+  // one bias row per 32-row block when the row groups are multiples of 32
+  const bool block_bias = a.rows_per_group % 32 == 0;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 2; ++i) {
+    const int n = nl + 64 * q + 32 * i + r32;
+    const bool n_new = n >= n0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int m = ml + 128 * grp + 32 * j + r32;
-      if (m < m0) continue;
+      const int mb = ml + 128 * grp + 32 * j;
+      if (mb + 31 < m0) continue;
+      if (block_bias) {
+        const int64_t bb = bias_base(a, mb) + n;
+        if constexpr (EPI == EPI_LOGITS) {
+          const float b = n_new ? a.bias_f32[bb] : 0.f;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int n = nl + 64 * q + 32 * i + 8 * t + 4 * kh;
-        const f32x4 v = f32x4{acc[i][j][4 * t], acc[i][j][4 * t + 1], acc[i][j][4 * t + 2], acc[i][j][4 * t + 3]};
-        if (n >= n0) {
-          emit4<EPI>(a, m, n, v, vec != 0);
+          for (int v = 0; v < 16; ++v) {
+            const int m = mb + 8 * (v >> 2) + 4 * kh + (v & 3);
+            if (m >= m0 && n_new) __builtin_nontemporal_store(acc[i][j][v] + b, a.out + int64_t(m) * N + n);
+          }
         } else {
+          const float hb = n_new ? bf16_to_f32(static_cast<const uint16_t*>(a.bias_act)[bb]) : 0.f;
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (n + e >= n0) emit<EPI, true>(a, m, n + e, v[e]);
+          for (int v = 0; v < 16; ++v) {
+            const int m = mb + 8 * (v >> 2) + 4 * kh + (v & 3);
+            if (m >= m0 && n_new) {
+              const int64_t o = int64_t(m) * N + n;
+              a.out[o] = acc[i][j][v];
+              static_cast<uint16_t*>(a.act_out)[o] = f32_to_bf16(tanhf(acc[i][j][v] + hb));
+            }
+          }
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int m = mb + 8 * (v >> 2) + 4 * kh + (v & 3);
+          if (m >= m0 && n_new) emit<EPI, true, EPI == EPI_LOGITS>(a, m, n, acc[i][j][v]);
         }
       }
     }
+  }
 }
 
 // The split tiles: 16 blocks per tile, each 16 rows x 256 columns; every
@@ -573,11 +604,11 @@ __global__ __launch_bounds__(256) void proj_big_fixup(KArgs a, int vec, BigPlan 
     f32x4 v = *reinterpret_cast<const f32x4*>(P + e);
     for (int pc = 1; pc < pl.pieces; ++pc) v += *reinterpret_cast<const f32x4*>(P + size_t(pc) * (GBM * GBN) + e);
     if (n >= tl.n0) {
-      emit4<EPI>(a, m, n, v, vec != 0);
+      emit4<EPI, EPI == EPI_LOGITS>(a, m, n, v, vec != 0);
     } else {
 #pragma unroll
       for (int k = 0; k < 4; ++k)
-        if (n + k >= tl.n0) emit<EPI, true>(a, m, n + k, v[k]);
+        if (n + k >= tl.n0) emit<EPI, true, EPI == EPI_LOGITS>(a, m, n + k, v[k]);
     }
   }
 }
