@@ -43,6 +43,10 @@ SMALL = {
     "bf16-k20": small(branch=20, width=24, budget=70, seed=48),       # top-k bucket 32
     # >= 512 parent rows: the head's 256x256 tiles split along K (512 rows: 4 tiles in 2 pieces each)
     "bf16-head-split": small(batch=8, width=64, branch=8, depth=4, budget=120, vocab=4099, hidden=512, seed=42),
+    # 540 rows in groups of 60 (not a multiple of 32): the head's 256x256 tiles split along K with
+    # a bias row looked up per element
+    "bf16-head-split-ragged": small(batch=9, width=60, branch=8, depth=4, budget=120, vocab=4099, hidden=512,
+                                    seed=44),
     # 1024 rows x 16400 vocabulary: 260 logit tiles, the 4 past one wave of 256 CUs split in 2 pieces
     "bf16-logits-split": small(batch=16, width=64, branch=8, depth=4, budget=100, vocab=16400, hidden=512,
                                seed=43),
