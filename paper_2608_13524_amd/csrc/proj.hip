@@ -102,6 +102,32 @@ __device__ __forceinline__ u32x4 ld_stream(const uint16_t* p) {
 __device__ __forceinline__ u32x4 ld_cached(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ int lds_swizzle(int row) { return (row ^ (row >> 3)) & 7; }
 
+typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+
+// The four bias values of outputs (m, n..n+3) as fp32 (vector path only).
+template <int EPI>
+__device__ __forceinline__ f32x4 bias4(const KArgs& a, int m, int n) {
+  const int64_t bb = bias_base(a, m) + n;
+  if constexpr (EPI == EPI_LOGITS) return *reinterpret_cast<const f32x4*>(a.bias_f32 + bb);
+  const u16x4 hb = *reinterpret_cast<const u16x4*>(static_cast<const uint16_t*>(a.bias_act) + bb);
+  return f32x4{bf16_to_f32(hb[0]), bf16_to_f32(hb[1]), bf16_to_f32(hb[2]), bf16_to_f32(hb[3])};
+}
+
+// emit4's vector path with the bias already loaded (the same arithmetic).
+template <int EPI>
+__device__ __forceinline__ void emit4_bias(const KArgs& a, int m, int n, f32x4 v, f32x4 b) {
+  const int64_t o = int64_t(m) * a.N + n;
+  if constexpr (EPI == EPI_LOGITS) {
+    *reinterpret_cast<f32x4*>(a.out + o) = v + b;
+  } else {
+    *reinterpret_cast<f32x4*>(a.out + o) = v;
+    u16x4 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = f32_to_bf16(tanhf(v[i] + b[i]));
+    *reinterpret_cast<u16x4*>(static_cast<uint16_t*>(a.act_out) + o) = r;
+  }
+}
+
 template <int EPI, bool NTS = false>
 __device__ __forceinline__ void emit4(const KArgs& a, int m, int n, f32x4 v, bool vec) {
   const int64_t bb = bias_base(a, m);
@@ -112,7 +138,6 @@ __device__ __forceinline__ void emit4(const KArgs& a, int m, int n, f32x4 v, boo
       if constexpr (NTS) __builtin_nontemporal_store(v + b, reinterpret_cast<f32x4*>(a.out + o));
       else *reinterpret_cast<f32x4*>(a.out + o) = v + b;
     } else {
-      typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
       const u16x4 hb = *reinterpret_cast<const u16x4*>(static_cast<const uint16_t*>(a.bias_act) + bb + n);
       *reinterpret_cast<f32x4*>(a.out + o) = v;
       u16x4 r;
@@ -164,6 +189,19 @@ __global__ __launch_bounds__(64 * KW) void proj_bf16_stream(KArgs a, int vec) {
   const uint16_t* xp[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) xp[mt] = X + int64_t(min(mt * 16 + r16, M - 1)) * K + kg * 8;
+
+  // When every wave emits at most one 16x16 tile, its lanes fetch their
+  // bias values now, so the epilogue does not wait on a last dependent load.
+  constexpr bool kPre = NT * MT <= KW;
+  f32x4 pre_b = f32x4{0.f, 0.f, 0.f, 0.f};
+  bool pre_ok = false;
+  if constexpr (kPre) {
+    if (wave < NT * MT) {
+      const int m = (wave % MT) * 16 + r16, n = n0 + (wave / MT) * 16 + kg * 4;
+      pre_ok = vec != 0 && m < M && n + 3 < N;
+      if (pre_ok) pre_b = bias4<EPI>(a, m, n);
+    }
+  }
 
   const int chunks = K >> 6;
   const int per = (chunks + KW - 1) / KW;
@@ -226,7 +264,10 @@ __global__ __launch_bounds__(64 * KW) void proj_bf16_stream(KArgs a, int vec) {
 #pragma unroll
     for (int w = 1; w < KW; ++w) v += red[w][p][lane];
     const int m = mt * 16 + r16;
-    if (m < M) emit4<EPI>(a, m, n0 + nt * 16 + kg * 4, v, vec != 0);
+    if (m < M) {
+      if (kPre && pre_ok) emit4_bias<EPI>(a, m, n0 + nt * 16 + kg * 4, v, pre_b);
+      else emit4<EPI>(a, m, n0 + nt * 16 + kg * 4, v, vec != 0);
+    }
   }
 }
 
