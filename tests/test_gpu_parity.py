@@ -50,6 +50,10 @@ SMALL = {
     # 1024 rows x 16400 vocabulary: 260 logit tiles, the 4 past one wave of 256 CUs split in 2 pieces
     "bf16-logits-split": small(batch=16, width=64, branch=8, depth=4, budget=100, vocab=16400, hidden=512,
                                seed=43),
+    # the largest vocabulary (2^20: token ids use every bit of their key field)
+    "bf16-max-vocab": small(batch=2, vocab=1 << 20, hidden=64, depth=3, width=8, branch=8, budget=16, seed=60),
+    # the largest selection: 512 parents x 8 children = 4096 candidates per request, |S| = 1096 > B
+    "bf16-max-sort": small(batch=1, vocab=5003, hidden=64, depth=4, width=512, branch=8, budget=600, seed=61),
     "fp32-small": small(precision=W.FP32, hidden=48, sigma_w=0.1, seed=40),
     "fp32-tiny-vocab": small(precision=W.FP32, vocab=7, hidden=5, branch=3, width=5, budget=12, seed=41),
     # shared candidate sets C_d = TopK(L_d^base, K)
