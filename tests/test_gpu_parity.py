@@ -54,6 +54,11 @@ SMALL = {
     "bf16-max-vocab": small(batch=2, vocab=1 << 20, hidden=64, depth=3, width=8, branch=8, budget=16, seed=60),
     # the largest selection: 512 parents x 8 children = 4096 candidates per request, |S| = 1096 > B
     "bf16-max-sort": small(batch=1, vocab=5003, hidden=64, depth=4, width=512, branch=8, budget=600, seed=61),
+    # the deepest tree (64 levels: every depth of the prune key and the ancestor mask)
+    "bf16-max-depth": small(batch=2, vocab=1031, hidden=64, depth=64, width=4, branch=2, budget=200, seed=62),
+    # the widest branching over the full vocabulary (k = 32, the top-k bucket's full size)
+    "bf16-k32": small(batch=2, vocab=4099, hidden=128, depth=4, width=100, branch=32, budget=150, temperature=0.7,
+                      seed=63),
     "fp32-small": small(precision=W.FP32, hidden=48, sigma_w=0.1, seed=40),
     "fp32-tiny-vocab": small(precision=W.FP32, vocab=7, hidden=5, branch=3, width=5, budget=12, seed=41),
     # shared candidate sets C_d = TopK(L_d^base, K)
