@@ -45,6 +45,7 @@ SMALL = {
     "heap-k12": small(branch=12, budget=40, seed=62),                  # top-k bucket 16
     "heap-k20": small(branch=20, budget=40, seed=63),                  # top-k bucket 32
     "heap-wide-B": small(batch=2, branch=8, budget=300, depth=6, seed=64),   # > 64 slots per arg-min
+    "heap-max-B": small(batch=2, vocab=1031, hidden=64, branch=8, depth=8, budget=1024, seed=77),   # the most pops
     "heap-dry": small(vocab=7, hidden=64, branch=2, depth=3, budget=40, seed=65),   # 14 prefixes exist
     "heap-depth1": small(depth=1, budget=6, seed=66),                  # every pop at depth L
     "heap-B1": small(budget=1, seed=67),
