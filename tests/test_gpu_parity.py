@@ -59,6 +59,8 @@ SMALL = {
     # the widest branching over the full vocabulary (k = 32, the top-k bucket's full size)
     "bf16-k32": small(batch=2, vocab=4099, hidden=128, depth=4, width=100, branch=32, budget=150, temperature=0.7,
                       seed=63),
+    # the widest level (2048 nodes; |S| = 4094 of at most 4096) and 1024-row depths
+    "bf16-max-width": small(batch=1, vocab=1031, hidden=64, depth=11, width=2048, branch=2, budget=3000, seed=64),
     "fp32-small": small(precision=W.FP32, hidden=48, sigma_w=0.1, seed=40),
     "fp32-tiny-vocab": small(precision=W.FP32, vocab=7, hidden=5, branch=3, width=5, budget=12, seed=41),
     # shared candidate sets C_d = TopK(L_d^base, K)
@@ -72,6 +74,7 @@ SMALL = {
     "shared-fp32": small(precision=W.FP32, hidden=48, candidates=9, branch=9, sigma_w=0.1, seed=54),
     "shared-K-eq-V": small(vocab=40, candidates=40, branch=6, width=6, hidden=64, seed=55),
     "shared-k1": small(candidates=8, branch=1, budget=8, seed=56),
+    "shared-K256": small(batch=2, candidates=256, branch=16, width=16, depth=4, budget=60, hidden=128, seed=65),
     "shared-K64-two-row-blocks": small(batch=2, candidates=64, branch=8, width=80, budget=120, vocab=3001,
                                        hidden=128, seed=58),   # 80 rows x 64 candidates
 
