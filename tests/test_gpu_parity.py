@@ -75,6 +75,9 @@ SMALL = {
     "shared-K-eq-V": small(vocab=40, candidates=40, branch=6, width=6, hidden=64, seed=55),
     "shared-k1": small(candidates=8, branch=1, budget=8, seed=56),
     "shared-K256": small(batch=2, candidates=256, branch=16, width=16, depth=4, budget=60, hidden=128, seed=65),
+    # the paper's fixed variant (Sec. 4.1): K = 64, 4 nodes at each of 16 depths = B, so nothing is pruned
+    "paper-fixed": small(batch=2, vocab=1031, hidden=64, depth=16, width=4, branch=4, budget=64, candidates=64,
+                         depth_bonus=0.0, seed=90),
     "shared-K64-two-row-blocks": small(batch=2, candidates=64, branch=8, width=80, budget=120, vocab=3001,
                                        hidden=128, seed=58),   # 80 rows x 64 candidates
 
