@@ -287,6 +287,8 @@ def main() -> int:
     ap.add_argument("--no-heap", action="store_true", help="skip the sequential-heap comparison")
     ap.add_argument("--schedule", default="dartree", choices=["dartree", "heap"],
                     help="heap: time only the sequential-heap baseline (for a kernel trace of it alone)")
+    ap.add_argument("--width", type=int, default=None, help="override the workload's layer width W (sweeps)")
+    ap.add_argument("--budget", type=int, default=None, help="override the workload's budget B (sweeps)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only (--gpus 1): the library builds trees on one device. Requests "
@@ -298,6 +300,9 @@ def main() -> int:
     assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
     dev = torch.device("cuda:0")
     cfg = W.CONFIGS[args.config]
+    if args.width is not None or args.budget is not None:
+        cfg = cfg.replace(width=args.width if args.width is not None else cfg.width,
+                          budget=args.budget if args.budget is not None else cfg.budget)
     log(f"workload {cfg.name}: generating inputs")
     inputs = W.make_inputs(cfg)
     p = D.Params.of(cfg)
