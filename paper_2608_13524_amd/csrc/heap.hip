@@ -43,8 +43,8 @@ template <int KB>
 __global__ __launch_bounds__(kHeapThreads) void heap_step(HeapArgs a) {
   __shared__ float c_lp[DARTREE_MAX_CANDIDATES];   // slot i's children in rank order
   __shared__ int32_t c_tok[DARTREE_MAX_CANDIDATES];
-  __shared__ float rz[DARTREE_MAX_CANDIDATES];     // the row over C_d (shared set)
-  __shared__ int32_t rid[DARTREE_MAX_CANDIDATES];
+  __shared__ __attribute__((aligned(16))) float rz[DARTREE_MAX_CANDIDATES];     // the row over C_d (shared set)
+  __shared__ __attribute__((aligned(16))) int32_t rid[DARTREE_MAX_CANDIDATES];
   __shared__ int s_slot, s_tok;
   const int q = blockIdx.x, i = a.step;
   const int B = a.budget, L = a.depth, k = a.k, b = a.batch;
@@ -78,9 +78,21 @@ __global__ __launch_bounds__(kHeapThreads) void heap_step(HeapArgs a) {
       for (int c = lane; c < K; c += 64) {
         const float v = rz[c];
         const int id = rid[c];
+        // 16-byte reads of four values and four ids at a time (every lane
+        // reads the same address), then the tail
+        typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+        const f32x4* rz4 = reinterpret_cast<const f32x4*>(rz);
+        const i32x4* rid4 = reinterpret_cast<const i32x4*>(rid);
+        const int K4 = K & ~3;
         int rank = 0;
-#pragma unroll 8
-        for (int o = 0; o < K; ++o) rank += int(better(rz[o], rid[o], v, id));
+#pragma unroll 4
+        for (int o = 0; o < K4; o += 4) {
+          const f32x4 zv = rz4[o >> 2];
+          const i32x4 iv = rid4[o >> 2];
+          rank += int(better(zv[0], iv[0], v, id)) + int(better(zv[1], iv[1], v, id)) +
+                  int(better(zv[2], iv[2], v, id)) + int(better(zv[3], iv[3], v, id));
+        }
+        for (int o = K4; o < K; ++o) rank += int(better(rz[o], rid[o], v, id));
         if (rank < k) {
           const float lp = (v - m) / a.tau - log_s;
           c_lp[rank] = lp;

@@ -58,8 +58,8 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
     // shared candidate set: row j's K corrected logits over C_d -> log q~
     // normalised over C_d, and its k best by (z desc, id asc), ranked by
     // counting over the row (staged in this wave's LDS row)
-    __shared__ float rz[16][DARTREE_MAX_CANDIDATES];
-    __shared__ int32_t rid[16][DARTREE_MAX_CANDIDATES];
+    __shared__ __attribute__((aligned(16))) float rz[16][DARTREE_MAX_CANDIDATES];
+    __shared__ __attribute__((aligned(16))) int32_t rid[16][DARTREE_MAX_CANDIDATES];
     const int nk = a.shared_k;
     const float scale = kLog2e / a.tau;
     const int lane = threadIdx.x & 63;
@@ -82,9 +82,21 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
       for (int c = lane; c < nk; c += 64) {
         const float v = rz[wave][c];
         const int id = rid[wave][c];
+        // 16-byte reads of four values and four ids at a time (every lane
+        // reads the same address), then the tail
+        typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+        const f32x4* rz4 = reinterpret_cast<const f32x4*>(rz[wave]);
+        const i32x4* rid4 = reinterpret_cast<const i32x4*>(rid[wave]);
+        const int nk4 = nk & ~3;
         int rank = 0;
-#pragma unroll 8
-        for (int o = 0; o < nk; ++o) rank += int(better(rz[wave][o], rid[wave][o], v, id));
+#pragma unroll 4
+        for (int o = 0; o < nk4; o += 4) {
+          const f32x4 zv = rz4[o >> 2];
+          const i32x4 iv = rid4[o >> 2];
+          rank += int(better(zv[0], iv[0], v, id)) + int(better(zv[1], iv[1], v, id)) +
+                  int(better(zv[2], iv[2], v, id)) + int(better(zv[3], iv[3], v, id));
+        }
+        for (int o = nk4; o < nk; ++o) rank += int(better(rz[wave][o], rid[wave][o], v, id));
         if (rank < k) {
           const float lp = (v - m) / a.tau - log_s;
           c_logp[j * k + rank] = lp;
