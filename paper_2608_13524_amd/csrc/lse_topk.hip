@@ -30,7 +30,7 @@ __device__ __forceinline__ uint64_t block_merge(Partial& p, const float (&tv)[K]
                                                 float scale, int* slot) {
   constexpr int kWaves = kBlock / 64;
   __shared__ Partial sp[kWaves];
-  __shared__ uint64_t sk[kWaves * K];
+  __shared__ __attribute__((aligned(16))) uint64_t sk[kWaves * K];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const Partial wp = wave_partial(p, scale);
   uint64_t key[K], out[K];
@@ -53,9 +53,12 @@ __device__ __forceinline__ uint64_t block_merge(Partial& p, const float (&tv)[K]
   if (t >= n) return 0;
   const uint64_t e = sk[t];
   int rank = 0;
-  for (int j = 0; j < n; ++j) {
-    const uint64_t o = sk[j];
-    rank += int(o > e) + int(o == e && j < t);
+  // 16-byte reads of two keys at a time (n = kWaves k is even)
+  typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+  const u64x2* sk2 = reinterpret_cast<const u64x2*>(sk);
+  for (int j = 0; j < n; j += 2) {
+    const u64x2 o = sk2[j >> 1];
+    rank += int(o.x > e) + int(o.x == e && j < t) + int(o.y > e) + int(o.y == e && j + 1 < t);
   }
   *slot = rank;
   return e;

@@ -254,7 +254,7 @@ __global__ __launch_bounds__(1024) void prune_emit(LevelShape shape, int budget,
   // per supertree node, staged once: token, parent slot, score
   __shared__ int32_t s_tok[kSortMax], s_par[kSortMax];
   __shared__ float s_score[kSortMax];
-  __shared__ uint32_t rank_key[DARTREE_MAX_WIDTH];
+  __shared__ __attribute__((aligned(16))) uint32_t rank_key[DARTREE_MAX_WIDTH];
   __shared__ int32_t kept_at_depth;
 
   const int q = blockIdx.x;
@@ -317,8 +317,17 @@ __global__ __launch_bounds__(1024) void prune_emit(LevelShape shape, int budget,
     for (int i = threadIdx.x; i < nd; i += blockDim.x) {
       const uint32_t mine = rank_key[i];
       if (mine == ~0u) continue;
+      // 16-byte reads of four keys at a time, then the tail
+      typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+      const u32x4v* rk4 = reinterpret_cast<const u32x4v*>(rank_key);
+      const int nd4 = nd & ~3;
       int r = 0;
-      for (int j = 0; j < nd; ++j) r += (rank_key[j] < mine) | ((rank_key[j] == mine) & (j < i));
+      for (int j = 0; j < nd4; j += 4) {
+        const u32x4v kv = rk4[j >> 2];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) r += (kv[e] < mine) | ((kv[e] == mine) & (j + e < i));
+      }
+      for (int j = nd4; j < nd; ++j) r += (rank_key[j] < mine) | ((rank_key[j] == mine) & (j < i));
       out_idx[od + i] = base + r;
       par_out[base + r] = d == 1 ? -1 : out_idx[parent_node(d, od + i)];
       atomicAdd(&kept_at_depth, 1);
