@@ -28,7 +28,8 @@
  *  - Device pointers are HIP device memory owned by the caller; the library
  *    never allocates or frees device memory and keeps no pointer after return.
  *  - All work is enqueued on `stream` (a hipStream_t; 0 = the null stream);
- *    no call synchronises the host with the device.  Outputs are valid once
+ *    no call synchronises the host with the device (except the debug checks
+ *    enabled by DARTREE_DEBUG=1, see "Depth order").  Outputs are valid once
  *    the stream's work completes.
  *  - Every argument is validated on the host before anything is enqueued;
  *    on any error nothing is enqueued and no output is written.
@@ -51,7 +52,7 @@
 extern "C" {
 #endif
 
-#define DARTREE_ABI_VERSION 7
+#define DARTREE_ABI_VERSION 8
 
 /* Limits of this implementation (calls beyond them return
  * DARTREE_ERR_UNSUPPORTED). */
@@ -68,7 +69,10 @@ typedef enum dartree_status {
   DARTREE_ERR_INVALID_ARG = 1, /* a size, value or pointer violates the contract */
   DARTREE_ERR_UNSUPPORTED = 2, /* valid per the paper but beyond this library's limits */
   DARTREE_ERR_WORKSPACE = 3,   /* workspace missing, misaligned or smaller than required */
-  DARTREE_ERR_HIP = 4          /* a kernel launch failed (hipGetLastError) */
+  DARTREE_ERR_HIP = 4,         /* a kernel launch failed (hipGetLastError) */
+  DARTREE_ERR_ORDER = 5,       /* Algorithm 1's depths out of order on a workspace: the call would read
+                                  levels no earlier call produced (see "Depth order" below) */
+  DARTREE_ERR_NONFINITE = 6    /* debug mode only: a normaliser of the depth just run is not finite */
 } dartree_status;
 
 typedef enum dartree_precision {
@@ -161,17 +165,35 @@ dartree_status dartree_validate(const dartree_params* p);
  * and the per-depth scratch (states, features, logits [b*W][V] fp32). */
 dartree_status dartree_workspace_size(const dartree_params* p, size_t* bytes);
 
+/* Depth order.  Algorithm 1's loop runs d = 1..L and depth d reads the level
+ * and states depth d - 1 left in the workspace.  The library records, per
+ * workspace (by address, up to 256 workspaces, least recently used dropped),
+ * the parameters and the last depth enqueued by dartree_expand_depth or
+ * dartree_build_tree on the host.  dartree_expand_depth(d > 1) on a
+ * workspace whose record is not (the same parameters, d - 1), and
+ * dartree_prune on one whose record is not depth L, return DARTREE_ERR_ORDER
+ * with nothing enqueued; d = 1 always starts a new round.  Replays of a
+ * captured graph do not update the record.  Each depth's selection kernel
+ * also writes {parameters, d} into the workspace; with the environment
+ * variable DARTREE_DEBUG=1 (read once per process) dartree_expand_depth and
+ * dartree_prune synchronise the stream and check that device record too,
+ * and dartree_expand_depth checks, after its kernels ran, that the depth's
+ * normalisers are finite (DARTREE_ERR_NONFINITE).  Debug checks are skipped
+ * while the stream is being captured. */
+
 /* One iteration of Algorithm 1's depth loop (d = 1..L): score every child of
  * every node of S_{d-1} over the full vocabulary, keep the top-W as S_d and
  * compute their states.  Reads S_{d-1} from `ws` (d = 1 reads
  * in->prefix_state), so depths must be enqueued in order 1..L on one stream
- * with the same workspace.  ws: device, 256-byte aligned, >= workspace_size. */
+ * with the same workspace (DARTREE_ERR_ORDER otherwise, see above).
+ * ws: device, 256-byte aligned, >= workspace_size. */
 dartree_status dartree_expand_depth(const dartree_params* p, const dartree_inputs* in,
                                     int32_t d, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Deferred best-first pruning (Sec. 3.3, Algorithm 1 after the loop): top-B of
  * the supertree held in `ws` after dartree_expand_depth(1..L), emitted as the
- * flattened tree with parent indices and the ancestor-or-self mask. */
+ * flattened tree with parent indices and the ancestor-or-self mask.
+ * DARTREE_ERR_ORDER if the workspace's record is not depth L. */
 dartree_status dartree_prune(const dartree_params* p, const void* ws, size_t ws_bytes,
                              const dartree_tree* out, hipStream_t stream);
 
@@ -202,7 +224,9 @@ dartree_status dartree_build_tree_timed(const dartree_params* p, const dartree_i
                                         hipStream_t stream);
 
 /* Copy the supertree levels and per-parent candidates out of `ws` into the
- * caller's device buffers (layouts in dartree_supertree), for inspection. */
+ * caller's device buffers (layouts in dartree_supertree), for inspection.
+ * Levels past the last depth enqueued hold stale values; DARTREE_ERR_ORDER
+ * if no depth has been enqueued on `ws` with these parameters. */
 dartree_status dartree_export_supertree(const dartree_params* p, const void* ws, size_t ws_bytes,
                                         const dartree_supertree* dst, hipStream_t stream);
 
@@ -210,9 +234,17 @@ dartree_status dartree_export_supertree(const dartree_params* p, const void* ws,
  * for slot i of request q) out of `ws` into `dst` (device).  Valid for
  * 1 <= d < L once dartree_expand_depth(d) has run and until
  * dartree_expand_depth(d + 2) is enqueued (states are double-buffered; the
- * last depth computes none). */
+ * last depth computes none); DARTREE_ERR_ORDER outside that window. */
 dartree_status dartree_export_states(const dartree_params* p, const void* ws, size_t ws_bytes, int32_t d,
                                      void* dst, hipStream_t stream);
+
+/* Copy the features a = act(tanh(A r + H_d)) of depth d's parent rows (act
+ * [b][n_{d-1}][h], row q*n_{d-1} + j for parent slot j of request q) out of
+ * `ws` into `dst` (device), for inspection.  Valid once
+ * dartree_expand_depth(d) has run and until the next depth is enqueued
+ * (DARTREE_ERR_ORDER otherwise). */
+dartree_status dartree_export_features(const dartree_params* p, const void* ws, size_t ws_bytes, int32_t d,
+                                       void* dst, hipStream_t stream);
 
 /* ---- single steps on caller buffers --------------------------------------
  * The kernels of one depth, exposed for callers that assemble their own loop
@@ -308,6 +340,7 @@ typedef struct dartree_heap_trace {
   int32_t* cand_ids;   /* [B][b][k] their token ids */
   void* states;        /* act [B+1][b][h] r of slot i (slots 1.. the head ran on) */
   int32_t* csets;      /* [b][L][K] shared candidate sets (candidates > 0 only) */
+  void* features;      /* act [B][b][h] the feature row a of slot i (steps the head ran) */
 } dartree_heap_trace;
 
 /* Bytes of device workspace for dartree_build_tree_heap (host only). */

@@ -180,14 +180,20 @@ def _rounder(precision: int) -> Callable[[np.ndarray], np.ndarray]:
 # One depth (Alg. 1, loop body)
 # ----------------------------------------------------------------------------
 
+def head_preimage(r: np.ndarray, A: np.ndarray, H_d: np.ndarray):
+    """Correction head before the feature is rounded: t_j = A r_j and
+    tanh(t_j + H_d), both [R][h] for ``r`` [R][h]."""
+    t = r @ A.T
+    return t, np.tanh(t + H_d[None, :])
+
+
 def head_features(r: np.ndarray, A: np.ndarray, H_d: np.ndarray, precision: int):
     """Correction head, state part: t_j = A r_j and a_j = rnd(tanh(t_j + H_d)).
 
     ``r`` is [R][h] (one parent state per row); returns (t, a), both [R][h].
     """
-    t = r @ A.T
-    a = _rounder(precision)(np.tanh(t + H_d[None, :]))
-    return t, a
+    t, pre = head_preimage(r, A, H_d)
+    return t, _rounder(precision)(pre)
 
 
 def vocab_logits(a: np.ndarray, U: np.ndarray, Lb_d: np.ndarray, chunk: int = 16384) -> np.ndarray:
@@ -252,6 +258,13 @@ def markov_states(U_tok: np.ndarray, e: float, precision: int) -> np.ndarray:
     return _rounder(precision)(e * U_tok)
 
 
+def state_preimage(p: Params, t_parent: np.ndarray, U_tok: np.ndarray) -> np.ndarray:
+    """The kept children's states before they are rounded: tanh(t + e U[u_d])
+    (recurrent head) or e U[u_d] (Markov head)."""
+    e = p.embed_scale
+    return e * U_tok if p.head == MARKOV else np.tanh(t_parent + e * U_tok)
+
+
 def next_states(p: Params, t_parent: np.ndarray, U_tok: np.ndarray) -> np.ndarray:
     """The state of each kept child under the configured head."""
     if p.head == MARKOV:
@@ -293,15 +306,17 @@ def _default_choose(req: int, d: int, parent, token, score, n_keep: int, level_r
 
 def build_supertree(dec: Decoded, requests=None, choose: Optional[Chooser] = None,
                     choose_topk: Optional[Callable] = None, keep_logp: bool = False,
-                    adopt_states: Optional[Callable] = None) -> Supertree:
+                    adopt_states: Optional[Callable] = None,
+                    adopt_features: Optional[Callable] = None) -> Supertree:
     """Alg. 1's depth loop for every request (slow: full fp64 vocabulary products).
 
     ``choose`` / ``choose_topk`` let a caller replace the two selections (used
     to follow another implementation's choices); by default the oracle makes
     its own.  ``choose_topk(req, d, j, z_row, logp_row, k)`` returns the ids of
-    parent j's candidate set.  ``adopt_states(req, d, r)`` may replace the
-    states of S_d computed here (to follow another implementation's rounding
-    of the recurrent state).
+    parent j's candidate set.  ``adopt_states(req, d, r, pre)`` may replace the
+    states of S_d computed here, and ``adopt_features(req, d, a, pre)`` the
+    features a of depth d's parent rows (to follow another implementation's
+    rounding); ``pre`` is the value before rounding (fp64).
     """
     p = dec.p
     choose = choose or _default_choose
@@ -316,6 +331,8 @@ def build_supertree(dec: Decoded, requests=None, choose: Optional[Chooser] = Non
         levels = []
         for d in range(1, p.depth + 1):
             t, a = head_features(r, dec.A, dec.H[b, d - 1], p.precision)
+            if adopt_features is not None:
+                a = adopt_features(b, d, a, head_preimage(r, dec.A, dec.H[b, d - 1])[1])
             cset = None
             if p.candidates > 0:
                 cset = candidate_set(dec.Lb[b, d - 1], p.candidates)
@@ -340,7 +357,7 @@ def build_supertree(dec: Decoded, requests=None, choose: Optional[Chooser] = Non
             levels.append(lvl)
             r = next_states(p, t[lvl.parent], dec.U[lvl.token])
             if adopt_states is not None and d < p.depth:
-                r = adopt_states(b, d, r)
+                r = adopt_states(b, d, r, state_preimage(p, t[lvl.parent], dec.U[lvl.token]))
             s = lvl.score
         out.append(levels)
     return Supertree(p, out)
@@ -455,14 +472,18 @@ def heap_entry(score: float, depth: int, parent: int, rank: int, token: int) -> 
 
 def sequential_heap(dec: Decoded, requests=None, choose_topk: Optional[Callable] = None,
                     choose_pop: Optional[Callable] = None,
-                    adopt_states: Optional[Callable] = None) -> list:
+                    adopt_states: Optional[Callable] = None,
+                    adopt_features: Optional[Callable] = None) -> list:
     """Sec. 3.1's exact best-first construction with the correction head run
     once per popped prefix (B pops per request).
 
     ``choose_topk(req, node, d, z_row, logp_row, k)`` may replace a node's
     k best children, ``choose_pop(req, step, heap)`` the index of the heap
-    item popped at a step (items are (key, (score, depth, parent, token))), and ``adopt_states(req, node, r)`` a popped node's
-    state (to follow another implementation's choices and rounding).
+    item popped at a step (items are (key, (score, depth, parent, token))),
+    ``adopt_states(req, node, r, pre)`` a popped node's state and
+    ``adopt_features(req, node, a, pre)`` the feature row the head computed on
+    it (to follow another implementation's choices and rounding; ``pre`` is
+    the value before rounding).
     """
     p = dec.p
     tau, e, beta = p.tau, p.embed_scale, p.depth_bonus
@@ -477,6 +498,8 @@ def sequential_heap(dec: Decoded, requests=None, choose_topk: Optional[Callable]
         def expand(n: int, r: np.ndarray):
             d = run.depth[n] + 1
             t, a = head_features(r[None, :], dec.A, dec.H[b, d - 1], p.precision)
+            if adopt_features is not None:
+                a = adopt_features(b, n, a, head_preimage(r[None, :], dec.A, dec.H[b, d - 1])[1])
             t_of[n] = t[0]
             cset = None
             if p.candidates > 0:
@@ -511,7 +534,7 @@ def sequential_heap(dec: Decoded, requests=None, choose_topk: Optional[Callable]
             if d < p.depth and len(run.token) - 1 < p.budget:   # the last pop's children are never popped
                 r = next_states(p, t_of[par][None, :], dec.U[v][None, :])[0]
                 if adopt_states is not None:
-                    r = adopt_states(b, n, r)
+                    r = adopt_states(b, n, r, state_preimage(p, t_of[par][None, :], dec.U[v][None, :])[0])
                 expand(n, r)
         runs.append(run)
     return runs

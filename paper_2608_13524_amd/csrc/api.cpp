@@ -2,9 +2,12 @@
 // of kernel launches for one round of Algorithm 1.  No function here touches
 // the device until every argument has been checked.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
+#include <vector>
 
 #include "internal.hpp"
 
@@ -44,6 +47,8 @@ Shape shape_of(const dartree_params& p) {
 }
 
 // Workspace layout (each region 256-byte aligned), R = b * W rows:
+//   hdr: u32 [4] {params key lo, key hi, last depth completed, 0} (written by
+//        the selection kernel of each depth; read by the debug order check)
 //   lvl_tok, lvl_par: i32 [L][b][W]     lvl_score: f32 [L][b][W]
 //   lse: f32 [L][R]   cand_logp: f32 [L][R][k]   cand_ids: i32 [L][R][k]
 //   state: act [2][R][h]   t: f32 [R][h]   a: act [R][h]   z: f32 [R][V]
@@ -52,7 +57,7 @@ Shape shape_of(const dartree_params& p) {
 //   split: partial sums of the projection tiles split along K (the head and
 //          the logits of one depth run one after the other and share it)
 struct Layout {
-  size_t lvl_tok, lvl_par, lvl_score, lse, cand_logp, cand_ids, state0, state1, t, a, z, k3, cset, cset_scratch,
+  size_t hdr, lvl_tok, lvl_par, lvl_score, lse, cand_logp, cand_ids, state0, state1, t, a, z, k3, cset, cset_scratch,
       split, split_bytes, total;
 };
 
@@ -71,6 +76,7 @@ Layout layout_of(const dartree_params& p, const Shape& s) {
   Layout l{};
   size_t o = 0;
   auto take = [&](size_t bytes) { const size_t at = o; o = align_up(o + bytes); return at; };
+  l.hdr = take(16);
   l.lvl_tok = take(L * b * W * 4);
   l.lvl_par = take(L * b * W * 4);
   l.lvl_score = take(L * b * W * 4);
@@ -161,6 +167,87 @@ const T* at(const void* base, size_t off) {
 
 dartree_status hip_status(hipError_t e) { return e == hipSuccess ? DARTREE_OK : DARTREE_ERR_HIP; }
 
+// ---------------------------------------------------------------------------
+// Depth order (Algorithm 1's loop runs d = 1..L, each depth reading the level
+// and states the previous one left in the workspace).
+//
+// Host record, always on: for each workspace the parameters it was last used
+// with and the last depth enqueued on it.  expand_depth(d > 1) needs d - 1,
+// prune needs L; otherwise DARTREE_ERR_ORDER before anything is enqueued.
+// The record follows the host calls: replays of a captured graph do not
+// update it.  At most kOrderSlots workspaces are remembered (least recently
+// used dropped; a dropped one must start again at depth 1).
+//
+// Device record: the selection kernel of depth d writes {key, d} into the
+// workspace header.  With DARTREE_DEBUG=1 in the environment (read once),
+// expand_depth(d > 1) and prune also synchronise the stream and compare that
+// record with the depth they need, and expand_depth checks after its launches
+// that the depth's normalisers are finite (DARTREE_ERR_NONFINITE).  Debug
+// checks are skipped while the stream is being captured.
+// ---------------------------------------------------------------------------
+uint64_t params_key(const dartree_params& p) {
+  uint64_t h = 1469598103934665603ull;   // FNV-1a over the struct's bytes
+  const unsigned char* b = reinterpret_cast<const unsigned char*>(&p);
+  for (size_t i = 0; i < sizeof(p); ++i) h = (h ^ b[i]) * 1099511628211ull;
+  return h | 1;   // never 0, so a zeroed header never matches
+}
+
+struct OrderSlot {
+  const void* ws;
+  uint64_t key;
+  int depth;
+  uint64_t used;
+};
+constexpr size_t kOrderSlots = 256;
+std::mutex g_order_mu;
+std::vector<OrderSlot> g_order;
+uint64_t g_order_tick = 0;
+
+int order_depth(const void* ws, uint64_t key) {
+  std::lock_guard<std::mutex> lk(g_order_mu);
+  for (OrderSlot& o : g_order)
+    if (o.ws == ws) return o.key == key ? (o.used = ++g_order_tick, o.depth) : -1;
+  return -1;
+}
+
+void order_set(const void* ws, uint64_t key, int depth) {
+  std::lock_guard<std::mutex> lk(g_order_mu);
+  for (OrderSlot& o : g_order)
+    if (o.ws == ws) {
+      o = OrderSlot{ws, key, depth, ++g_order_tick};
+      return;
+    }
+  if (g_order.size() >= kOrderSlots)
+    g_order.erase(std::min_element(g_order.begin(), g_order.end(),
+                                   [](const OrderSlot& a, const OrderSlot& b) { return a.used < b.used; }));
+  g_order.push_back(OrderSlot{ws, key, depth, ++g_order_tick});
+}
+
+bool debug_mode() {
+  static const bool on = [] {
+    const char* v = getenv("DARTREE_DEBUG");
+    return v && v[0] && strcmp(v, "0") != 0;
+  }();
+  return on;
+}
+
+bool capturing(hipStream_t st) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  return hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone;
+}
+
+// Debug: the depth the device record of `ws` holds for these parameters
+// (-1: none), after the stream's work so far.
+dartree_status device_depth(const void* ws, size_t hdr, uint64_t key, hipStream_t st, int* depth) {
+  uint32_t rec[3] = {0, 0, 0};
+  if (hipStreamSynchronize(st) != hipSuccess) return DARTREE_ERR_HIP;
+  if (hipMemcpy(rec, static_cast<const char*>(ws) + hdr, sizeof(rec), hipMemcpyDeviceToHost) != hipSuccess)
+    return DARTREE_ERR_HIP;
+  const bool same = rec[0] == uint32_t(key) && rec[1] == uint32_t(key >> 32);
+  *depth = same ? int(rec[2]) : -1;
+  return DARTREE_OK;
+}
+
 LevelShape level_shape(const dartree_params& p, const Shape& s) {
   LevelShape ls{};
   ls.depth = p.depth;
@@ -201,7 +288,7 @@ dartree_status expand_shared(const dartree_params& p, const dartree_inputs& in, 
   }
   tm.mark(tb + DARTREE_KERNEL_LSE, 1);
   tm.mark(tb + DARTREE_KERNEL_LOGITS, 0);
-  err = launch_shared_logits(p.precision, int(b), int(np), K, int(h), a, in.head_U,
+  err = launch_shared_logits(p.precision, int(b), int(np), K, int(h), int(V), a, in.head_U,
                              in.drafter_logits + size_t(d - 1) * V, L * V, csets + (d - 1) * K, L * K, nullptr, z, st);
   tm.mark(tb + DARTREE_KERNEL_LOGITS, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
@@ -237,6 +324,11 @@ dartree_status expand_shared(const dartree_params& p, const dartree_inputs& in, 
   la.U = in.head_U;
   la.e = float(sqrt(double(p.hidden)));
   la.r_out = r_out;
+  const uint64_t key = params_key(p);
+  la.stamp = at<uint32_t>(ws, l.hdr);
+  la.stamp_key_lo = uint32_t(key);
+  la.stamp_key_hi = uint32_t(key >> 32);
+  la.stamp_depth = d;
   tm.mark(tb + DARTREE_KERNEL_SELECT, 0);
   err = launch_select_level(la, st);
   tm.mark(tb + DARTREE_KERNEL_SELECT, 1);
@@ -343,6 +435,11 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   la.U = in.head_U;
   la.e = e;
   la.r_out = r_out;
+  const uint64_t key = params_key(p);
+  la.stamp = at<uint32_t>(ws, l.hdr);
+  la.stamp_key_lo = uint32_t(key);
+  la.stamp_key_hi = uint32_t(key >> 32);
+  la.stamp_depth = d;
   tm.mark(tb + DARTREE_KERNEL_SELECT, 0);
   err = launch_select_level(la, st);
   tm.mark(tb + DARTREE_KERNEL_SELECT, 1);
@@ -366,7 +463,7 @@ dartree_status validate_heap(const dartree_params* p) {
 //   slot_score: f32 [b][B+1]   cand_key: u64 [b][B+1]
 //   ch_lse: f32 [B][b]   ch_lp: f32 [B][b][k]   ch_tok: i32 [B][b][k]
 //   n_pop, gidx: i32 [b]
-//   r_store: act [B+1][b][h]   t_store: f32 [B][b][h]   a: act [b][h]
+//   r_store: act [B+1][b][h]   t_store: f32 [B][b][h]   a_store: act [B][b][h] (step i's features)
 //   z: f32 [b][V] (or [b][K])   k3: the row-split partials of b rows
 //   cset: i32 [b][L][K] and its scratch (K > 0)
 struct HeapLayout {
@@ -395,7 +492,7 @@ HeapLayout heap_layout_of(const dartree_params& p) {
   l.gidx = take(b * 4);
   l.r_store = take((B + 1) * b * h * ab);
   l.t_store = take(B * b * h * 4);
-  l.a = take(b * h * ab);
+  l.a = take(B * b * h * ab);
   l.z = take(b * (K > 0 ? K : V) * 4);
   l.k3 = take(K > 0 ? 0 : lse_topk_scratch_bytes(int64_t(b), V, int(k)));
   l.cset = take(b * L * K * 4);
@@ -463,6 +560,7 @@ dartree_status build_heap(const dartree_params& p, const dartree_inputs& in, voi
   }
   for (int64_t i = 0; i < B; ++i) {
     const int32_t* gi = i == 0 ? nullptr : gidx;
+    void* a_i = static_cast<char*>(a) + size_t(i) * b * h * ab;   // step i's features, kept for inspection
     ProjArgs head{};
     head.precision = p.precision;
     head.epilogue = EPI_HEAD;
@@ -476,11 +574,11 @@ dartree_status build_heap(const dartree_params& p, const dartree_inputs& in, voi
     head.bias_stride = i == 0 ? L * h : h;
     head.group_index = gi;
     head.out = at<float>(ws, l.t_store) + size_t(i) * b * h;
-    head.act_out = a;
+    head.act_out = a_i;
     if ((err = launch_project(head, st)) != hipSuccess) return DARTREE_ERR_HIP;
     if (K > 0) {
-      err = launch_shared_logits(p.precision, int(b), 1, K, int(h), a, in.head_U, in.drafter_logits,
-                                 i == 0 ? L * V : V, csets, i == 0 ? L * K : K, gi, z, st);
+      err = launch_shared_logits(p.precision, int(b), 1, K, int(h), int(V), a_i, in.head_U,
+                                 in.drafter_logits, i == 0 ? L * V : V, csets, i == 0 ? L * K : K, gi, z, st);
       if (err != hipSuccess) return DARTREE_ERR_HIP;
     } else {
       ProjArgs lg{};
@@ -490,7 +588,7 @@ dartree_status build_heap(const dartree_params& p, const dartree_inputs& in, voi
       lg.N = V;
       lg.K = h;
       lg.rows_per_group = 1;
-      lg.x = a;
+      lg.x = a_i;
       lg.w = in.head_U;
       lg.bias_f32 = in.drafter_logits;
       lg.bias_stride = i == 0 ? L * V : V;
@@ -520,6 +618,8 @@ const char* dartree_status_string(dartree_status status) {
     case DARTREE_ERR_UNSUPPORTED: return "unsupported: beyond this library's limits";
     case DARTREE_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case DARTREE_ERR_HIP: return "HIP kernel launch failed";
+    case DARTREE_ERR_ORDER: return "depths out of order: the workspace does not hold the levels this call reads";
+    case DARTREE_ERR_NONFINITE: return "non-finite normaliser (debug check)";
   }
   return "unknown status";
 }
@@ -542,7 +642,27 @@ dartree_status dartree_expand_depth(const dartree_params* p, const dartree_input
   if (d < 1 || d > p->depth) return DARTREE_ERR_INVALID_ARG;
   Layout l;
   if ((v = check_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
-  return expand(*p, *in, d, ws, l, shape_of(*p), stream);
+  const uint64_t key = params_key(*p);
+  if (d > 1 && order_depth(ws, key) != d - 1) return DARTREE_ERR_ORDER;
+  const bool dbg = debug_mode() && !capturing(stream);
+  if (dbg && d > 1) {
+    int dev_d = -1;
+    if ((v = device_depth(ws, l.hdr, key, stream, &dev_d)) != DARTREE_OK) return v;
+    if (dev_d != d - 1) return DARTREE_ERR_ORDER;
+  }
+  if ((v = expand(*p, *in, d, ws, l, shape_of(*p), stream)) != DARTREE_OK) return v;
+  order_set(ws, key, d);
+  if (dbg) {   // the depth's normalisers, one per parent row
+    const Shape s = shape_of(*p);
+    std::vector<float> lse(size_t(p->batch) * s.n[d - 1]);
+    if (hipStreamSynchronize(stream) != hipSuccess ||
+        hipMemcpy(lse.data(), at<char>(ws, l.lse + size_t(d - 1) * p->batch * p->width * 4), lse.size() * 4,
+                  hipMemcpyDeviceToHost) != hipSuccess)
+      return DARTREE_ERR_HIP;
+    for (float x : lse)
+      if (!isfinite(x)) return DARTREE_ERR_NONFINITE;
+  }
+  return DARTREE_OK;
 }
 
 dartree_status dartree_prune(const dartree_params* p, const void* ws, size_t ws_bytes, const dartree_tree* out,
@@ -552,6 +672,13 @@ dartree_status dartree_prune(const dartree_params* p, const void* ws, size_t ws_
   if ((v = check_tree(out)) != DARTREE_OK) return v;
   Layout l;
   if ((v = check_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
+  const uint64_t key = params_key(*p);
+  if (order_depth(ws, key) != p->depth) return DARTREE_ERR_ORDER;
+  if (debug_mode() && !capturing(stream)) {
+    int dev_d = -1;
+    if ((v = device_depth(ws, l.hdr, key, stream, &dev_d)) != DARTREE_OK) return v;
+    if (dev_d != p->depth) return DARTREE_ERR_ORDER;
+  }
   const Shape s = shape_of(*p);
   return hip_status(launch_prune_emit(p->batch, level_shape(*p, s), p->budget, at<int32_t>(ws, l.lvl_tok),
                                       at<int32_t>(ws, l.lvl_par), at<float>(ws, l.lvl_score), *out, stream));
@@ -569,8 +696,11 @@ dartree_status dartree_build_tree_timed(const dartree_params* p, const dartree_i
   Timer tm;
   tm.ev = events;
   tm.st = stream;
-  for (int d = 1; d <= p->depth; ++d)
+  const uint64_t key = params_key(*p);
+  for (int d = 1; d <= p->depth; ++d) {
     if ((v = expand(*p, *in, d, ws, l, s, stream, tm)) != DARTREE_OK) return v;
+    order_set(ws, key, d);
+  }
   const int ti = p->depth * DARTREE_KERNELS_PER_DEPTH;
   tm.mark(ti, 0);
   v = hip_status(launch_prune_emit(p->batch, level_shape(*p, s), p->budget, at<int32_t>(ws, l.lvl_tok),
@@ -591,6 +721,7 @@ dartree_status dartree_export_supertree(const dartree_params* p, const void* ws,
   if (!dst) return DARTREE_ERR_INVALID_ARG;
   Layout l;
   if ((v = check_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
+  if (order_depth(ws, params_key(*p)) < 1) return DARTREE_ERR_ORDER;
   const size_t L = p->depth, b = p->batch, W = p->width, k = p->branch;
   struct Item { void* to; size_t off; size_t bytes; } items[] = {
       {dst->tokens, l.lvl_tok, L * b * W * 4},   {dst->parents, l.lvl_par, L * b * W * 4},
@@ -611,10 +742,25 @@ dartree_status dartree_export_states(const dartree_params* p, const void* ws, si
   if (!dst || d < 1 || d >= p->depth) return DARTREE_ERR_INVALID_ARG;
   Layout l;
   if ((v = check_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
+  const int last = order_depth(ws, params_key(*p));
+  if (last != d && last != d + 1) return DARTREE_ERR_ORDER;
   const Shape s = shape_of(*p);
   const size_t bytes = size_t(p->batch) * s.n[d] * p->hidden * act_bytes(p->precision);
   const void* src = at<char>(ws, d % 2 ? l.state1 : l.state0);
   return hip_status(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, stream));
+}
+
+dartree_status dartree_export_features(const dartree_params* p, const void* ws, size_t ws_bytes, int32_t d, void* dst,
+                                       hipStream_t stream) {
+  dartree_status v = validate(p);
+  if (v != DARTREE_OK) return v;
+  if (!dst || d < 1 || d > p->depth || p->candidates < 0) return DARTREE_ERR_INVALID_ARG;
+  Layout l;
+  if ((v = check_ws(*p, ws, ws_bytes, &l)) != DARTREE_OK) return v;
+  if (order_depth(ws, params_key(*p)) != d) return DARTREE_ERR_ORDER;
+  const Shape s = shape_of(*p);
+  const size_t bytes = size_t(p->batch) * s.n[d - 1] * p->hidden * act_bytes(p->precision);
+  return hip_status(hipMemcpyAsync(dst, at<char>(ws, l.a), bytes, hipMemcpyDeviceToDevice, stream));
 }
 
 dartree_status dartree_project_workspace_size(int32_t precision, int32_t rows, int32_t vocab, int32_t hidden,
@@ -857,6 +1003,7 @@ dartree_status dartree_export_heap(const dartree_params* p, const void* ws, size
       {dst->num_popped, l.n_pop, b * 4},     {dst->lse, l.ch_lse, B * b * 4},
       {dst->cand_logp, l.ch_lp, B * b * k * 4}, {dst->cand_ids, l.ch_tok, B * b * k * 4},
       {dst->states, l.r_store, (B + 1) * b * h * act_bytes(p->precision)},
+      {dst->features, l.a, B * b * h * act_bytes(p->precision)},
       {p->candidates > 0 ? dst->csets : nullptr, l.cset, b * L * size_t(p->candidates) * 4},
   };
   for (const Item& it : items)

@@ -67,7 +67,7 @@ __global__ __launch_bounds__(kHeapThreads) void heap_step(HeapArgs a) {
       for (int c = lane; c < K; c += 64) {
         const float v = zr[c];
         rz[c] = v;
-        rid[c] = set[c];
+        rid[c] = min(max(set[c], 0), a.vocab - 1);   // workspace ids, clamped into U
         m = fmaxf(m, v);
       }
       m = wave_max(m);

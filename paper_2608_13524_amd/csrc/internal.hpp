@@ -103,6 +103,9 @@ struct LevelArgs {
   const void* U;                  // act [V][hidden]
   float e;
   void* r_out;                    // act [batch * n_keep][hidden]
+  uint32_t* stamp;                // optional: block 0 writes {key_lo, key_hi, depth} (the order check)
+  uint32_t stamp_key_lo, stamp_key_hi;
+  int stamp_depth;
 };
 hipError_t launch_select_level(const LevelArgs& a, hipStream_t s);
 
@@ -116,9 +119,10 @@ hipError_t launch_candidate_sets(const float* logits, int64_t rows, int64_t voca
 // Corrected logits over the shared set: z[q*np + j][c] = lb[g*lb_stride + C[c]]
 // + U[C[c]] . a[q*np + j], with C = cset + g * cset_stride and g =
 // group_index[q] (device memory) if group_index is set, else q.
-hipError_t launch_shared_logits(int precision, int batch, int np, int K, int hidden, const void* a, const void* U,
-                                const float* lb, int64_t lb_stride, const int32_t* cset, int64_t cset_stride,
-                                const int32_t* group_index, float* z, hipStream_t s);
+// Set ids are clamped into [0, vocab).
+hipError_t launch_shared_logits(int precision, int batch, int np, int K, int hidden, int vocab, const void* a,
+                                const void* U, const float* lb, int64_t lb_stride, const int32_t* cset,
+                                int64_t cset_stride, const int32_t* group_index, float* z, hipStream_t s);
 
 // Deferred top-B prune and tree emission (K6).
 struct LevelShape {

@@ -203,7 +203,7 @@ constexpr int kRowTiles = 4;  // node-row tiles of 16 per block
 // grid: batch * ncb * nrb; block (q, cb, rb): candidates 16 cb .. 16 cb + 15,
 // node rows 64 rb .. 64 rb + 63 of request q.  Rows past K or n_parent are
 // clamped (computed, never stored).
-__global__ __launch_bounds__(1024) void shared_logits_bf16(int np, int K, int hidden, int ncb, int nrb,
+__global__ __launch_bounds__(1024) void shared_logits_bf16(int np, int K, int hidden, int vocab, int ncb, int nrb,
                                                           const uint16_t* __restrict__ a,
                                                           const uint16_t* __restrict__ U,
                                                           const float* __restrict__ lb, int64_t lb_stride,
@@ -219,7 +219,10 @@ __global__ __launch_bounds__(1024) void shared_logits_bf16(int np, int K, int hi
   const int64_t g = group_index ? group_index[q] : q;   // L^base / C_d row of request q
   const int32_t* set = cset + g * cset_stride;
   const int c = min(16 * cb + r16, K - 1);
-  const uint16_t* urow = U + int64_t(set[c]) * hidden + kg * 8;
+  // set ids come from the workspace: clamped into the vocabulary, so a set
+  // that was never built (depths enqueued out of order) cannot index past U
+  auto id_at = [&](int i) { return min(max(set[i], 0), vocab - 1); };
+  const uint16_t* urow = U + int64_t(id_at(c)) * hidden + kg * 8;
   const uint16_t* arow[kRowTiles];
 #pragma unroll
   for (int t = 0; t < kRowTiles; ++t) {
@@ -234,7 +237,7 @@ __global__ __launch_bounds__(1024) void shared_logits_bf16(int np, int K, int hi
   if (wave == 0) {
     const float* lbq = lb + g * lb_stride;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) lbv[i] = lbq[set[min(16 * cb + 4 * kg + i, K - 1)]];
+    for (int i = 0; i < 4; ++i) lbv[i] = lbq[id_at(min(16 * cb + 4 * kg + i, K - 1))];
   }
   f32x4 acc[kRowTiles];
 #pragma unroll
@@ -271,7 +274,8 @@ __global__ __launch_bounds__(1024) void shared_logits_bf16(int np, int K, int hi
 }
 
 // fp32: grid batch * ceil(np K / 256); thread (q, j, c) computes one dot product.
-__global__ __launch_bounds__(256) void shared_logits_f32(int np, int K, int hidden, int nblk, const float* __restrict__ a,
+__global__ __launch_bounds__(256) void shared_logits_f32(int np, int K, int hidden, int vocab, int nblk,
+                                                         const float* __restrict__ a,
                                                          const float* __restrict__ U, const float* __restrict__ lb,
                                                          int64_t lb_stride, const int32_t* __restrict__ cset,
                                                          int64_t cset_stride, const int32_t* __restrict__ group_index,
@@ -281,7 +285,7 @@ __global__ __launch_bounds__(256) void shared_logits_f32(int np, int K, int hidd
   if (e >= np * K) return;
   const int j = e / K, cc = e % K;
   const int64_t g = group_index ? group_index[q] : q;
-  const int tok = cset[g * cset_stride + cc];
+  const int tok = min(max(cset[g * cset_stride + cc], 0), vocab - 1);   // clamped as above
   const float* ar = a + (int64_t(q) * np + j) * hidden;
   const float* ur = U + int64_t(tok) * hidden;
   float acc = 0.f;
@@ -310,18 +314,18 @@ hipError_t launch_candidate_sets(const float* logits, int64_t rows, int64_t voca
   return hipGetLastError();
 }
 
-hipError_t launch_shared_logits(int precision, int batch, int np, int K, int hidden, const void* a, const void* U,
-                                const float* lb, int64_t lb_stride, const int32_t* cset, int64_t cset_stride,
-                                const int32_t* group_index, float* z, hipStream_t s) {
+hipError_t launch_shared_logits(int precision, int batch, int np, int K, int hidden, int vocab, const void* a,
+                                const void* U, const float* lb, int64_t lb_stride, const int32_t* cset,
+                                int64_t cset_stride, const int32_t* group_index, float* z, hipStream_t s) {
   if (batch <= 0) return hipSuccess;
   if (precision == DARTREE_BF16) {
     const int ncb = (K + 15) / 16, nrb = (np + 16 * kRowTiles - 1) / (16 * kRowTiles);
-    hipLaunchKernelGGL(shared_logits_bf16, dim3(unsigned(batch * ncb * nrb)), dim3(1024), 0, s, np, K, hidden, ncb, nrb,
-                       static_cast<const uint16_t*>(a), static_cast<const uint16_t*>(U), lb, lb_stride, cset,
+    hipLaunchKernelGGL(shared_logits_bf16, dim3(unsigned(batch * ncb * nrb)), dim3(1024), 0, s, np, K, hidden, vocab,
+                       ncb, nrb, static_cast<const uint16_t*>(a), static_cast<const uint16_t*>(U), lb, lb_stride, cset,
                        cset_stride, group_index, z);
   } else {
     const int nblk = (np * K + 255) / 256;
-    hipLaunchKernelGGL(shared_logits_f32, dim3(unsigned(batch * nblk)), dim3(256), 0, s, np, K, hidden, nblk,
+    hipLaunchKernelGGL(shared_logits_f32, dim3(unsigned(batch * nblk)), dim3(256), 0, s, np, K, hidden, vocab, nblk,
                        static_cast<const float*>(a), static_cast<const float*>(U), lb, lb_stride, cset, cset_stride,
                        group_index, z);
   }

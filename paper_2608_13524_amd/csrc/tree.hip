@@ -52,6 +52,11 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
   const int np = a.n_parent, k = a.k;
   int n = np * k;
   const int64_t rbase = int64_t(q) * np;
+  if (a.stamp && blockIdx.x == 0 && threadIdx.x == 0) {   // the workspace's depth record
+    a.stamp[0] = a.stamp_key_lo;
+    a.stamp[1] = a.stamp_key_hi;
+    a.stamp[2] = uint32_t(a.stamp_depth);
+  }
   for (int j = threadIdx.x; j < np; j += blockDim.x)
     ps[j] = a.parent_score ? a.parent_score[int64_t(q) * a.parent_stride + j] : 0.f;
   if (a.shared_k > 0) {
@@ -71,7 +76,7 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
       for (int c = lane; c < nk; c += 64) {
         const float v = zr[c];
         rz[wave][c] = v;
-        rid[wave][c] = set[c];
+        rid[wave][c] = min(max(set[c], 0), a.vocab - 1);   // workspace ids, clamped into U
         m = fmaxf(m, v);
       }
       m = wave_max(m);
@@ -165,7 +170,8 @@ __global__ __launch_bounds__(select_threads<K>()) void select_level(LevelArgs a,
     const int j = c / kk;
     const int r = c - j * kk;
     const float sc = score_at(j, r);
-    return (uint64_t(score_desc_key(sc)) << 32) | (uint32_t(j) << 20) | uint32_t(c_ids[j * k + r]);
+    // ids < 2^20; the mask keeps a malformed id out of the parent-slot field
+    return (uint64_t(score_desc_key(sc)) << 32) | (uint32_t(j) << 20) | (uint32_t(c_ids[j * k + r]) & 0xFFFFFu);
   };
   const uint64_t* kept = keys;   // the n_keep best, in order
   if (n <= int(blockDim.x)) {

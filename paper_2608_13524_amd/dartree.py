@@ -19,9 +19,9 @@ BF16 = 1
 HEAD_RNN = 0
 HEAD_MARKOV = 1
 
-OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_ORDER, ERR_NONFINITE = range(7)
 
-ABI_VERSION = 7   # DARTREE_ABI_VERSION of include/dartree.h this binding follows
+ABI_VERSION = 8   # DARTREE_ABI_VERSION of include/dartree.h this binding follows
 
 MAX_VOCAB = 1 << 20
 MAX_DEPTH = 64
@@ -34,7 +34,8 @@ MAX_HEAP_BUDGET = 1024
 SYMBOLS = [
     "dartree_abi_version", "dartree_status_string", "dartree_validate",
     "dartree_workspace_size", "dartree_expand_depth", "dartree_prune",
-    "dartree_build_tree", "dartree_build_tree_timed", "dartree_export_supertree", "dartree_export_states", "dartree_project",
+    "dartree_build_tree", "dartree_build_tree_timed", "dartree_export_supertree", "dartree_export_states",
+    "dartree_export_features", "dartree_project",
     "dartree_project_workspace_size",
     "dartree_lse_topk_workspace_size", "dartree_lse_topk", "dartree_select_topw",
     "dartree_prune_levels", "dartree_candidate_sets_workspace_size", "dartree_candidate_sets",
@@ -87,7 +88,7 @@ class HeapTraceC(ctypes.Structure):
     _fields_ = [("tokens", ctypes.c_void_p), ("parents", ctypes.c_void_p), ("depths", ctypes.c_void_p),
                 ("scores", ctypes.c_void_p), ("num_popped", ctypes.c_void_p), ("lse", ctypes.c_void_p),
                 ("cand_logp", ctypes.c_void_p), ("cand_ids", ctypes.c_void_p), ("states", ctypes.c_void_p),
-                ("csets", ctypes.c_void_p)]
+                ("csets", ctypes.c_void_p), ("features", ctypes.c_void_p)]
 
 
 class AttnParams(ctypes.Structure):
@@ -130,6 +131,7 @@ def lib() -> ctypes.CDLL:
                                            ctypes.POINTER(vp), vp]
     L.dartree_export_supertree.argtypes = [P, vp, sz, ctypes.POINTER(SupertreeC), vp]
     L.dartree_export_states.argtypes = [P, vp, sz, i32, vp, vp]
+    L.dartree_export_features.argtypes = [P, vp, sz, i32, vp, vp]
     L.dartree_project.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, i64, vp, vp, sz, vp]
     L.dartree_project_workspace_size.argtypes = [i32, i32, i32, i32, ctypes.POINTER(sz)]
     L.dartree_lse_topk_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(sz)]
@@ -310,12 +312,14 @@ class DeviceHeapTrace:
     cand_ids: object
     states: object = None   # act [B+1][b][h] (int16 bit patterns in bf16 mode)
     csets: object = None    # [b][L][K] (candidates > 0)
+    features: object = None  # act [B][b][h]
 
     def c(self) -> HeapTraceC:
         return HeapTraceC(*(_ptr(getattr(self, f.name)) for f in dataclasses.fields(self)))
 
     @staticmethod
     def alloc(p: Params, states: bool = True, device="cuda") -> "DeviceHeapTrace":
+        """``states``: also the per-slot states and per-step features."""
         import torch
         b, B, k, h, L, K = p.batch, p.budget, p.branch, p.hidden, p.depth, p.candidates
         i32 = dict(dtype=torch.int32, device=device)
@@ -325,7 +329,8 @@ class DeviceHeapTrace:
                                torch.empty(b, B + 1, **i32), torch.empty(b, B + 1, **f32), torch.empty(b, **i32),
                                torch.empty(B, b, **f32), torch.empty(B, b, k, **f32), torch.empty(B, b, k, **i32),
                                torch.empty(B + 1, b, h, dtype=act, device=device) if states else None,
-                               torch.empty(b, L, K, **i32) if K > 0 else None)
+                               torch.empty(b, L, K, **i32) if K > 0 else None,
+                               torch.empty(B, b, h, dtype=act, device=device) if states else None)
 
     def host(self) -> dict:
         return {f.name: getattr(self, f.name).cpu().numpy() for f in dataclasses.fields(self)
@@ -370,7 +375,7 @@ KERNEL_NAMES = ["head", "logits", "lse_topk", "select"]   # per depth, launch or
 
 
 def build_tree_timed(p: Params, inputs: DeviceInputs, ws, out: DeviceTree, events, stream=None) -> None:
-    """build_tree recording ``events`` (2 * (5 L + 1) raw hipEvent_t handles or
+    """build_tree recording ``events`` (2 * (4 L + 1) raw hipEvent_t handles or
     None) around each launch; see dartree_build_tree_timed."""
     ic, tc = inputs.c(), out.c()
     n = 2 * (len(KERNEL_NAMES) * p.depth + 1)
@@ -402,6 +407,13 @@ def export_states(p: Params, ws, d: int, dst, stream=None) -> None:
     """States of S_d into dst (act [b * n_d][h]); see the header for validity."""
     _check(lib().dartree_export_states(ctypes.byref(p), _ptr(ws), ws.numel(), d, _ptr(dst), _stream(stream)),
            "dartree_export_states")
+
+
+def export_features(p: Params, ws, d: int, dst, stream=None) -> None:
+    """Features of depth d's parent rows into dst (act [b * n_{d-1}][h]),
+    right after expand_depth(d)."""
+    _check(lib().dartree_export_features(ctypes.byref(p), _ptr(ws), ws.numel(), d, _ptr(dst), _stream(stream)),
+           "dartree_export_features")
 
 
 def project_workspace_size(precision: int, rows: int, vocab: int, hidden: int) -> int:

@@ -47,8 +47,9 @@ def to_dev(a: np.ndarray):
 
 
 def run_stepwise(cfg, inputs):
-    """expand_depth(1..L) with the states of every depth exported, then prune.
-    Returns (tree dict, supertree dict, {d: host states of S_d})."""
+    """expand_depth(1..L) with the features and states of every depth
+    exported, then prune.  Returns (tree dict, supertree dict, {d: host
+    states of S_d}, {d: host features of depth d's parent rows})."""
     dev = device()
     p = D.Params.of(cfg)
     di = D.DeviceInputs.from_host(inputs, dev)
@@ -56,10 +57,13 @@ def run_stepwise(cfg, inputs):
     out = D.DeviceTree.alloc(cfg.batch, cfg.budget, dev)
     sizes = p.level_sizes()
     act = torch.int16 if cfg.precision == D.BF16 else torch.float32
-    states = {}
+    states, feats = {}, {}
     say(f"stepwise {cfg.name} b={cfg.batch} V={cfg.vocab} h={cfg.hidden} L={cfg.depth} W={cfg.width}")
     for d in range(1, cfg.depth + 1):
         D.expand_depth(p, di, d, ws)
+        fb = torch.empty(cfg.batch * (sizes[d - 2] if d > 1 else 1), cfg.hidden, dtype=act, device=dev)
+        D.export_features(p, ws, d, fb)
+        feats[d] = fb.cpu().numpy()
         if d < cfg.depth:
             buf = torch.empty(cfg.batch * sizes[d - 1], cfg.hidden, dtype=act, device=dev)
             D.export_states(p, ws, d, buf)
@@ -68,4 +72,10 @@ def run_stepwise(cfg, inputs):
     st = D.DeviceSupertree.alloc(p, dev)
     D.export_supertree(p, ws, st)
     torch.cuda.synchronize()
-    return out.host(), st.host(), states
+    return out.host(), st.host(), states, feats
+
+
+def decoded(exports: dict, precision: int) -> dict:
+    """Decode exported state or feature buffers ({d: bits}) to fp64."""
+    from tests import replay
+    return {d: replay.decode_states(v, precision) for d, v in exports.items()}

@@ -8,6 +8,7 @@ looks the oracle up through the module object at call time.
 """
 from __future__ import annotations
 
+import dataclasses
 import math
 
 import numpy as np
@@ -127,6 +128,18 @@ def pin_head_scalar():
             for v in (0, 4):
                 rc = R.child_states(t[0][None, :], dec.U[v][None, :], R.Params.of(cfg).embed_scale, prec)
                 assert np.allclose(rc[0], head.child(ts, v), atol=1e-9)
+            # values before rounding (what a follower checks rounding near-ties against)
+            tp, a_pre = R.head_preimage(np.array([r]), dec.A, dec.H[0, d - 1])
+            assert np.allclose(tp[0], ts, atol=1e-12)
+            assert np.allclose(a_pre[0], [math.tanh(ts[i] + head.H[0][d - 1][i]) for i in range(cfg.hidden)],
+                               atol=1e-12)
+            for hd in (R.RNN, R.MARKOV):
+                pp = dataclasses.replace(R.Params.of(cfg), head=hd)
+                pre = R.state_preimage(pp, t[0][None, :], dec.U[4][None, :])[0]
+                e = pp.embed_scale
+                want = [e * head.U[4][i] if hd == R.MARKOV else math.tanh(ts[i] + e * head.U[4][i])
+                        for i in range(cfg.hidden)]
+                assert np.allclose(pre, want, atol=1e-12)
 
 
 # ---------------------------------------------------------------------------

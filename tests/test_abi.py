@@ -22,7 +22,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     syms = declared_symbols()
-    assert len(syms) == 27, syms
+    assert len(syms) == 28, syms
     lib = D.lib()
     for s in syms:
         assert hasattr(lib, s), s
@@ -30,8 +30,8 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert D.abi_version() == D.ABI_VERSION == 7
-    for s in range(5):
+    assert D.abi_version() == D.ABI_VERSION == 8
+    for s in range(7):
         assert D.status_string(s)
     assert D.status_string(99) == "unknown status"
 
@@ -261,3 +261,26 @@ def test_consumer_rejects_bad_arguments():
     assert call(F, n, q=None) == D.ERR_INVALID_ARG
     assert call(F, n, kc=None) == D.ERR_INVALID_ARG                 # context expected
     assert call(F, n, q=ctypes.c_void_p(FAKE + 2)) == D.ERR_INVALID_ARG
+
+
+def test_depth_order_checked_before_any_launch():
+    """Algorithm 1's depths run 1..L: a call that would read levels no earlier
+    call produced returns DARTREE_ERR_ORDER with nothing enqueued (on a
+    workspace address the library has never seen)."""
+    lib = D.lib()
+    p = _p()
+    need = D.workspace_size(p)
+    byref = ctypes.byref
+    fresh = 0x7A000000   # never used as a workspace in this process
+    assert D.status_string(D.ERR_ORDER) and D.status_string(D.ERR_NONFINITE)
+    for d in (2, 5, 16):
+        assert lib.dartree_expand_depth(byref(p), byref(_inputs()), d, fresh, need, None) == D.ERR_ORDER
+    assert lib.dartree_prune(byref(p), fresh, need, byref(_tree()), None) == D.ERR_ORDER
+    assert lib.dartree_export_states(byref(p), fresh, need, 3, FAKE, None) == D.ERR_ORDER
+    assert lib.dartree_export_features(byref(p), fresh, need, 1, FAKE, None) == D.ERR_ORDER
+    assert lib.dartree_export_supertree(byref(p), fresh, need, byref(D.SupertreeC()), None) == D.ERR_ORDER
+    # argument errors still come first
+    assert lib.dartree_export_features(byref(p), fresh, need, 0, FAKE, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_export_features(byref(p), fresh, need, 17, FAKE, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_export_features(byref(p), fresh, need - 1, 1, FAKE, None) == D.ERR_WORKSPACE
+    assert lib.dartree_expand_depth(byref(p), byref(_inputs()), 2, fresh, need - 1, None) == D.ERR_WORKSPACE

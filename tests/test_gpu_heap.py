@@ -70,8 +70,10 @@ def test_heap_small_parity(name):
     dec = R.prepare(inputs)
     reqs = list(range(cfg.batch))
     gs = replay.decode_states(trace["states"], cfg.precision)
-    rep = replay.follow_heap(dec, trace, tree, reqs, reqs, gpu_states=gs)
+    gf = replay.decode_states(trace["features"], cfg.precision)
+    rep = replay.follow_heap(dec, trace, tree, reqs, reqs, gpu_states=gs, gpu_features=gf)
     _log_report(name, "heap-follow-states", rep)
+    assert rep.max_lse_ratio <= 1 and rep.max_logp_ratio <= 1
     free = replay.follow_heap(dec, trace, tree, reqs, reqs)
     _log_report(name, "heap-free-running", free)
     if free.events == 0:   # then the GPU equals the free-running oracle outright
@@ -104,19 +106,15 @@ def test_heap_zeroed_correction_is_ddtree():
             assert abs(s - tree["scores"][q, o]) < 1e-4
 
 
-# Full-size workloads: requests the oracle re-derives, and the budget (the
-# first B pops of a round do not depend on a larger budget).
-FULL = {"tiny": ([0], None), "qwen3-4b": ([0], None), "qwen3-4b-shared": ([0], None),
-        "qwen3-8b-x4": ([1], 64), "qwen3-8b-shared-x4": ([0, 3], None), "stress-x16": ([5], 32),
-        "qwen3-4b-markov": ([0], None)}
+# Full-size workloads at their own budgets: the requests the oracle re-derives.
+FULL = {"tiny": [0], "qwen3-4b": [0], "qwen3-4b-wide": [0], "qwen3-4b-shared": [0], "qwen3-8b-x4": [1],
+        "qwen3-8b-shared-x4": [0, 3], "stress-x16": [5], "qwen3-4b-markov": [0]}
 
 
 @pytest.mark.parametrize("name", list(FULL))
 def test_heap_full_size_parity(name):
-    reqs, budget = FULL[name]
+    reqs = FULL[name]
     cfg = W.CONFIGS[name]
-    if budget is not None:
-        cfg = cfg.replace(budget=budget)
     weights = W.make_weights(cfg)
     inputs = W.make_inputs(cfg, weights=weights)
     tree, trace = run_heap(cfg, inputs)
@@ -128,15 +126,21 @@ def test_heap_full_size_parity(name):
         assert (np.diff(s) <= 1e-6).all()           # pops in non-increasing score order
     sub = W.make_inputs(cfg, requests=reqs, weights=weights)
     states = trace["states"][:, reqs]
-    trace = {k: (v[:, reqs] if k in ("lse", "cand_logp", "cand_ids") else v[reqs] if k != "states" else None)
-             for k, v in trace.items()}
+    feats = trace["features"][:, reqs]
+    trace = {k: (v[:, reqs] if k in ("lse", "cand_logp", "cand_ids") else v[reqs])
+             for k, v in trace.items() if k not in ("states", "features")}
     tree = {k: v[reqs] for k, v in tree.items()}
     del inputs
     dec = R.prepare(sub)
     idx = list(range(len(reqs)))
-    rep = replay.follow_heap(dec, trace, tree, idx, idx, gpu_states=replay.decode_states(states, cfg.precision))
+    # every differing state or feature element must be a proven rounding near-tie
+    # (replay.check_rounded), and every normaliser and log-probability within its
+    # fp32 bound; the comparator raises otherwise
+    rep = replay.follow_heap(dec, trace, tree, idx, idx, gpu_states=replay.decode_states(states, cfg.precision),
+                             gpu_features=replay.decode_states(feats, cfg.precision))
     _log_report(name, "heap-follow-states", rep)
-    assert rep.state_mismatch <= 0.01 * max(rep.state_elems, 1)
+    assert rep.max_lse_ratio <= 1 and rep.max_logp_ratio <= 1 and rep.max_tie_ratio <= 1
+    assert rep.max_score_err < replay.SCORE_TOL
 
 
 def test_heap_graph_replay_matches_eager():

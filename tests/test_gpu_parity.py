@@ -17,7 +17,7 @@ import oracle.dartree_ref as R
 from paper_2608_13524_amd import dartree as D
 from paper_2608_13524_amd import workloads as W
 from tests import replay
-from tests.gpu_util import device, run_build, run_stepwise, say
+from tests.gpu_util import decoded, device, run_build, run_stepwise, say
 
 pytestmark = pytest.mark.gpu
 
@@ -90,13 +90,25 @@ SMALL = {
 
 @pytest.mark.parametrize("name", list(SMALL))
 def test_small_parity(name):
+    """Strict (the GPU's features and states followed, each differing element
+    a proven rounding near-tie, normalisers and log-probabilities within their
+    fp32 bounds), then free-running; the launch sequence build_tree runs gives
+    the same tree as the depth-by-depth one."""
     cfg = SMALL[name]
     inputs = W.make_inputs(cfg)
-    tree, sup, _ = run_build(cfg, inputs)
+    tree, sup, states, feats = run_stepwise(cfg, inputs)
+    t2, _, _ = run_build(cfg, inputs, export=False)
+    for k in tree:
+        assert np.array_equal(tree[k], t2[k]), k
     dec = R.prepare(inputs)
-    rep = replay.follow(dec, sup, tree, batch_index=list(range(cfg.batch)), requests=list(range(cfg.batch)))
-    print(name, rep)
-    if rep.events == 0:  # then the GPU equals the free-running oracle outright
+    reqs = list(range(cfg.batch))
+    rep = replay.follow(dec, sup, tree, reqs, reqs, gpu_states=decoded(states, cfg.precision),
+                        gpu_features=decoded(feats, cfg.precision))
+    _log_report(name, "follow-states", rep)
+    assert rep.max_lse_ratio <= 1 and rep.max_logp_ratio <= 1 and rep.max_tie_ratio <= 1
+    free = replay.follow(dec, sup, tree, reqs, reqs)
+    _log_report(name, "free-running", free)
+    if free.events == 0:  # then the GPU equals the free-running oracle outright
         want, _ = R.build_tree(dec)
         assert np.array_equal(tree["tokens"], want.tokens) and np.array_equal(tree["mask"], want.mask)
 
@@ -160,6 +172,15 @@ FULL_SAMPLE = {"tiny": [0], "qwen3-4b": [0], "qwen3-4b-wide": [0], "qwen3-8b-x4"
                "stress-x16": [0, 15], "qwen3-4b-shared": [0], "qwen3-8b-shared-x4": [0, 3],
                "qwen3-4b-markov": [0]}
 
+# Free-running leg (nothing followed): the largest number of selections allowed
+# to differ from the oracle's own inside the drift window.  Three times the
+# counts measured on MI355X, plus three (measured: 0, 1, 1, 10, 26, 0, 1, 0).
+# bf16 states drift apart by about one rounding step per element over the
+# depths, so near-ties at the drift scale differ; the Markov head's states are
+# token embeddings and do not drift.
+FREE_RUNNING_MAX_EVENTS = {"tiny": 3, "qwen3-4b": 6, "qwen3-4b-wide": 6, "qwen3-8b-x4": 33, "stress-x16": 81,
+                           "qwen3-4b-shared": 3, "qwen3-8b-shared-x4": 6, "qwen3-4b-markov": 3}
+
 
 def _log_report(name, mode, rep):
     path = os.environ.get("PARITY_REPORT")
@@ -172,14 +193,17 @@ def _log_report(name, mode, rep):
 
 @pytest.mark.parametrize("name", W.CONFIG_ORDER)
 def test_full_size_parity(name):
-    """Strict check (every depth recomputed from the GPU's parent states,
-    near-tie window 1e-3, states within one bf16 rounding step), then the
-    free-running oracle over the whole round with the score tolerance as the
-    window."""
+    """Strict check: every depth recomputed in fp64 from the GPU's parent
+    states and features, each differing state or feature element a proven
+    bf16 rounding near-tie, selections within the 1e-3 near-tie window,
+    normalisers and log-probabilities within their fp32 bounds, emitted arrays
+    bit-exact and scores within 2e-2.  Then the free-running oracle over the
+    whole round inside the stated drift window, with a stated cap on the
+    selections that may differ."""
     cfg = W.CONFIGS[name]
     weights = W.make_weights(cfg)
     inputs = W.make_inputs(cfg, weights=weights)
-    tree, sup, states = run_stepwise(cfg, inputs)
+    tree, sup, states, feats = run_stepwise(cfg, inputs)
     t2, s2, _ = run_build(cfg, inputs)          # the launch sequence the benchmark times
     for k in tree:
         assert np.array_equal(tree[k], t2[k]), k
@@ -192,17 +216,19 @@ def test_full_size_parity(name):
     sub = W.make_inputs(cfg, requests=reqs, weights=weights)
     del inputs
     dec = R.prepare(sub)
-    gs = {d: replay.decode_states(v, cfg.precision) for d, v in states.items()}
-    rep = replay.follow(dec, sup, tree, batch_index=reqs, requests=reqs, gpu_states=gs)
+    rep = replay.follow(dec, sup, tree, batch_index=reqs, requests=reqs, gpu_states=decoded(states, cfg.precision),
+                        gpu_features=decoded(feats, cfg.precision))
     _log_report(name, "follow-states", rep)
     assert rep.max_score_err < replay.SCORE_TOL
-    assert rep.state_mismatch <= 0.01 * max(rep.state_elems, 1)
+    assert rep.max_lse_ratio <= 1 and rep.max_logp_ratio <= 1 and rep.max_tie_ratio <= 1
+    assert rep.max_fp32_ratio <= 1
     # whole round against the free-running oracle: bf16 states drift by up to
     # one rounding step per element, so the window scales with that drift
-    tol = replay.free_running_tol(dec.p) * float(np.std(dec.U[:4096]))
-    tol = max(tol, replay.EPS)
-    free = replay.follow(dec, sup, tree, batch_index=reqs, requests=reqs, eps=tol, score_tol=max(tol, replay.SCORE_TOL))
+    tol = max(replay.free_running_tol(dec.p) * float(np.std(dec.U[:4096])), replay.EPS)
+    free = replay.follow(dec, sup, tree, batch_index=reqs, requests=reqs, eps=tol, score_tol=tol)
     _log_report(name, f"free-running(window {tol:.3g})", free)
+    assert free.events <= FREE_RUNNING_MAX_EVENTS[name], free
+    assert free.max_score_err <= tol
 
 
 def test_graph_replay_matches_eager():
@@ -234,3 +260,86 @@ def test_graph_replay_matches_eager():
         got = out.host()
         for k in want:
             assert np.array_equal(got[k], want[k]), (rep, k)
+
+
+# ---------------------------------------------------------------------------
+# Special cases at the Qwen3-4B shape (V = 151936, h = 2560, L = 16)
+# ---------------------------------------------------------------------------
+
+def _paths(tree, q):
+    out = []
+    for o in range(int(tree["num_nodes"][q])):
+        path, j = [], o
+        while j >= 0:
+            path.append(int(tree["tokens"][q, j]))
+            j = int(tree["parents"][q, j])
+        out.append(path[::-1])
+    return out
+
+
+def test_full_shape_zeroed_correction():
+    """U = 0 (Sec. 2.3): the correction vanishes, every node of depth d sees
+    the drafter's marginal softmax(L_d^base), and every emitted score is the
+    sum of marginal log-probabilities along the path plus beta d; the tree
+    equals the oracle's (no state can drift: z = L^base exactly)."""
+    cfg = W.CONFIGS["qwen3-4b"]
+    A, U = W.make_weights(cfg)
+    inputs = W.make_inputs(cfg, weights=(A, np.zeros_like(U)))
+    tree, sup, _ = run_build(cfg, inputs)
+    dec = R.prepare(inputs)
+    rep = replay.follow(dec, sup, tree, [0], [0])   # bit-exact against the oracle along the GPU's choices
+    _log_report("qwen3-4b-U0", "free-running", rep)
+    if rep.events == 0:
+        want, _ = R.build_tree(dec)
+        for name in ("tokens", "parents", "depths", "mask", "num_nodes"):
+            assert np.array_equal(tree[name], getattr(want, name)), name
+    marg = R.log_softmax(inputs.Lb[0].astype(np.float64), 1.0)   # [L][V]
+    for o, path in enumerate(_paths(tree, 0)):
+        s = sum(marg[i, v] + cfg.depth_bonus for i, v in enumerate(path))
+        assert abs(s - tree["scores"][0, o]) < 1e-4, (o, s, tree["scores"][0, o])
+
+
+def test_full_shape_chain_w1():
+    """W = 1: the corrected single chain (one node per depth, each the best
+    child of the previous), strict parity with the oracle's chain."""
+    cfg = W.CONFIGS["qwen3-4b"].replace(width=1)
+    inputs = W.make_inputs(cfg)
+    tree, sup, states, feats = run_stepwise(cfg, inputs)
+    dec = R.prepare(inputs)
+    rep = replay.follow(dec, sup, tree, [0], [0], gpu_states=decoded(states, cfg.precision),
+                        gpu_features=decoded(feats, cfg.precision))
+    _log_report("qwen3-4b-W1", "follow-states", rep)
+    n = int(tree["num_nodes"][0])
+    assert n == cfg.depth
+    assert np.array_equal(tree["parents"][0, :n], np.arange(-1, n - 1))
+    assert np.array_equal(tree["depths"][0, :n], np.arange(1, n + 1))
+    # each kept token is its parent row's best child (the GPU's own top-1)
+    for d in range(1, n + 1):
+        assert tree["tokens"][0, d - 1] == sup["cand_ids"][d - 1, 0, 0]
+
+
+def test_full_shape_batch_invariance():
+    """A request's tree at V = 151936 alone and inside a batch.  At the 4B
+    shape a batch of two leaves every kernel's blocking and the softmax
+    pass's row segmentation unchanged, so the trees are bit-identical.  At the
+    8B shape (four requests) depths 2..16 have 64 parent rows instead of 16,
+    which splits each row's normaliser into fewer segments and changes the
+    product's blocking: tokens, parents and mask agree, scores within
+    rounding."""
+    cfg = W.CONFIGS["qwen3-4b"].replace(batch=2)
+    weights = W.make_weights(cfg)
+    both, _, _ = run_build(cfg, W.make_inputs(cfg, weights=weights), export=False)
+    one = W.make_inputs(cfg, requests=[1], weights=weights)
+    alone, _, _ = run_build(one.cfg, one, export=False)
+    for k in ("tokens", "parents", "depths", "scores", "mask", "num_nodes"):
+        assert np.array_equal(both[k][1], alone[k][0]), k
+
+    cfg = W.CONFIGS["qwen3-8b-x4"]
+    weights = W.make_weights(cfg)
+    batch, _, _ = run_build(cfg, W.make_inputs(cfg, weights=weights), export=False)
+    one = W.make_inputs(cfg, requests=[2], weights=weights)
+    alone, _, _ = run_build(one.cfg, one, export=False)
+    for k in ("tokens", "parents", "depths", "mask", "num_nodes"):
+        assert np.array_equal(batch[k][2], alone[k][0]), k
+    err = np.abs(batch["scores"][2] - alone["scores"][0])
+    assert float(err[np.isfinite(err)].max()) < 1e-4

@@ -1,6 +1,8 @@
 """The sequential-heap replay comparator on the CPU: a trace made from the
 oracle's own run passes with no events, and planted mistakes in a trace
-(a pop out of order, a wrong score, a wrong child set, a wrong state) fail."""
+(a pop out of order, a wrong score, a wrong child set, a wrong state, a
+state or feature rounded to the wrong side away from a near-tie, a normaliser
+beyond its fp32 bound) fail."""
 import numpy as np
 import pytest
 
@@ -36,19 +38,24 @@ def trace_of(dec, runs):
 
 
 def states_of(dec, runs):
-    """Each expanded slot's state, recomputed along the oracle's own pops."""
+    """Each expanded slot's state and feature row, recomputed along the
+    oracle's own pops: (states [B+1][b][h], features [B][b][h])."""
     p = dec.p
     out = np.zeros((p.budget + 1, len(runs), p.hidden))
+    feat = np.zeros((p.budget, len(runs), p.hidden))
     for q, run in enumerate(runs):
-        t_of = {0: R.head_features(dec.r0[q][None, :], dec.A, dec.H[q, 0], p.precision)[0][0]}
+        t0, a0 = R.head_features(dec.r0[q][None, :], dec.A, dec.H[q, 0], p.precision)
+        t_of = {0: t0[0]}
+        feat[0, q] = a0[0]
         for n in sorted(run.expansions):
             if n == 0:
                 continue
-            r = R.child_states(t_of[run.parent[n]][None, :], dec.U[run.token[n]][None, :], p.embed_scale,
-                               p.precision)[0]
+            r = R.next_states(p, t_of[run.parent[n]][None, :], dec.U[run.token[n]][None, :])[0]
             out[n, q] = r
-            t_of[n] = R.head_features(r[None, :], dec.A, dec.H[q, run.depth[n]], p.precision)[0][0]
-    return out
+            t, a = R.head_features(r[None, :], dec.A, dec.H[q, run.depth[n]], p.precision)
+            t_of[n] = t[0]
+            feat[n, q] = a[0]
+    return out, feat
 
 
 def tree_dict(tree):
@@ -67,8 +74,10 @@ def _setup(**kw):
                                 dict(budget=60, depth=2)])   # 60 > 3 + 9: the heap runs dry
 def test_oracle_trace_passes(kw):
     dec, runs, trace, tree = _setup(**kw)
-    rep = replay.follow_heap(dec, trace, tree, [0, 1], [0, 1], gpu_states=states_of(dec, runs))
-    assert rep.events == 0 and rep.max_score_err < 1e-6 and rep.state_mismatch == 0
+    st, ft = states_of(dec, runs)
+    rep = replay.follow_heap(dec, trace, tree, [0, 1], [0, 1], gpu_states=st, gpu_features=ft)
+    assert rep.events == 0 and rep.max_score_err < 1e-6 and rep.state_ties == 0 and rep.feature_ties == 0
+    assert rep.state_elems > 0 and rep.feature_elems > 0 and rep.max_lse_ratio <= 1 and rep.max_logp_ratio <= 1
     rep = replay.follow_heap(dec, trace, tree, [0, 1], [0, 1])
     assert rep.events == 0
 
@@ -103,11 +112,36 @@ def test_planted_mistakes_fail():
         replay.follow_heap(dec, trace, tree, [0, 1], [0, 1])
 
     dec, runs, trace, tree = _setup()
-    st = states_of(dec, runs)
+    st, ft = states_of(dec, runs)
     node = max(n for n in runs[0].expansions if n > 0)
     st[node, 0, :4] += 0.25
     with pytest.raises(replay.ParityError, match="state"):
-        replay.follow_heap(dec, trace, tree, [0, 1], [0, 1], gpu_states=st)
+        replay.follow_heap(dec, trace, tree, [0, 1], [0, 1], gpu_states=st, gpu_features=ft)
+
+    # one state element moved to its neighbouring bf16 value far from a rounding midpoint
+    dec, runs, trace, tree = _setup()
+    st, ft = states_of(dec, runs)
+    j = int(np.argmax(np.abs(st[node, 0])))
+    dn, up = replay._bf16_neighbours(st[node, 0, j:j + 1])
+    st[node, 0, j] = up[0]
+    with pytest.raises(replay.ParityError, match="near-ties"):
+        replay.follow_heap(dec, trace, tree, [0, 1], [0, 1], gpu_states=st, gpu_features=ft)
+
+    # a feature element one step off
+    dec, runs, trace, tree = _setup()
+    st, ft = states_of(dec, runs)
+    j = int(np.argmax(np.abs(ft[0, 1])))
+    dn, up = replay._bf16_neighbours(ft[0, 1, j:j + 1])
+    ft[0, 1, j] = dn[0]
+    with pytest.raises(replay.ParityError, match="features"):
+        replay.follow_heap(dec, trace, tree, [0, 1], [0, 1], gpu_states=st, gpu_features=ft)
+
+    # a normaliser off by more than its fp32 bound (the child ranking is unchanged)
+    dec, runs, trace, tree = _setup()
+    st, ft = states_of(dec, runs)
+    trace["lse"][0, 0] += 1e-3
+    with pytest.raises(replay.ParityError, match="lse"):
+        replay.follow_heap(dec, trace, tree, [0, 1], [0, 1], gpu_states=st, gpu_features=ft)
 
     dec, runs, trace, tree = _setup()
     trace["num_popped"][1] -= 1
