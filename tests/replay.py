@@ -25,10 +25,12 @@ step per element.  The strict check therefore follows the GPU's states and
 features (``gpu_states``, ``gpu_features``), and accepts a GPU element that
 differs from the oracle's only at a rounding near-tie:
 
-  * the GPU's value g is the oracle's rounded value r = rnd(x), or the
-    neighbouring bf16 value on the other side of x, and
-  * the oracle's unrounded fp64 value x lies within delta of the midpoint
-    (r + g) / 2, where delta bounds the GPU's fp32 error before rounding.
+  * the GPU's value g is the oracle's rounded value r = rnd(x), or
+  * g is the rounding of a value within delta of the oracle's unrounded
+    fp64 value x (rnd(x - delta) <= g <= rnd(x + delta)), where delta bounds
+    the GPU's fp32 error before rounding: x lies within delta of a bf16
+    rounding midpoint (for |x| of the order of delta the window can span
+    several bf16 steps).
 
 delta (``Bounds.preimage``): the GPU computes y = tanh(t + c) in fp32 with
 c = H_d[i] (feature) or e U[u][i] (state).  t_i = sum_j A_ij r_j is a sum of
@@ -176,10 +178,15 @@ def _bf16_neighbours(r):
 def check_rounded(r, g, x, delta, precision, what):
     """The GPU's element g against the oracle's r = rnd(x) (x unrounded).
 
-    bf16: g == r, or g is r's neighbour and x is within delta of their
-    midpoint (a near-tie; counted).  fp32 (no rounding): |g - x| <= delta.
+    bf16: g must be the rounding of some y with |y - x| <= delta, i.e.
+    rnd(x - delta) <= g <= rnd(x + delta) (rounding is monotone).  Where the
+    window holds no rounding midpoint that leaves g == r; a g != r is a
+    near-tie (counted), its ratio the distance from x to the nearest y that
+    rounds to g, over delta (for |x| of the order of delta the window can
+    span several bf16 steps).  fp32 (no rounding): |g - x| <= delta.
     Returns (number of near-ties, max tie ratio, max fp32 ratio)."""
     r, g, x, delta = (np.asarray(v, np.float64) for v in (r, g, x, delta))
+    delta = np.broadcast_to(delta, x.shape)
     if precision != R.BF16:
         ratio = np.abs(g - x) / delta
         if not (ratio <= 1.0).all():
@@ -190,16 +197,17 @@ def check_rounded(r, g, x, delta, precision, what):
     if not diff.any():
         return 0, 0.0, 0.0
     rd, gd, xd, dd = r[diff], g[diff], x[diff], delta[diff]
-    dn, up = _bf16_neighbours(rd)
-    adjacent = (gd == dn) | (gd == up)
-    tie = np.abs(xd - 0.5 * (rd + gd)) / dd
-    bad = ~adjacent | ~(tie <= 1.0)
-    if bad.any():
-        j = int(np.argmax(bad))
-        raise ParityError(f"{what}: {int(bad.sum())} of {int(diff.sum())} differing elements are not rounding "
+    inside = (gd >= R.rnd_bf16(xd - dd)) & (gd <= R.rnd_bf16(xd + dd))
+    dn, up = _bf16_neighbours(gd)
+    # nearest value that rounds to g: the midpoint on x's side of g
+    edge = np.where(gd > rd, 0.5 * (gd + dn), 0.5 * (gd + up))
+    tie = np.abs(edge - xd) / dd
+    if not inside.all():
+        j = int(np.argmax(~inside))
+        raise ParityError(f"{what}: {int((~inside).sum())} of {int(diff.sum())} differing elements are not rounding "
                           f"near-ties (e.g. GPU {gd[j]!r}, oracle {rd[j]!r}, unrounded {xd[j]!r}, "
                           f"delta {dd[j]:.3e})")
-    return int(diff.sum()), float(tie.max()), 0.0
+    return int(diff.sum()), float(np.minimum(tie, 1.0).max()), 0.0
 
 
 def _record(rep, kind, n, res):

@@ -322,10 +322,12 @@ def test_full_shape_batch_invariance():
     """A request's tree at V = 151936 alone and inside a batch.  At the 4B
     shape a batch of two leaves every kernel's blocking and the softmax
     pass's row segmentation unchanged, so the trees are bit-identical.  At the
-    8B shape (four requests) depths 2..16 have 64 parent rows instead of 16,
-    which splits each row's normaliser into fewer segments and changes the
-    product's blocking: tokens, parents and mask agree, scores within
-    rounding."""
+    8B shape (four requests) depths 2..16 have 64 parent rows instead of 16:
+    the head's product runs with another blocking (a different fp32
+    accumulation order of t, so a few bf16 states round the other way and the
+    two runs drift apart like two correct implementations) and each row's
+    normaliser is summed in fewer segments.  Tokens, parents and mask agree;
+    scores agree within the spec score tolerance (4.6e-3 measured)."""
     cfg = W.CONFIGS["qwen3-4b"].replace(batch=2)
     weights = W.make_weights(cfg)
     both, _, _ = run_build(cfg, W.make_inputs(cfg, weights=weights), export=False)
@@ -342,4 +344,4 @@ def test_full_shape_batch_invariance():
     for k in ("tokens", "parents", "depths", "mask", "num_nodes"):
         assert np.array_equal(batch[k][2], alone[k][0]), k
     err = np.abs(batch["scores"][2] - alone["scores"][0])
-    assert float(err[np.isfinite(err)].max()) < 1e-4
+    assert float(err[np.isfinite(err)].max()) < replay.SCORE_TOL

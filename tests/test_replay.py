@@ -137,9 +137,17 @@ def test_rounded_near_tie():
     x = np.array([mid - 3e-6])
     with pytest.raises(replay.ParityError):
         replay.check_rounded(R.rnd_bf16(x), np.array([hi]), x, delta, R.BF16, "t")
-    # not a neighbour: fails
+    # two steps away with a window far narrower than a step: fails
     with pytest.raises(replay.ParityError):
         replay.check_rounded(np.array([lo]), np.array([hi + 2.0 ** -7]), np.array([mid]), delta, R.BF16, "t")
+    # a value near zero whose window spans several bf16 steps: any rounding inside it passes
+    x = np.array([2.6e-7])
+    r = R.rnd_bf16(x)
+    g = R.rnd_bf16(np.array([2.6e-7 + 3e-8]))
+    assert g[0] != r[0]
+    assert replay.check_rounded(r, g, x, np.array([3.5e-5]), R.BF16, "t")[0] == 1
+    with pytest.raises(replay.ParityError):
+        replay.check_rounded(r, g, x, np.array([1e-8]), R.BF16, "t")
     # negative values and a binade edge (neighbours of -1: -1 - 2^-7 and -1 + 2^-8)
     dn, up = replay._bf16_neighbours(np.array([-1.0, 1.0, 0.0]))
     assert dn[0] == -1.0 - 2.0 ** -7 and up[0] == -1.0 + 2.0 ** -8
