@@ -282,6 +282,22 @@ dartree_status dartree_lse_topk(const float* z, int32_t rows, int32_t vocab, int
                                 float temperature, float* lse, float* cand_logp,
                                 int32_t* cand_ids, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* dartree_lse_topk for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same kernels and results, with the row-segment records kept in a
+ * static device array of the library, DARTREE_LSE_TOPK_STATIC_SCRATCH_BYTES
+ * per GPU, held until the process ends.  That size covers every call
+ * dartree_lse_topk_workspace_size accepts (a larger need would return
+ * DARTREE_ERR_UNSUPPORTED).  The call allocates nothing and takes no
+ * workspace; its first call on a device looks up the array's address there
+ * (DARTREE_ERR_HIP if that fails).  Every call on one GPU shares the array:
+ * calls that may overlap on one GPU (several streams, several host threads)
+ * race and give undefined results; calls ordered on one stream do not. */
+#define DARTREE_LSE_TOPK_STATIC_SCRATCH_BYTES (576 * 1024)
+dartree_status dartree_lse_topk_noalloc(const float* z, int32_t rows, int32_t vocab, int32_t k,
+                                        float temperature, float* lse, float* cand_logp, int32_t* cand_ids,
+                                        hipStream_t stream);
+
 /* Shared candidate sets (Alg. 1, C_d = TopK(L_d^base, K)) of `rows` rows of
  * fp32 logits [rows][vocab]: ids [rows][K] in (value desc, id asc) order,
  * 1 <= K <= min(vocab, DARTREE_MAX_CANDIDATES).  The workspace (size from

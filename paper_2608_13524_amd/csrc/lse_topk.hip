@@ -13,6 +13,8 @@
 // keeps the lower id first; every merge compares (value desc, id asc).
 #include <float.h>
 
+#include <mutex>
+
 #include "reduce.hpp"
 
 namespace dartree {
@@ -268,3 +270,55 @@ hipError_t launch_lse_topk(const float* z, int64_t rows, int64_t vocab, int k, f
 }
 
 }  // namespace dartree
+
+// ---------------------------------------------------------------------------
+// dartree_lse_topk without a workspace argument and without allocating: the
+// segment records live in `scratch`, a device array of the library that each
+// GPU holds until the process ends.  Its address on a device comes from
+// hipGetSymbolAddress, taken once per device with that device current (the
+// array's name in host code is not a device address).
+// ---------------------------------------------------------------------------
+namespace {
+
+// rows * segments <= 2047 whenever a row is split (a split needs fewer than
+// 1024 rows, and then rows * ceil(1024 / rows) < 2048), times the largest
+// record (68 floats at k <= 32): 556784 bytes of every valid call fit.
+static_assert(2047 * dartree::record_floats_of(32) * 4 <= DARTREE_LSE_TOPK_STATIC_SCRATCH_BYTES,
+              "static scratch too small for the largest split");
+static __device__ __align__(256) float scratch[DARTREE_LSE_TOPK_STATIC_SCRATCH_BYTES / sizeof(float)];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// The current device's address of `scratch` (nullptr on failure).
+void* scratch_on_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" dartree_status dartree_lse_topk_noalloc(const float* z, int32_t rows, int32_t vocab, int32_t k,
+                                                   float temperature, float* lse, float* cand_logp,
+                                                   int32_t* cand_ids, hipStream_t stream) {
+  size_t need = 0;
+  dartree_status v = dartree_lse_topk_workspace_size(rows, vocab, k, &need);
+  if (v != DARTREE_OK) return v;
+  if (!__builtin_isfinite(temperature) || temperature < 0.f) return DARTREE_ERR_INVALID_ARG;
+  if (!z || !lse || !cand_logp || !cand_ids) return DARTREE_ERR_INVALID_ARG;
+  if (need > DARTREE_LSE_TOPK_STATIC_SCRATCH_BYTES) return DARTREE_ERR_UNSUPPORTED;
+  void* ptr = need > 0 ? scratch_on_current_device() : nullptr;
+  if (need > 0 && !ptr) return DARTREE_ERR_HIP;
+  const float tau = temperature > 0.f ? temperature : 1.f;
+  return dartree::launch_lse_topk(z, rows, vocab, k, tau, lse, cand_logp, cand_ids, ptr, true, stream) == hipSuccess
+             ? DARTREE_OK
+             : DARTREE_ERR_HIP;
+}

@@ -30,6 +30,7 @@ MAX_BRANCH = 32
 MAX_CANDIDATES = 256
 MAX_SORT = 4096
 MAX_HEAP_BUDGET = 1024
+LSE_TOPK_STATIC_SCRATCH_BYTES = 576 * 1024
 
 SYMBOLS = [
     "dartree_abi_version", "dartree_status_string", "dartree_validate",
@@ -37,7 +38,7 @@ SYMBOLS = [
     "dartree_build_tree", "dartree_build_tree_timed", "dartree_export_supertree", "dartree_export_states",
     "dartree_export_features", "dartree_project",
     "dartree_project_workspace_size",
-    "dartree_lse_topk_workspace_size", "dartree_lse_topk", "dartree_select_topw",
+    "dartree_lse_topk_workspace_size", "dartree_lse_topk", "dartree_lse_topk_noalloc", "dartree_select_topw",
     "dartree_prune_levels", "dartree_candidate_sets_workspace_size", "dartree_candidate_sets",
     "dartree_heap_workspace_size", "dartree_build_tree_heap", "dartree_export_heap",
     "dartree_accept_walk", "dartree_tree_attention_workspace_size", "dartree_tree_attention",
@@ -136,6 +137,7 @@ def lib() -> ctypes.CDLL:
     L.dartree_project_workspace_size.argtypes = [i32, i32, i32, i32, ctypes.POINTER(sz)]
     L.dartree_lse_topk_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(sz)]
     L.dartree_lse_topk.argtypes = [vp, i32, i32, i32, f32, vp, vp, vp, vp, sz, vp]
+    L.dartree_lse_topk_noalloc.argtypes = [vp, i32, i32, i32, f32, vp, vp, vp, vp]
     L.dartree_select_topw.argtypes = [i32, i32, i32, i32, f32, vp, vp, vp, vp, vp, vp, vp]
     L.dartree_prune_levels.argtypes = [P, vp, vp, vp, ctypes.POINTER(TreeC), vp]
     L.dartree_candidate_sets_workspace_size.argtypes = [i32, i32, i32, ctypes.POINTER(sz)]
@@ -436,6 +438,13 @@ def lse_topk(z, k: int, temperature: float, lse, cand_logp, cand_ids, ws=None, s
     _check(lib().dartree_lse_topk(_ptr(z), rows, vocab, k, temperature, _ptr(lse), _ptr(cand_logp),
                                   _ptr(cand_ids), _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)),
            "dartree_lse_topk")
+
+
+def lse_topk_noalloc(z, k: int, temperature: float, lse, cand_logp, cand_ids, stream=None) -> None:
+    """lse_topk with the library's static scratch (no workspace, nothing allocated)."""
+    rows, vocab = z.shape
+    _check(lib().dartree_lse_topk_noalloc(_ptr(z), rows, vocab, k, temperature, _ptr(lse), _ptr(cand_logp),
+                                          _ptr(cand_ids), _stream(stream)), "dartree_lse_topk_noalloc")
 
 
 def select_topw(batch: int, n_parent: int, k: int, n_keep: int, depth_bonus: float, parent_score,
