@@ -220,6 +220,85 @@ def time_consumer(torch, cfg, out, stream, reps: int = 50) -> dict:
             "attention_roofline": roof}
 
 
+# The per-kernel targets are stated for the throughput-stress shape: 16
+# requests x 64 nodes = 1024 parent rows against the 151936-token vocabulary
+# at hidden 5120 (the only shape above the MFMA ridge).
+TARGET_SHAPE = dict(rows=1024, vocab=151936, hidden=5120, k=8, rows_per_group=64)
+
+
+def time_targets(torch, dev, stream, reps: int = 10, calibration: bool = False) -> dict:
+    """The projection and the softmax/top-k pass at the stress shape, through
+    dartree_project and dartree_lse_topk on device buffers filled with random
+    bf16 features (tanh of normals, like the head's output) and weights
+    N(0, 0.02^2) (random operands: the matrix cores' power draw, and so their
+    clock, depends on the data).  No host inputs and no oracle.  Each launch is
+    timed by its own event pair on the stream it runs on; the projection and
+    the pass alternate as in a round, so the pass reads logits the projection
+    has just written."""
+    s = TARGET_SHAPE
+    R, V, h, k = s["rows"], s["vocab"], s["hidden"], s["k"]
+    g = torch.Generator(device=dev).manual_seed(11)
+    x = torch.tanh(torch.randn(R, h, device=dev, generator=g) * 1.4).to(torch.bfloat16)
+    U = (torch.randn(V, h, device=dev, generator=g) * 0.02).to(torch.bfloat16)
+    groups = R // s["rows_per_group"]
+    bias = torch.randn(groups, V, device=dev, generator=g) * 2.0
+    z = torch.empty(R, V, dtype=torch.float32, device=dev)
+    nws = D.project_workspace_size(D.BF16, R, V, h)
+    pws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    lse = torch.empty(R, dtype=torch.float32, device=dev)
+    lp = torch.empty(R, k, dtype=torch.float32, device=dev)
+    ids = torch.empty(R, k, dtype=torch.int32, device=dev)
+    lws = torch.empty(max(D.lse_topk_workspace_size(R, V, k), 1), dtype=torch.uint8, device=dev)
+    xi, Ui = x.view(torch.int16), U.view(torch.int16)
+
+    def proj():
+        D.project(D.BF16, xi, Ui, bias, V, z, s["rows_per_group"], pws)
+
+    def soft():
+        D.lse_topk(z, k, 1.0, lse, lp, ids, lws)
+
+    for _ in range(2):
+        proj()
+        soft()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(2 * reps)]
+    for i in range(reps):
+        ev[2 * i][0].record(stream)
+        proj()
+        ev[2 * i][1].record(stream)
+        ev[2 * i + 1][0].record(stream)
+        soft()
+        ev[2 * i + 1][1].record(stream)
+    torch.cuda.synchronize()
+    pt = np.array([a.elapsed_time(b) * 1e3 for a, b in ev[0::2]])
+    st = np.array([a.elapsed_time(b) * 1e3 for a, b in ev[1::2]])
+    flops = 2.0 * R * h * V
+    pbytes = V * (2 * h + 4 * groups + 4 * R) + 2 * h * R
+    lbytes = 4.0 * R * V
+    p_tf = flops / pt.mean() / 1e6
+    l_gb = lbytes / st.mean() / 1e3
+    out = {
+        "shape": {"rows": R, "vocab": V, "hidden": h, "k": k, "bias_rows": groups},
+        "projection": {"avg_launch_us": float(pt.mean()), "min_launch_us": float(pt.min()),
+                       "algorithmic_flops_per_launch": flops, "algorithmic_bytes_per_launch": pbytes,
+                       "achieved_TFs": p_tf, "peak_TFs": MFMA_BF16_PEAK_TFS, "frac": p_tf / MFMA_BF16_PEAK_TFS,
+                       "target_frac": 0.5, "launches": reps,
+                       "note": "includes the fix-up launch of the split last wave when the split applies"},
+        "lse_topk": {"avg_launch_us": float(st.mean()), "min_launch_us": float(st.min()),
+                     "algorithmic_bytes_per_launch": lbytes, "achieved_GBs": l_gb, "peak_GBs": HBM_PEAK_GBS,
+                     "frac": l_gb / HBM_PEAK_GBS, "target_frac": 0.6, "launches": reps},
+        "timing": "HIP events around each dartree_project / dartree_lse_topk call on the launch stream",
+    }
+    out["projection_mfma_frac"] = out["projection"]["frac"]
+    out["lse_topk_hbm_frac"] = out["lse_topk"]["frac"]
+    del x, bias, z, pws, lws
+    if calibration:   # the copy of known size that scales the traffic counters, in the same process
+        out["calibration"] = calibrate(torch, dev, U, stream)
+    del U
+    torch.cuda.empty_cache()
+    return out
+
+
 def gpu_env(torch) -> dict:
     """Device, HIP runtime and the shader clock, read from the device's
     pp_dpm_sclk file in sysfs (the level marked current), sampled right after
@@ -289,6 +368,10 @@ def main() -> int:
                     help="heap: time only the sequential-heap baseline (for a kernel trace of it alone)")
     ap.add_argument("--width", type=int, default=None, help="override the workload's layer width W (sweeps)")
     ap.add_argument("--budget", type=int, default=None, help="override the workload's budget B (sweeps)")
+    ap.add_argument("--no-targets", action="store_true",
+                    help="skip the per-kernel target leg at the stress shape")
+    ap.add_argument("--targets-only", action="store_true",
+                    help="run only the per-kernel target leg (for its counter runs)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only (--gpus 1): the library builds trees on one device. Requests "
@@ -321,6 +404,14 @@ def main() -> int:
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         return np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(K)]), ev[0].elapsed_time(ev[K]), wall
+
+    if args.targets_only:
+        log("per-kernel targets at the stress shape only")
+        tg = time_targets(torch, dev, torch.cuda.current_stream(), reps=max(args.steps, 1), calibration=True)
+        log(f"  projection {tg['projection']['avg_launch_us']:.1f} us ({tg['projection_mfma_frac']:.3f} of MFMA), "
+            f"softmax/top-k {tg['lse_topk']['avg_launch_us']:.1f} us ({tg['lse_topk_hbm_frac']:.3f} of HBM)")
+        print(json.dumps({"targets": tg, "env": gpu_env(torch)}), flush=True)
+        return 0
 
     if args.schedule == "heap":
         log(f"sequential heap only: {args.steps} rounds")
@@ -498,6 +589,15 @@ def main() -> int:
         heap["vs_dartree"] = heap["us_per_round"] / us_round
         log(f"  {heap['us_per_round']:.1f} us/round, {heap['vs_dartree']:.2f}x DARTree's round")
 
+    targets = None
+    if not args.no_targets and cfg.precision == W.BF16:
+        log("per-kernel targets at the stress shape (1024 x 151936 x 5120)")
+        targets = time_targets(torch, dev, stream)
+        log(f"  projection {targets['projection']['avg_launch_us']:.1f} us/launch = "
+            f"{targets['projection']['achieved_TFs']:.0f} TFLOP/s ({targets['projection_mfma_frac']:.3f} of MFMA); "
+            f"softmax/top-k {targets['lse_topk']['avg_launch_us']:.1f} us/launch = "
+            f"{targets['lse_topk']['achieved_GBs']:.0f} GB/s ({targets['lse_topk_hbm_frac']:.3f} of HBM)")
+
     consumer = None
     if cfg.precision == W.BF16:
         consumer = time_consumer(torch, cfg, out, stream)
@@ -529,7 +629,8 @@ def main() -> int:
         "projection_tflops": proj_flops,
         "projection_mfma_frac": proj_flops / MFMA_BF16_PEAK_TFS,
         "kernels": kernels, "instrumented_us_per_round": instrumented_us,
-        "roofline": roof, "lse_topk_roofline": lse_roof, "calibration": cal, "sequential_heap": heap,
+        "roofline": roof, "lse_topk_roofline": lse_roof, "targets": targets, "calibration": cal,
+        "sequential_heap": heap,
         "consumer": consumer, "env": env,
         "cpu_baseline": cpu,
     }

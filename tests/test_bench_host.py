@@ -42,3 +42,12 @@ def test_softmax_pass_work_is_one_read_of_z():
 def test_traffic_is_reported_only_for_a_summarised_kernel():
     assert bench.measured_traffic("qwen3-4b", "lse_topk") is None
     assert bench.measured_traffic("no-such-workload", "logits") is None
+
+
+def test_target_shape_is_the_stress_workload():
+    """The per-kernel targets are measured at the stress workload's steady
+    shape: 16 requests x 64 nodes = 1024 parent rows, V = 151936, h = 5120."""
+    cfg = W.CONFIGS["stress-x16"]
+    s = bench.TARGET_SHAPE
+    assert s["rows"] == cfg.batch * cfg.width and s["vocab"] == cfg.vocab and s["hidden"] == cfg.hidden
+    assert s["k"] == cfg.branch and s["rows"] // s["rows_per_group"] == cfg.batch
