@@ -251,7 +251,9 @@ dartree_status dartree_export_features(const dartree_params* p, const void* ws, 
  * (and for testing each step on injected inputs). */
 
 /* Bytes of device scratch dartree_project needs for this shape (host only;
- * 0 for shapes that never split a tile along K). */
+ * 0 for shapes that never split a tile along K).  bf16 with >= 512 rows and
+ * >= 16384 columns: 64 MB for partial tiles, plus rows * hidden * 2 bytes for
+ * a copy of x in MFMA-fragment order when rows is a multiple of 512. */
 dartree_status dartree_project_workspace_size(int32_t precision, int32_t rows, int32_t vocab, int32_t hidden,
                                               size_t* bytes);
 

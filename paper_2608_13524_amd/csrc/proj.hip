@@ -20,6 +20,7 @@
 //    rows).  128x128 output tiles, 64-deep K steps staged through
 //    double-buffered, padded LDS tiles shared by 4 waves (64x64 each).
 // fp32 path: plain FMA loop (small problems only).
+
 #include <algorithm>
 
 #include "internal.hpp"
@@ -627,6 +628,254 @@ __global__ __launch_bounds__(512) void proj_bf16_big(KArgs a, int vec, BigPlan p
   }
 }
 
+// ---------------------------------------------------------------------------
+// Many rows, wide node tiles: 512 node rows x 128 weight rows per block (the
+// same 256 KB of accumulators as 256 x 256), 8 waves, two per SIMD, each
+// 64 node rows x 128 weight rows (2 x 4 tiles of 32x32).  Only the weights go
+// through LDS: 16 KB per 64-deep step, a ring of WAHEAD + WBAR stages filled
+// WAHEAD steps ahead with buffer loads straight to swizzled LDS, one barrier
+// every WBAR steps.  Each wave loads its own node-row fragments into registers
+// one step ahead, from a copy of the node rows rearranged into fragment order
+// (1 KB contiguous per load).  Per step the LDS carries 16 KB of fills and
+// 128 KB of fragment reads (the 256x256 kernel: 64 KB and 192 KB).
+// ---------------------------------------------------------------------------
+constexpr int WBM = 512, WBN = 128;
+constexpr int WAHEAD = 6, WBAR = 2;
+
+// N-tile major: the node tiles of one weight tile are consecutive tiles, so
+// they run at the same time on one XCD and share the weights in its L2.
+__device__ __forceinline__ BigTile wide_tile(int M, int N, int t) {
+  const int ntm = (M + WBM - 1) / WBM;
+  BigTile b;
+  b.n0 = (t / ntm) * WBN;
+  b.m0 = (t % ntm) * WBM;
+  b.nl = min(b.n0, N - WBN);
+  b.ml = min(b.m0, M - WBM);
+  return b;
+}
+
+constexpr int vmcnt_imm(int n) { return ((n >> 4) << 14) | (n & 15) | 0x0F70; }
+
+// Node rows in MFMA-fragment order: 16-byte chunk c (k = 8c..8c+7) of row
+// 32 rb + r at element ((rb * (K / 8) + c) * 32 + r) * 8, so the 64 lanes of
+// one operand load (32 rows, two adjacent chunks) read 1 KB contiguously.
+__global__ __launch_bounds__(256) void pack_x_frag(const uint16_t* __restrict__ x, int M, int K,
+                                                   uint16_t* __restrict__ xp) {
+  const int64_t t = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  const int kc = K / 8;
+  const int64_t total = int64_t(M) * kc;
+  if (t >= total) return;
+  const int r = int(t & 31);
+  const int64_t rc = t >> 5;                 // (rb, c)
+  const int c = int(rc % kc);
+  const int rb = int(rc / kc);
+  const int m = 32 * rb + r;
+  *reinterpret_cast<u32x4*>(xp + t * 8) = *reinterpret_cast<const u32x4*>(x + int64_t(m) * K + 8 * c);
+}
+
+template <int EPI>
+__global__ __launch_bounds__(512, 2) void proj_bf16_wide(KArgs a, int vec, BigPlan pl, const uint16_t* xpk) {
+  constexpr int BAR = WBAR;
+  constexpr int kWStage = WAHEAD + BAR;   // a fill never overwrites a stage read since the last barrier
+  constexpr int kStage = WBN * GBK;       // 8192 elements = 16 KB
+  __shared__ __attribute__((aligned(16))) uint16_t smem[kWStage * kStage];
+  const int lane = threadIdx.x & 63, r32 = lane & 31, kh = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int M = a.M, N = a.N, K = a.K;
+  const int nk_all = K / GBK;
+  int t, ks = 0, nk = nk_all, slot = -1;
+  if (int(blockIdx.x) < pl.full) {
+    t = xcd_order(blockIdx.x, pl.full);
+  } else {
+    const int item = xcd_order(int(blockIdx.x) - pl.full, pl.rem * pl.pieces);
+    const int piece = item / pl.rem, r = item % pl.rem;
+    t = pl.full + r;
+    ks = piece * nk_all / pl.pieces;
+    nk = (piece + 1) * nk_all / pl.pieces - ks;
+    slot = r * pl.pieces + piece;
+  }
+  const BigTile tl = wide_tile(M, N, t);
+  const int m0 = tl.m0, n0 = tl.n0, ml = tl.ml, nl = tl.nl;
+  const uint16_t* Wt = static_cast<const uint16_t*>(a.w);
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(Wt + int64_t(nl) * K), (short)0, WBN * K * 2, 0x00020000);
+  const int lrow = lane >> 3, lcp = lane & 7;
+  const unsigned vo0 = unsigned(lrow * K * 2 + ((lcp ^ swz16(lrow)) * 16));
+  const unsigned vo1 = unsigned(lrow * K * 2 + ((lcp ^ swz16(8 + lrow)) * 16));
+  const int sw = swz16(r32 & 15);
+  // packed node rows: row block (ml + 64 wave + 32 j) / 32, chunk 8 step + 2 sub + kh, row r32
+  const uint16_t* xr[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+    xr[j] = xpk + ((int64_t((ml + 64 * wave + 32 * j) >> 5) * (K / 8) + ks * 8 + kh) * 32 + r32) * 8;
+
+  f32x16 acc[2][4];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[j][i][v] = 0.f;
+
+  // Every step issues the same loads (past the last step they repeat it into
+  // a stage or buffer nothing reads), so the compiler's wait counts never
+  // have to assume a path with fewer loads in flight.
+  auto dma = [&](int kt) {
+    LDS_AS uint16_t* base = (LDS_AS uint16_t*)smem + (kt % kWStage) * kStage + 16 * wave * GBK;
+    const int ksrc = min(kt, nk - 1);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const unsigned so = unsigned((16 * wave + 8 * i) * K * 2 + (ks + ksrc) * GBK * 2);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (LDS_AS void*)(base + 8 * i * GBK), 16, i ? vo1 : vo0, so, 0, 0);
+    }
+  };
+  u32x4 xf[2][4][2];   // [step parity][sub][node tile]
+  auto load_x = [&](int kt, int buf) {
+    kt = min(kt, nk - 1);
+#pragma unroll
+    for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) xf[buf][sub][j] = *reinterpret_cast<const u32x4*>(xr[j] + (kt * 8 + 2 * sub) * 256);
+  };
+  bf16x8 wf[2][4];     // [sub parity][weight tile]
+  auto read_w = [&](int kt, int sub, int buf) {
+    const LDS_AS uint16_t* Sw = (const LDS_AS uint16_t*)smem + (kt % kWStage) * kStage;
+    const int c = ((2 * sub + kh) ^ sw) * 8;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      wf[buf][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const LDS_AS u32x4*>(Sw + (32 * i + r32) * GBK + c));
+  };
+  auto barrier = [] { asm volatile("s_barrier" ::: "memory"); };
+
+  // prologue: weight stages of steps 0 .. WAHEAD - 1 and node rows of step 0
+  for (int kt = 0; kt < WAHEAD; ++kt) dma(kt);
+  load_x(0, 0);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  barrier();
+  read_w(0, 0, 0);
+  // one 64-deep step; the node rows of step s2 sit in buffer `half`
+  auto step = [&](int s2, int half) __attribute__((always_inline)) {
+    load_x(s2 + 1, half ^ 1);
+    dma(s2 + WAHEAD);
+    __builtin_amdgcn_sched_barrier(0);   // the step's loads go out before its products
+#pragma unroll
+    for (int sub = 0; sub < 4; ++sub) {
+      if (sub < 3) {
+        read_w(s2, sub + 1, (sub + 1) & 1);
+      } else if (s2 + 1 < nk) {
+        if ((s2 + 1) % BAR == 0) {
+          // the next BAR steps' weights landed (this wave's share; the last
+          // of them was issued WAHEAD - BAR steps ago, and each step since
+          // issued 8 node-row loads and 2 fills) and every wave is done
+          // reading the stages the fills after this barrier reuse
+          __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+          __builtin_amdgcn_s_waitcnt(vmcnt_imm(10 * (WAHEAD - BAR)));
+          barrier();
+        }
+        read_w(s2 + 1, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);   // the next weights' reads overlap these products
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          acc[j][i] = mfma32(__builtin_bit_cast(bf16x8, xf[half][sub][j]), wf[sub & 1][i], acc[j][i]);
+    }
+  };
+  // steps in pairs (buffers alternate), both halves unconditional so that
+  // every path around the loop carries the same loads in flight
+#pragma unroll 1
+  for (int st = 0; st + 1 < nk; st += 2) {
+    step(st, 0);
+    step(st + 1, 1);
+  }
+  if (nk & 1) step(nk - 1, 0);
+
+  // the repeated loads past the last step land before the block's LDS goes
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+
+  // element v of acc[j][i] in lane l is out[m][n] at node row m = 64 wave +
+  // 32 j + 8 (v / 4) + 4 (l / 32) + v % 4 and weight row n = 32 i + l % 32
+  // (whole 128-byte lines per store instruction)
+  (void)vec;
+  if (slot >= 0) {
+    float* P = pl.split + size_t(slot) * (WBM * WBN);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          P[(64 * wave + 32 * j + 8 * (v >> 2) + 4 * kh + (v & 3)) * WBN + 32 * i + r32] = acc[j][i][v];
+    return;
+  }
+  const bool block_bias = a.rows_per_group % 32 == 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int n = nl + 32 * i + r32;
+    const bool n_new = n >= n0;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int mb = ml + 64 * wave + 32 * j;
+      if (mb + 31 < m0) continue;
+      if (block_bias) {
+        const int64_t bb = bias_base(a, mb) + n;
+        if constexpr (EPI == EPI_LOGITS) {
+          const float b = n_new ? a.bias_f32[bb] : 0.f;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int m = mb + 8 * (v >> 2) + 4 * kh + (v & 3);
+            if (m >= m0 && n_new) __builtin_nontemporal_store(acc[j][i][v] + b, a.out + int64_t(m) * N + n);
+          }
+        } else {
+          const float hb = n_new ? bf16_to_f32(static_cast<const uint16_t*>(a.bias_act)[bb]) : 0.f;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int m = mb + 8 * (v >> 2) + 4 * kh + (v & 3);
+            if (m >= m0 && n_new) {
+              const int64_t o = int64_t(m) * N + n;
+              a.out[o] = acc[j][i][v];
+              static_cast<uint16_t*>(a.act_out)[o] = f32_to_bf16(tanhf(acc[j][i][v] + hb));
+            }
+          }
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int m = mb + 8 * (v >> 2) + 4 * kh + (v & 3);
+          if (m >= m0 && n_new) emit<EPI, true, EPI == EPI_LOGITS>(a, m, n, acc[j][i][v]);
+        }
+      }
+    }
+  }
+}
+
+// The split wide tiles: 16 blocks per tile, each 32 rows x 128 columns.
+template <int EPI>
+__global__ __launch_bounds__(256) void proj_wide_fixup(KArgs a, int vec, BigPlan pl) {
+  const int r = blockIdx.x / 16, row0 = (blockIdx.x % 16) * 32;
+  const BigTile tl = wide_tile(a.M, a.N, pl.full + r);
+  const float* P = pl.split + size_t(r) * pl.pieces * (WBM * WBN);
+  const int c4 = threadIdx.x & 31;
+  const int n = tl.nl + 4 * c4;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int row = row0 + (threadIdx.x >> 5) + 8 * u;
+    const int m = tl.ml + row;
+    if (m < tl.m0) continue;
+    const size_t e = size_t(row) * WBN + 4 * c4;
+    f32x4 v = *reinterpret_cast<const f32x4*>(P + e);
+    for (int pc = 1; pc < pl.pieces; ++pc) v += *reinterpret_cast<const f32x4*>(P + size_t(pc) * (WBM * WBN) + e);
+    if (n >= tl.n0) {
+      emit4<EPI, EPI == EPI_LOGITS>(a, m, n, v, vec != 0);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (n + k >= tl.n0) emit<EPI, true, EPI == EPI_LOGITS>(a, m, n + k, v[k]);
+    }
+  }
+}
+
 // The split tiles: 16 blocks per tile, each 16 rows x 256 columns; every
 // thread sums the pieces of 4 float4s in piece order and applies the epilogue.
 template <int EPI>
@@ -711,6 +960,9 @@ hipError_t launch_stream_nt(const KArgs& k, int epi, hipStream_t s) {
 // and at least kMinPieceSteps 64-deep K steps per piece.
 constexpr int kSplitMaxBlocks = 256;
 constexpr int kMinPieceSteps = 4;
+// one partial tile per split block; the two many-row tilings hold the same
+constexpr size_t kSplitBytes = size_t(kSplitMaxBlocks) * GBM * GBN * sizeof(float);
+static_assert(WBM * WBN == GBM * GBN, "split partial slots");
 
 // Compute units of the current device (cached per device).
 int device_cus() {
@@ -728,6 +980,11 @@ int device_cus() {
 // Shapes the 256x256-tile kernel takes: the vocabulary at >= 512 rows, and
 // (only when split) the head at >= 512 rows.
 bool big_logits(const KArgs& k) { return k.M >= 2 * GBM && k.N >= 64 * GBN; }
+// The 512-row tiles where they compute no more rows than the 256-row ones
+// (their node-row blocks are 32 rows, so also M % 32 == 0).
+bool wide_logits(const KArgs& k) {
+  return big_logits(k) && k.M % 32 == 0 && (k.M + WBM - 1) / WBM * WBM == (k.M + GBM - 1) / GBM * GBM;
+}
 bool big_head_candidate(const KArgs& k) { return k.M >= 2 * GBM && k.N >= GBN && k.K >= 2 * kMinPieceSteps * GBK; }
 
 BigPlan big_plan(const KArgs& k, float* split) {
@@ -750,6 +1007,30 @@ hipError_t launch_big(const KArgs& k, const BigPlan& pl, hipStream_t s) {
   return hipGetLastError();
 }
 
+BigPlan wide_plan(const KArgs& k, float* split) {
+  const int T = ((k.M + WBM - 1) / WBM) * ((k.N + WBN - 1) / WBN);
+  BigPlan pl{T, 0, 1, nullptr};
+  if (!split) return pl;
+  const int ncu = std::min(device_cus(), kSplitMaxBlocks);
+  const int rem = T % ncu;
+  if (rem == 0) return pl;
+  const int pieces = std::min(ncu / rem, (k.K / GBK) / kMinPieceSteps);
+  if (pieces < 2) return pl;
+  return BigPlan{T - rem, rem, pieces, split};
+}
+
+template <int EPI>
+hipError_t launch_wide(const KArgs& k, const BigPlan& pl, uint16_t* xpk, hipStream_t s) {
+  const int vec = epilogue_vec_ok(k, EPI);
+  const int64_t chunks = int64_t(k.M) * (k.K / 8);
+  hipLaunchKernelGGL(pack_x_frag, dim3(unsigned((chunks + 255) / 256)), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(k.x), k.M, k.K, xpk);
+  const dim3 grid(pl.full + pl.rem * pl.pieces);
+  hipLaunchKernelGGL((proj_bf16_wide<EPI>), grid, dim3(512), 0, s, k, vec, pl, static_cast<const uint16_t*>(xpk));
+  if (pl.rem > 0) hipLaunchKernelGGL((proj_wide_fixup<EPI>), dim3(pl.rem * 16), dim3(256), 0, s, k, vec, pl);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 size_t proj_split_bytes(int precision, int epilogue, int64_t M, int64_t N, int64_t K) {
@@ -759,7 +1040,9 @@ size_t proj_split_bytes(int precision, int epilogue, int64_t M, int64_t N, int64
   k.N = int(N);
   k.K = int(K);
   const bool big = epilogue == EPI_LOGITS ? big_logits(k) : big_head_candidate(k);
-  return big ? size_t(kSplitMaxBlocks) * GBM * GBN * sizeof(float) : 0;
+  // the split partials, then (512-row tiles) the node rows in fragment order
+  const size_t packed = epilogue == EPI_LOGITS && wide_logits(k) ? size_t(M) * size_t(K) * 2 : 0;
+  return big ? kSplitBytes + packed : 0;
 }
 
 hipError_t launch_project(const ProjArgs& p, hipStream_t s) {
@@ -789,7 +1072,12 @@ hipError_t launch_project(const ProjArgs& p, hipStream_t s) {
   if (k.M <= 32) return launch_stream_nt<2>(k, p.epilogue, s);
   if (k.M <= 48) return launch_stream_nt<3>(k, p.epilogue, s);
   if (k.M <= 64) return launch_stream_nt<4>(k, p.epilogue, s);
-  if (p.epilogue == EPI_LOGITS && big_logits(k)) return launch_big<EPI_LOGITS>(k, big_plan(k, p.split), s);
+  if (p.epilogue == EPI_LOGITS && big_logits(k)) {
+    if (wide_logits(k) && p.split)
+      return launch_wide<EPI_LOGITS>(k, wide_plan(k, p.split),
+                                     reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(p.split) + kSplitBytes), s);
+    return launch_big<EPI_LOGITS>(k, big_plan(k, p.split), s);
+  }
   if (p.epilogue == EPI_HEAD && big_head_candidate(k)) {
     const BigPlan pl = big_plan(k, p.split);
     if (pl.rem > 0) return launch_big<EPI_HEAD>(k, pl, s);

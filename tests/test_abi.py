@@ -122,11 +122,15 @@ def test_entry_points_reject_before_any_launch():
     assert lib.dartree_project(1, 8, 100, 65, 8, FAKE, FAKE, FAKE, 100, FAKE, None, 0, None) == D.ERR_UNSUPPORTED
     assert lib.dartree_project(1, 0, 100, 64, 8, FAKE, FAKE, FAKE, 100, FAKE, None, 0, None) == D.ERR_INVALID_ARG
     assert lib.dartree_project(1, 8, 100, 64, 8, FAKE + 2, FAKE, FAKE, 100, FAKE, None, 0, None) == D.ERR_INVALID_ARG
-    # split scratch: none for few rows or fp32, 64 MB for the 256x256-tile kernel's shapes
+    # split scratch: none for few rows or fp32; 64 MB of split partials for the
+    # many-row tilings, plus the node rows in fragment order for the 512-row
+    # tiles (row counts that are multiples of 512, as 1024)
     assert D.project_workspace_size(D.BF16, 64, 151936, 2560) == 0
     assert D.project_workspace_size(D.FP32, 1024, 151936, 2560) == 0
+    assert D.project_workspace_size(D.BF16, 768, 151936, 5120) == 256 * 256 * 256 * 4
+    assert D.project_workspace_size(D.BF16, 1000, 151936, 5120) == 256 * 256 * 256 * 4
     split = D.project_workspace_size(D.BF16, 1024, 151936, 5120)
-    assert split == 256 * 256 * 256 * 4
+    assert split == 256 * 256 * 256 * 4 + 1024 * 5120 * 2
     assert lib.dartree_project(1, 1024, 151936, 5120, 64, FAKE, FAKE, FAKE, 0, FAKE, None, 0, None) == D.ERR_WORKSPACE
     assert lib.dartree_project(1, 1024, 151936, 5120, 64, FAKE, FAKE, FAKE, 0, FAKE, FAKE, split - 1,
                                None) == D.ERR_WORKSPACE

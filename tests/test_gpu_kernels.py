@@ -76,13 +76,17 @@ def test_lse_topk(rows, vocab, k, T, dist):
     # 17..64 rows against a long vocabulary: 128-row blocks, 4 waves over K
     # (ragged: the last block runs past the vocabulary)
     (20, 65600, 320, 4), (33, 70000, 256, 11), (64, 66000, 512, 16),
-    # >= 512 rows against >= 16384 columns: the 256x256-tile kernel, ragged in both
+    # >= 512 rows against >= 16384 columns: the 512x128-tile kernel where the
+    # rows are a multiple of 512 (512, 1024, 2048), else the 256x256-tile one;
+    # ragged in the vocabulary, and in the rows for the 256x256 tiles
     (512, 16400, 256, 64), (600, 16390, 128, 75), (1024, 20000, 512, 64),
-    # one and three 64-deep K steps: every depth of the load pipeline's prologue
-    (512, 16384, 64, 64), (520, 16500, 192, 13),
-    # a last partial wave of tiles split along K (on 256 CUs: 60 tiles in 4
-    # pieces; 69 tiles in 3 pieces, ragged in M and N)
-    (1024, 20000, 1024, 64), (1030, 16400, 768, 103),
+    # one, three and five 64-deep K steps: every depth of the load pipelines'
+    # prologues, an odd step count (the 512-row kernel runs steps in pairs)
+    (512, 16384, 64, 64), (520, 16500, 192, 13), (2048, 16500, 320, 64),
+    # a last partial wave of tiles split along K (on 256 CUs, 512-row tiles:
+    # 58 tiles in 4 pieces of 4 steps, in 2 pieces of 5 steps; 256x256 tiles:
+    # 69 tiles in 3 pieces, ragged in M and N)
+    (1024, 20000, 1024, 64), (1024, 20000, 640, 32), (1030, 16400, 768, 103),
 ])
 def test_project_bf16_within_error_bound(rows, vocab, hidden, group):
     rng = np.random.default_rng(rows + vocab + hidden)
