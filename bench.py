@@ -129,9 +129,55 @@ def calibrate(torch, dev, U, stream, reps: int = 5) -> dict:
     blocks, iters = 256, 2048
     flops = D.calib_mfma(blocks, iters, sink)
     mfma_us = mean_us(lambda: D.calib_mfma(blocks, iters, sink))
-    return {"read_GBs": u_bytes / read_us / 1e3, "read_bytes": u_bytes,
-            "copy_GBs": 2 * src.numel() * 4 / copy_us / 1e3, "copy_bytes": src.numel() * 4,
-            "mfma_TFs": flops / mfma_us / 1e6}
+    out = {"read_GBs": u_bytes / read_us / 1e3, "read_bytes": u_bytes,
+           "copy_GBs": 2 * src.numel() * 4 / copy_us / 1e3, "copy_bytes": src.numel() * 4,
+           "mfma_TFs": flops / mfma_us / 1e6}
+    out.update(sync_costs(torch, dev, stream, reps))
+    return out
+
+
+def sync_costs(torch, dev, stream, reps: int = 5) -> dict:
+    """The two ways the steps of a round can be ordered, priced on this GPU
+    with one workgroup of 1024 threads per compute unit: the boundary between
+    consecutive launches replayed from a graph, and a grid-wide barrier
+    inside one launch (what a single persistent kernel per round would need)."""
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    n = 20
+    D.calib_empty(cus)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(n):
+            D.calib_empty(cus)
+    graph.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    launch = []
+    for _ in range(reps):
+        a.record(stream)
+        graph.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        launch.append(a.elapsed_time(b) * 1e3 / n)
+    counters = torch.zeros(D.CALIB_MAX_BARRIERS, dtype=torch.int32, device=dev)
+    fail = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def kernel_us(nbar):
+        ts = []
+        for _ in range(reps):
+            counters.zero_()
+            a.record(stream)
+            D.calib_grid_barrier(cus, nbar, counters, fail)
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b) * 1e3)
+        return float(np.mean(ts))
+
+    nbar = 16
+    t0, tn = kernel_us(0), kernel_us(nbar)
+    ok = int(fail.item()) == 0
+    return {"sync_blocks": cus, "launch_us": float(np.mean(launch)),
+            "grid_barrier_us": (tn - t0) / nbar if ok else None}
 
 
 def time_heap(torch, cfg, di, stream, steps: int, timed) -> dict:
@@ -558,8 +604,10 @@ def main() -> int:
     # achievable ceilings measured in this job: stream U once (the projection's
     # access pattern), copy 1 GiB, and a register-only MFMA loop
     cal = calibrate(torch, dev, di.U, stream)
+    gb = cal["grid_barrier_us"]
     log(f"calibration: read {cal['read_GBs']:.0f} GB/s, copy {cal['copy_GBs']:.0f} GB/s, "
-        f"mfma {cal['mfma_TFs']:.0f} TFLOP/s")
+        f"mfma {cal['mfma_TFs']:.0f} TFLOP/s; launch boundary {cal['launch_us']:.2f} us, grid barrier "
+        + (f"{gb:.2f} us" if gb is not None else "gave up"))
     meas = cal["mfma_TFs"] if roof["bound"] == "mfma" else cal["read_GBs"]
     roof["measured_peak"] = meas
     roof["frac_of_measured"] = roof["achieved"] / meas

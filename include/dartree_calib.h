@@ -11,6 +11,9 @@
  *   - a register-only loop of bf16 matrix-core instructions on pseudo-random
  *     operands (the sustained matrix-core rate depends on the operand bits:
  *     power limits the clock, and random operands draw the most).
+ * Two more price the ways kernels of one round can hand data to each other:
+ * the boundary between consecutive launches, and a grid-wide barrier inside
+ * one launch (the alternative of a single persistent kernel per round).
  * They compute nothing of the method.  Conventions as in dartree.h: caller-
  * owned device memory, work enqueued on `stream`, arguments validated before
  * anything is enqueued (DARTREE_ERR_INVALID_ARG otherwise).
@@ -44,6 +47,25 @@ dartree_status dartree_calib_copy(void* dst, const void* src, size_t bytes, hipS
  * Writes one value per workgroup to sink so the work is not eliminated.
  * blocks: 1 .. DARTREE_CALIB_SINK_FLOATS; iters: >= 1. */
 dartree_status dartree_calib_mfma(int32_t blocks, int32_t iters, float* sink, hipStream_t stream);
+
+/* Most barriers one dartree_calib_grid_barrier call passes. */
+#define DARTREE_CALIB_MAX_BARRIERS 64
+
+/* One kernel of `blocks` workgroups of 1024 threads that does nothing (a
+ * graph of such launches prices the boundary between consecutive kernels).
+ * blocks: 1 .. DARTREE_CALIB_SINK_FLOATS. */
+dartree_status dartree_calib_empty(int32_t blocks, hipStream_t stream);
+
+/* One kernel of `blocks` workgroups of 1024 threads passing `nbar` grid-wide
+ * barriers: at barrier i every workgroup adds 1 to counters[i] (device-scope
+ * atomic after a release fence) and polls it (relaxed loads, then an acquire
+ * fence) until it reads `blocks`.  blocks: 1 .. the current device's number
+ * of compute units, so that every workgroup is resident at once; nbar: 0 ..
+ * DARTREE_CALIB_MAX_BARRIERS.  counters: device, nbar words the caller set to
+ * zero beforehand.  A wait gives up after about 2^22 polls and sets *fail to
+ * 1 (device word; left unchanged otherwise), so the kernel always ends. */
+dartree_status dartree_calib_grid_barrier(int32_t blocks, int32_t nbar, uint32_t* counters, uint32_t* fail,
+                                          hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -1,5 +1,6 @@
 // Calibration kernels: a streaming read, a copy and a matrix-core-only loop,
-// the achievable ceilings for the HBM-bound and MFMA-bound kernels.
+// the achievable ceilings for the HBM-bound and MFMA-bound kernels; an empty
+// launch and a grid-wide barrier, the two ways to order a round's steps.
 #include "dartree_calib.h"
 #include "internal.hpp"
 
@@ -108,6 +109,34 @@ __global__ __launch_bounds__(kThreads) void calib_mfma(int iters, float* sink) {
   if (threadIdx.x == 0) sink[blockIdx.x] = red[0] + red[1] + red[2] + red[3];
 }
 
+__global__ __launch_bounds__(1024) void calib_empty(float* never) {
+  if (never && threadIdx.x == 0 && blockIdx.x == 0xFFFFFFFu) never[0] = 0.f;
+}
+
+// Grid-wide barriers among resident workgroups: one lane per workgroup
+// arrives (release fence, device-scope atomic add) and polls with relaxed
+// loads, so no cache invalidation repeats while it waits.
+constexpr uint32_t kMaxPolls = 1u << 22;
+__global__ __launch_bounds__(1024) void calib_grid_barrier(int nbar, uint32_t* counters, uint32_t* fail) {
+  for (int i = 0; i < nbar; ++i) {
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      __hip_atomic_fetch_add(counters + i, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      uint32_t polls = 0;
+      while (__hip_atomic_load(counters + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < gridDim.x) {
+        __builtin_amdgcn_s_sleep(1);
+        if (++polls >= kMaxPolls) {
+          __hip_atomic_store(fail, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
+  }
+  __syncthreads();
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Enough workgroups for several per CU on 256 CUs, within the sink.
@@ -146,6 +175,25 @@ dartree_status dartree_calib_copy(void* dst, const void* src, size_t bytes, hipS
 dartree_status dartree_calib_mfma(int32_t blocks, int32_t iters, float* sink, hipStream_t stream) {
   if (!sink || blocks < 1 || blocks > DARTREE_CALIB_SINK_FLOATS || iters < 1) return DARTREE_ERR_INVALID_ARG;
   hipLaunchKernelGGL(calib_mfma, dim3(unsigned(blocks)), dim3(kThreads), 0, stream, int(iters), sink);
+  return hipGetLastError() == hipSuccess ? DARTREE_OK : DARTREE_ERR_HIP;
+}
+
+dartree_status dartree_calib_empty(int32_t blocks, hipStream_t stream) {
+  if (blocks < 1 || blocks > DARTREE_CALIB_SINK_FLOATS) return DARTREE_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(calib_empty, dim3(unsigned(blocks)), dim3(1024), 0, stream, nullptr);
+  return hipGetLastError() == hipSuccess ? DARTREE_OK : DARTREE_ERR_HIP;
+}
+
+dartree_status dartree_calib_grid_barrier(int32_t blocks, int32_t nbar, uint32_t* counters, uint32_t* fail,
+                                          hipStream_t stream) {
+  if (blocks < 1 || nbar < 0 || nbar > DARTREE_CALIB_MAX_BARRIERS || !fail || (nbar > 0 && !counters))
+    return DARTREE_ERR_INVALID_ARG;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return DARTREE_ERR_HIP;
+  if (blocks > cus) return DARTREE_ERR_INVALID_ARG;   // not every workgroup could be resident
+  hipLaunchKernelGGL(calib_grid_barrier, dim3(unsigned(blocks)), dim3(1024), 0, stream, int(nbar), counters, fail);
   return hipGetLastError() == hipSuccess ? DARTREE_OK : DARTREE_ERR_HIP;
 }
 

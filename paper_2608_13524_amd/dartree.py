@@ -42,8 +42,10 @@ SYMBOLS = [
     "dartree_prune_levels", "dartree_candidate_sets_workspace_size", "dartree_candidate_sets",
     "dartree_heap_workspace_size", "dartree_build_tree_heap", "dartree_export_heap",
     "dartree_accept_walk", "dartree_tree_attention_workspace_size", "dartree_tree_attention",
-    "dartree_calib_read", "dartree_calib_copy", "dartree_calib_mfma",
+    "dartree_calib_read", "dartree_calib_copy", "dartree_calib_mfma", "dartree_calib_empty",
+    "dartree_calib_grid_barrier",
 ]
+CALIB_MAX_BARRIERS = 64
 CALIB_SINK_FLOATS = 4096
 
 
@@ -151,6 +153,8 @@ def lib() -> ctypes.CDLL:
     L.dartree_calib_read.argtypes = [vp, sz, vp, vp]
     L.dartree_calib_copy.argtypes = [vp, vp, sz, vp]
     L.dartree_calib_mfma.argtypes = [i32, i32, vp, vp]
+    L.dartree_calib_empty.argtypes = [i32, vp]
+    L.dartree_calib_grid_barrier.argtypes = [i32, i32, vp, vp, vp]
     for name in SYMBOLS:
         if name not in ("dartree_abi_version", "dartree_status_string"):
             getattr(L, name).restype = ctypes.c_int
@@ -478,6 +482,18 @@ def calib_mfma(blocks: int, iters: int, sink, stream=None) -> float:
     """Launch the MFMA-only loop; returns its flop count."""
     _check(lib().dartree_calib_mfma(blocks, iters, _ptr(sink), _stream(stream)), "dartree_calib_mfma")
     return float(blocks) * 4 * iters * 64 * (2 * 16 * 16 * 32)
+
+
+def calib_empty(blocks: int, stream=None) -> None:
+    """One launch of `blocks` workgroups that does nothing."""
+    _check(lib().dartree_calib_empty(blocks, _stream(stream)), "dartree_calib_empty")
+
+
+def calib_grid_barrier(blocks: int, nbar: int, counters, fail, stream=None) -> None:
+    """One launch passing `nbar` grid-wide barriers (counters: >= nbar zeroed
+    int32 words on the device; fail: one int32 word set to 1 if a wait gave up)."""
+    _check(lib().dartree_calib_grid_barrier(blocks, nbar, _ptr(counters) if nbar else None, _ptr(fail),
+                                            _stream(stream)), "dartree_calib_grid_barrier")
 
 
 def candidate_sets(logits, K: int, ids, ws=None, stream=None) -> None:

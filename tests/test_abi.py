@@ -22,7 +22,7 @@ def declared_symbols():
 
 def test_library_exports_every_declared_symbol():
     syms = declared_symbols()
-    assert len(syms) == 29, syms
+    assert len(syms) == 31, syms
     lib = D.lib()
     for s in syms:
         assert hasattr(lib, s), s
@@ -166,6 +166,14 @@ def test_calibration_kernels_reject_bad_arguments():
     assert lib.dartree_calib_copy(ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE + 4096), 1000, None) == D.ERR_INVALID_ARG
     assert lib.dartree_calib_copy(None, ctypes.c_void_p(FAKE), 1024, None) == D.ERR_INVALID_ARG
     assert lib.dartree_calib_mfma(0, 10, sink, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_empty(0, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_empty(D.CALIB_SINK_FLOATS + 1, None) == D.ERR_INVALID_ARG
+    cnt = ctypes.c_void_p(FAKE)
+    assert lib.dartree_calib_grid_barrier(0, 1, cnt, cnt, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_grid_barrier(8, -1, cnt, cnt, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_grid_barrier(8, D.CALIB_MAX_BARRIERS + 1, cnt, cnt, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_grid_barrier(8, 1, None, cnt, None) == D.ERR_INVALID_ARG
+    assert lib.dartree_calib_grid_barrier(8, 1, cnt, None, None) == D.ERR_INVALID_ARG
     assert lib.dartree_calib_mfma(D.CALIB_SINK_FLOATS + 1, 10, sink, None) == D.ERR_INVALID_ARG
     assert lib.dartree_calib_mfma(4, 0, sink, None) == D.ERR_INVALID_ARG
     assert lib.dartree_calib_mfma(4, 10, None, None) == D.ERR_INVALID_ARG
