@@ -313,6 +313,31 @@ def test_calibration_kernels():
     assert got[0] == got[1] == got[2]
 
 
+def test_sync_calibration_kernels():
+    """The launch and grid-barrier calibrations: every workgroup passes every
+    barrier (each counter ends at the number of workgroups, nothing gives up),
+    and a launch of empty workgroups completes."""
+    dev = device()
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    counters = torch.zeros(D.CALIB_MAX_BARRIERS, dtype=torch.int32, device=dev)
+    fail = torch.zeros(1, dtype=torch.int32, device=dev)
+    for blocks, nbar in ((1, 1), (cus, 3), (cus // 2, D.CALIB_MAX_BARRIERS)):
+        counters.zero_()
+        say(f"calib grid barrier blocks={blocks} nbar={nbar}")
+        D.calib_grid_barrier(blocks, nbar, counters, fail)
+        torch.cuda.synchronize()
+        assert int(fail.item()) == 0
+        got = counters.cpu().numpy()
+        assert (got[:nbar] == blocks).all() and (got[nbar:] == 0).all(), got[:8]
+    D.calib_grid_barrier(cus, 0, counters, fail)
+    say("calib empty launches")
+    for _ in range(3):
+        D.calib_empty(cus)
+    torch.cuda.synchronize()
+    with pytest.raises(D.DartreeError):
+        D.calib_grid_barrier(cus + 1, 1, counters, fail)   # not every workgroup could be resident
+
+
 @pytest.mark.parametrize("rows,vocab,K,dist", [
     (3, 151936, 64, "normal"), (2, 151936, 256, "ties"), (4, 20001, 17, "ties"), (2, 8193, 64, "normal"),
     (5, 100, 7, "ties"), (3, 8192, 1, "normal"), (2, 40, 40, "ties"),
