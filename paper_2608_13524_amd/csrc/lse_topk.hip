@@ -95,6 +95,106 @@ __device__ void fold_records(const float* recs, int nseg, int k, float scale, Pa
   }
 }
 
+// A segment of at most 4 kBlock CH values, held in registers after one pass
+// of loads.  Every thread's best (value desc, id asc) is a distinct element,
+// so the k-th best of those kBlock keys, T, is met or beaten by k elements of
+// the segment and its k best are among the keys >= T.  Only the k threads
+// whose best is >= T hold such keys, at most 4 CH each: they are compacted
+// and ranked by counting.  The (max, sum) pair is merged as in block_merge.
+// Writes the row's result (one segment) or the segment's record.
+template <int K, int CH, bool NTL>
+__device__ __forceinline__ void segment_in_registers(const float* zr, int v0, int v1, int nseg, int k, float tau,
+                                                     float scale, int64_t row, int seg, float* lse, float* cand_logp,
+                                                     int32_t* cand_ids, float* part) {
+  constexpr int kWaves = kBlock / 64;
+  constexpr int kCap = K * 4 * CH;
+  __shared__ __attribute__((aligned(16))) uint64_t tkey[kBlock];
+  __shared__ uint64_t cand[kCap];
+  __shared__ Partial sp[kWaves];
+  __shared__ uint64_t thr_s;
+  __shared__ int count;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  f32x4 x[CH];
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    const int v = v0 + 4 * tid + 4 * kBlock * c;
+    const f32x4* src = reinterpret_cast<const f32x4*>(zr + v);
+    x[c] = v < v1 ? (NTL ? __builtin_nontemporal_load(src) : *src) : f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+  }
+  float mx = -INFINITY;
+  uint64_t best = rank_key(-INFINITY, INT32_MAX);
+#pragma unroll
+  for (int c = 0; c < CH; ++c)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int v = v0 + 4 * tid + 4 * kBlock * c + i;
+      mx = fmaxf(mx, x[c][i]);
+      if (v < v1) best = max(best, rank_key(x[c][i], v));
+    }
+  Partial p{mx, 0.f};
+  if (mx > -INFINITY) {
+#pragma unroll
+    for (int c = 0; c < CH; ++c)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) p.s += __builtin_amdgcn_exp2f((x[c][i] - mx) * scale);
+  }
+  const Partial wp = wave_partial(p, scale);
+  if (lane == 0) sp[wave] = wp;
+  tkey[tid] = best;
+  if (tid == 0) {
+    count = 0;
+    thr_s = rank_key(-INFINITY, INT32_MAX);   // fewer than k threads hold values: take them all
+  }
+  __syncthreads();
+  // the k-th largest thread key (keys of threads holding values are distinct:
+  // one id each; the others hold the empty key, the least of all)
+  {
+    typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+    const u64x2* t2 = reinterpret_cast<const u64x2*>(tkey);
+    int rank = 0;
+#pragma unroll 8
+    for (int j = 0; j < kBlock / 2; ++j) {
+      const u64x2 o = t2[j];
+      rank += int(o.x > best) + int(o.y > best);
+    }
+    if (rank == k - 1) thr_s = best;
+  }
+  __syncthreads();
+  const uint64_t thr = thr_s;
+#pragma unroll
+  for (int c = 0; c < CH; ++c)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int v = v0 + 4 * tid + 4 * kBlock * c + i;
+      if (v < v1) {
+        const uint64_t key = rank_key(x[c][i], v);
+        if (key >= thr) cand[atomicAdd(&count, 1)] = key;
+      }
+    }
+  __syncthreads();
+  Partial q{-INFINITY, 0.f};
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) q = combine(q, sp[w], scale);  // fixed order
+  const int n = count;
+  constexpr int RF = record_floats<K>();
+  float* rec = part + (row * nseg + seg) * RF;
+  if (nseg > 1 && tid == 0) {
+    rec[0] = q.m;
+    rec[1] = q.s;
+  }
+  for (int t = tid; t < n; t += kBlock) {
+    const uint64_t key = cand[t];
+    int slot = 0;
+    for (int j = 0; j < n; ++j) slot += int(cand[j] > key);
+    if (nseg == 1) {
+      emit_row(row, q, key, slot, k, tau, lse, cand_logp, cand_ids);
+    } else if (slot < k) {
+      rec[4 + slot] = key_value(key);
+      rec[4 + K + slot] = __int_as_float(key_id(key));
+    }
+  }
+}
+
 // grid: rows * nseg blocks, block = row * nseg + segment.  One segment per
 // row writes the result directly; otherwise every block writes its segment's
 // record for lse_topk_merge.
@@ -117,6 +217,13 @@ __global__ __launch_bounds__(kBlock) void lse_topk_rows(const float* __restrict_
   const int tid = threadIdx.x;
 
   Partial p{-INFINITY, 0.f};
+  if constexpr (VEC && !NTL) {
+    if (v1 - v0 <= 4 * kBlock * CH) {
+      // the whole segment in one pass of loads (few rows: cache-resident z)
+      segment_in_registers<K, CH, NTL>(zr, v0, v1, nseg, k, tau, scale, row, seg, lse, cand_logp, cand_ids, part);
+      return;
+    }
+  }
   float tv[K];
   int ti[K];
 #pragma unroll

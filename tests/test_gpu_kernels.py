@@ -31,6 +31,8 @@ LSE_CASES = [
     (7, 151936, 16, 0.0, "ties"),
     (2, 40, 1, 0.0, "ties"),
     (4, 9, 9, 2.0, "normal"),           # k = V
+    # a segment held in registers where fewer than k threads hold values
+    (3, 16, 8, 1.0, "ties"), (2, 28, 8, 0.0, "normal"),
 ]
 
 
