@@ -6,10 +6,14 @@
 // [N][K] row-major (K contiguous), so one family of kernels serves both.
 //
 // bf16 path, gfx950 MFMA v_mfma_f32_16x16x32_bf16 (fp32 accumulation):
-//  * proj_bf16_stream: few rows (M <= 64).  The product is a stream over the
-//    weight matrix (U is 0.78-1.56 GB per depth, far beyond the caches), so
-//    every weight element is read once from HBM with coalesced non-temporal
-//    loads and staged through LDS into MFMA operand layout.
+//  * proj_bf16_stream: few rows (M <= 64; against the vocabulary M <= 16).
+//    The product is a stream over the weight matrix (U is 0.78-1.56 GB per
+//    depth, far beyond the caches), so every weight element is read once from
+//    HBM with coalesced non-temporal loads and staged through LDS into MFMA
+//    operand layout.
+//  * proj_bf16_sweep: 17..64 rows against the vocabulary.  One wave per run
+//    of weight tiles, accumulating them over the whole K loop; the weights
+//    and node rows stream into the wave's own LDS by buffer loads.
 //  * proj_bf16_big: many rows (>= 512) against the vocabulary, and the head at
 //    >= 512 rows when its tiles are too few to fill the chip.  256x256 tiles,
 //    8 waves in two groups alternating LDS reads and MFMAs, buffer loads
@@ -22,6 +26,8 @@
 // fp32 path: plain FMA loop (small problems only).
 
 #include <algorithm>
+#include <type_traits>
+#include <utility>
 
 #include "internal.hpp"
 
@@ -850,6 +856,203 @@ __global__ __launch_bounds__(512, 2) void proj_bf16_wide(KArgs a, int vec, BigPl
   }
 }
 
+// ---------------------------------------------------------------------------
+// 17..64 rows against the vocabulary: a sweep.  One wave per block; wave w
+// owns TPW consecutive 32-row weight tiles (rows 32 TPW w ..) and keeps their
+// accumulators over the whole K loop.  Every operand goes memory -> LDS by
+// buffer loads (nothing held in registers while in flight) into LDS private
+// to the wave: the weights through a ring of TPW + 1 stages of 32 rows x 64 k
+// (4 KB), in chunk-major order (c, t) = (0, 0) .. (0, TPW - 1), (1, 0) ..,
+// each stage filled one chunk (TPW stages) ahead; the node rows of a chunk
+// (MT x 32 rows x 64 k) into one of two slots, filled with the chunk before
+// and read into registers once for the chunk's TPW tiles.  Only the owning
+// wave reads its LDS, so each wait is the wave's own vmcnt: no barriers, and
+// no cross-wave reduction (the wave owns whole output columns).
+// The waits count only LDS fills: register loads can complete ahead of older
+// fills, so none is in flight during the stream.  Every counted fill reads
+// memory (rows past N or M repeat the last row), and the last chunk, which
+// has no fills of its own, waits for all.
+// v_mfma_f32_32x32x16_bf16 with A = node rows, B = weight rows: lane l holds
+// output column 32 t + l % 32, so each store instruction covers whole lines.
+// ---------------------------------------------------------------------------
+// f(integral_constant<int, I>) for each I of the sequence, in order
+template <class F, int... I>
+__device__ __forceinline__ void each_index(std::integer_sequence<int, I...>, F&& f) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+
+constexpr int kAuxNT = 2;   // cache policy of the weight fills: non-temporal
+// LDS of one wave: the weight ring and two node-row slots
+constexpr int sweep_lds_bytes(int MT, int TPW) { return (TPW + 1) * 4096 + 2 * MT * 4096; }
+
+template <int MT, int TPW, bool PRE>
+__global__ __launch_bounds__(64) void proj_bf16_sweep(KArgs a) {
+  constexpr int S = TPW + 1;   // the fill of stage s + TPW reuses stage s - 1's slot
+  static_assert(4 * TPW + 4 * MT <= 63, "vmcnt range");
+  __shared__ __attribute__((aligned(16))) uint16_t lds[sweep_lds_bytes(MT, TPW) / 2];
+  LDS_AS uint16_t* const ring = (LDS_AS uint16_t*)lds;
+  LDS_AS uint16_t* const xslots = ring + S * 2048;
+  const int lane = threadIdx.x, r32 = lane & 31, kh = lane >> 5;
+  const int M = a.M, N = a.N, K = a.K;
+  const int nk = K >> 6;
+  const int row0 = int(blockIdx.x) * (32 * TPW);
+  const int rows = min(32 * TPW, N - row0);
+  const unsigned rowb = unsigned(K * 2);
+  const uint16_t* Wt = static_cast<const uint16_t*>(a.w);
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(Wt + int64_t(row0) * K), (short)0, rows * K * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(a.x), (short)0, M * K * 2, 0x00020000);
+  // fill instruction i of a 32-row block: LDS rows 8 i + l / 8, 16-byte piece
+  // l % 8 of the row's 128 bytes stored at position (l % 8) ^ swz
+  // (conflict-free operand reads; rows 8 i + l / 8 and 8 (i + 2) + l / 8
+  // share the swizzle); source rows clamped to the last valid one
+  const int lrow = lane >> 3;
+  const unsigned pz0 = unsigned(((lane & 7) ^ swz16(lrow)) * 16), pz1 = unsigned(((lane & 7) ^ swz16(8 + lrow)) * 16);
+  const int sw = swz16(r32 & 15);
+
+  // bias of the four 4-row groups a lane stores per tile (rows 32 mt + 8 q +
+  // 4 kh + 0..3 share a bias row when rows_per_group % 4 == 0), loaded
+  // together, before the stream (PRE; waited for before its first fill) or
+  // after it (where the stream's registers are free)
+  const bool grp4 = a.rows_per_group % 4 == 0;
+  float bz[TPW][MT][4];
+  auto load_bias = [&](auto T0, auto T1) __attribute__((always_inline)) {
+    int gq[MT][4];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) gq[mt][q] = min(32 * mt + 8 * q + 4 * kh, M - 1) / a.rows_per_group;
+    if (a.group_index) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) gq[mt][q] = a.group_index[gq[mt][q]];
+    }
+#pragma unroll
+    for (int t = decltype(T0)::value; t < decltype(T1)::value; ++t)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          bz[t][mt][q] = a.bias_f32[int64_t(gq[mt][q]) * a.bias_stride + min(row0 + 32 * t + r32, N - 1)];
+  };
+  if constexpr (PRE) {
+    if (grp4) load_bias(std::integral_constant<int, 0>{}, std::integral_constant<int, TPW>{});
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  f32x16 acc[TPW][MT];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[t][mt][v] = 0.f;
+
+  // fill of the weight stage (c, t) into ring slot `slot`
+  auto fill = [&](int c, int t, int slot) __attribute__((always_inline)) {
+    const unsigned last = unsigned(rows - 1) * rowb;
+    LDS_AS uint16_t* base = ring + slot * 2048;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const unsigned r = unsigned(32 * t + 8 * i + lrow) * rowb;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (LDS_AS void*)(base + 512 * i), 16,
+                                               min(r, last) + ((i & 1) ? pz1 : pz0) + unsigned(c) * 128u, 0, 0, kAuxNT);
+    }
+  };
+  // fill of chunk c's node rows into slot c % 2
+  auto fill_x = [&](int c) __attribute__((always_inline)) {
+    LDS_AS uint16_t* base = xslots + (c & 1) * (MT * 2048);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS_AS void*)(base + mt * 2048 + 512 * i), 16,
+                                                 unsigned(min(32 * mt + 8 * i + lrow, M - 1)) * rowb +
+                                                     ((i & 1) ? pz1 : pz0) + unsigned(c) * 128u, 0, 0, 0);
+  };
+
+  // chunk 0 (its node rows, then its TPW stages into slots 0 .. TPW - 1)
+  fill_x(0);
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) fill(0, t, t);
+
+  u32x4 xf[MT][4];
+  int slot = 0;   // ring slot of the current stage
+  auto chunk = [&](int c, auto FILL) __attribute__((always_inline)) {
+    constexpr bool filling = decltype(FILL)::value;
+    each_index(std::make_integer_sequence<int, TPW>{}, [&](auto T) __attribute__((always_inline)) {
+      constexpr int t = decltype(T)::value;
+      if constexpr (filling) {
+        if constexpr (t == 0) fill_x(c + 1);
+        fill(c + 1, t, slot == 0 ? S - 1 : slot - 1);
+        // stage (c, t) (and chunk c's node rows, filled before it) landed:
+        // only the TPW weight fills and chunk c + 1's node rows issued since
+        // may be in flight
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * TPW + 4 * MT));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if constexpr (t == 0) {
+        const LDS_AS uint16_t* Xs = xslots + (c & 1) * (MT * 2048) + r32 * 64;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int sub = 0; sub < 4; ++sub)
+            xf[mt][sub] = *reinterpret_cast<const LDS_AS u32x4*>(Xs + mt * 2048 + (((2 * sub + kh) ^ sw) * 8));
+      }
+      const LDS_AS uint16_t* Sw = ring + slot * 2048 + r32 * 64;
+      bf16x8 uf[4];
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+        uf[sub] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const LDS_AS u32x4*>(Sw + (((2 * sub + kh) ^ sw) * 8)));
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          acc[t][mt] = mfma32(__builtin_bit_cast(bf16x8, xf[mt][sub]), uf[sub], acc[t][mt]);
+      slot = slot == S - 1 ? 0 : slot + 1;
+    });
+  };
+#pragma unroll 1
+  for (int c = 0; c + 1 < nk; ++c) chunk(c, std::true_type{});
+  // the last chunk was filled during the one before: wait for all of it
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  __builtin_amdgcn_sched_barrier(0);
+  chunk(nk - 1, std::false_type{});
+
+  // element v of acc[t][mt] in lane l: node row m = 32 mt + 8 (v / 4) +
+  // 4 (l / 32) + v % 4, weight row n = row0 + 32 t + l % 32
+  auto store = [&](auto T0, auto T1) __attribute__((always_inline)) {
+#pragma unroll
+    for (int t = decltype(T0)::value; t < decltype(T1)::value; ++t) {
+      const int n = row0 + 32 * t + r32;
+      if (n >= N) continue;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int m = 32 * mt + 8 * (v >> 2) + 4 * kh + (v & 3);
+          if (m >= M) continue;
+          const float b = grp4 ? bz[t][mt][v >> 2] : a.bias_f32[bias_base(a, m) + n];
+          __builtin_nontemporal_store(acc[t][mt][v] + b, a.out + int64_t(m) * N + n);
+        }
+    }
+  };
+  if constexpr (PRE) {
+    store(std::integral_constant<int, 0>{}, std::integral_constant<int, TPW>{});
+  } else {
+    // in two halves, each loading its bias values together
+    constexpr int H = (TPW + 1) / 2;
+    if (grp4) load_bias(std::integral_constant<int, 0>{}, std::integral_constant<int, H>{});
+    store(std::integral_constant<int, 0>{}, std::integral_constant<int, H>{});
+    if (grp4) load_bias(std::integral_constant<int, H>{}, std::integral_constant<int, TPW>{});
+    store(std::integral_constant<int, H>{}, std::integral_constant<int, TPW>{});
+  }
+}
+
 // The split wide tiles: 16 blocks per tile, each 32 rows x 128 columns.
 template <int EPI>
 __global__ __launch_bounds__(256) void proj_wide_fixup(KArgs a, int vec, BigPlan pl) {
@@ -999,6 +1202,39 @@ BigPlan big_plan(const KArgs& k, float* split) {
   return BigPlan{T - rem, rem, pieces, split};
 }
 
+// The sweep: waves per compute unit as the LDS allows (four at <= 32 node
+// rows, three at <= 64, where the node-row slots are twice as large), tiles
+// per wave so that all waves are resident at once (2 to 7).
+constexpr int sweep_waves_per_cu(int MT) { return MT == 1 ? 4 : 3; }
+
+template <int MT, int TPW>
+hipError_t launch_sweep(const KArgs& k, hipStream_t s) {
+  static_assert(sweep_waves_per_cu(MT) * sweep_lds_bytes(MT, TPW) <= 160 * 1024, "LDS of the resident waves");
+  const int tiles = (k.N + 31) / 32;
+  hipLaunchKernelGGL((proj_bf16_sweep<MT, TPW, MT == 1>), dim3((tiles + TPW - 1) / TPW), dim3(64), 0, s, k);
+  return hipGetLastError();
+}
+
+// Tiles per wave, 0 where more than 7 would be needed.
+int sweep_tpw(const KArgs& k, int MT) {
+  const int tiles = (k.N + 31) / 32;
+  const int slots = sweep_waves_per_cu(MT) * device_cus();
+  const int tpw = std::max(2, (tiles + slots - 1) / slots);
+  return tpw <= 7 ? tpw : 0;
+}
+
+template <int MT>
+hipError_t launch_sweep_tpw(const KArgs& k, int tpw, hipStream_t s) {
+  switch (tpw) {
+    case 2: return launch_sweep<MT, 2>(k, s);
+    case 3: return launch_sweep<MT, 3>(k, s);
+    case 4: return launch_sweep<MT, 4>(k, s);
+    case 5: return launch_sweep<MT, 5>(k, s);
+    case 6: return launch_sweep<MT, 6>(k, s);
+    default: return launch_sweep<MT, 7>(k, s);
+  }
+}
+
 template <int EPI>
 hipError_t launch_big(const KArgs& k, const BigPlan& pl, hipStream_t s) {
   const int vec = epilogue_vec_ok(k, EPI);
@@ -1067,6 +1303,11 @@ hipError_t launch_project(const ProjArgs& p, hipStream_t s) {
     if (p.epilogue == EPI_LOGITS) hipLaunchKernelGGL((proj_f32<EPI_LOGITS>), grid, dim3(256), 0, s, k, nblk_n);
     else hipLaunchKernelGGL((proj_f32<EPI_HEAD>), grid, dim3(256), 0, s, k, nblk_n);
     return hipGetLastError();
+  }
+  if (p.epilogue == EPI_LOGITS && k.M > 16 && k.M <= 64 && k.N >= 32 * 2048) {
+    const int mt = k.M <= 32 ? 1 : 2;
+    const int tpw = sweep_tpw(k, mt);
+    if (tpw > 0) return mt == 1 ? launch_sweep_tpw<1>(k, tpw, s) : launch_sweep_tpw<2>(k, tpw, s);
   }
   if (k.M <= 16) return launch_stream_nt<1>(k, p.epilogue, s);
   if (k.M <= 32) return launch_stream_nt<2>(k, p.epilogue, s);

@@ -75,9 +75,14 @@ def test_lse_topk(rows, vocab, k, T, dist):
     (1, 4099, 2560, 1), (8, 4099, 2560, 8), (13, 5000, 512, 5), (16, 151936, 2560, 8),
     (33, 3001, 1024, 11), (64, 4099, 4096, 16), (100, 4099, 512, 25), (128, 4103, 1024, 64),
     (200, 3000, 256, 50),
-    # 17..64 rows against a long vocabulary: 128-row blocks, 4 waves over K
-    # (ragged: the last block runs past the vocabulary)
+    # 17..64 rows against a long vocabulary: the sweep, one wave per run of
+    # 32-row weight tiles (on 256 CUs: 2, 3, 4 tiles per wave at <= 32 rows;
+    # 3, 5, 6 at <= 64); ragged last tile and last wave; 1 to 8 64-deep chunks
+    # (a single chunk has no fills ahead); groups of 4, 6, 8, 11 (per-element
+    # bias) and 16 rows
     (20, 65600, 320, 4), (33, 70000, 256, 11), (64, 66000, 512, 16),
+    (24, 65536, 192, 8), (18, 110000, 192, 6), (48, 100000, 128, 16), (40, 128300, 64, 8),
+    (1, 151936, 64, 1),
     # >= 512 rows against >= 16384 columns: the 512x128-tile kernel where the
     # rows are a multiple of 512 (512, 1024, 2048), else the 256x256-tile one;
     # ragged in the vocabulary, and in the rows for the 256x256 tiles
