@@ -279,6 +279,134 @@ __global__ __launch_bounds__(64 * KW) void proj_bf16_stream(KArgs a, int vec) {
 }
 
 // ---------------------------------------------------------------------------
+// At most 16 node rows against the vocabulary: blocks of 32 weight rows (two
+// 16-row tiles), KW waves splitting K into ranges of 128-deep pairs, partial
+// sums added through LDS in wave order.  A wave streams stages of 16 rows x
+// 128 k (one tile of one pair, 4 KB: every load instruction covers 4 rows x
+// 256 bytes, whole 256-byte row pieces, which stream from HBM faster than
+// 128-byte ones), two stages in flight in registers, each written to the
+// wave's private LDS slot (16 XOR-swizzled 16-byte positions per 256-byte
+// row, conflict-free both ways) and read back in MFMA operand layout for
+// v_mfma_f32_16x16x32_bf16 (A = 16 weight rows, B = the node rows).  The
+// result lane l holds D[n = 4 (l >> 4) + i][m = l & 15], i = 0..3.
+// ---------------------------------------------------------------------------
+template <int KW, int EPI>
+__global__ __launch_bounds__(64 * KW) void proj_bf16_pairs(KArgs a, int vec) {
+  constexpr int NT = 2;
+  constexpr int kSlotBytes = KW * 16 * 128 * 2;
+  constexpr int kRedBytes = KW * NT * 64 * 16;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[kSlotBytes > kRedBytes ? kSlotBytes : kRedBytes];
+  auto slot = reinterpret_cast<uint16_t(*)[16 * 128]>(smem);
+  auto red = reinterpret_cast<f32x4(*)[NT][64]>(smem);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int n0 = blockIdx.x * (16 * NT);
+  const int M = a.M, N = a.N, K = a.K;
+  const uint16_t* X = static_cast<const uint16_t*>(a.x);
+  const uint16_t* Wt = static_cast<const uint16_t*>(a.w);
+
+  // load instruction i of a stage: tile row 4 i + l / 16, 16-byte piece
+  // l % 16 of the row's 256 bytes, stored at position piece ^ row.  Rows
+  // past N are clamped to the last row: computed, never stored.
+  const uint16_t* wg[NT][4];
+  int woff[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 4 * i + kg;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) wg[nt][i] = Wt + int64_t(min(n0 + 16 * nt + row, N - 1)) * K + r16 * 8;
+    woff[i] = row * 128 + ((r16 ^ row) * 8);
+  }
+  // operand j (k = 32 j .. 32 j + 31 of the pair) of lane l: row l % 16,
+  // piece 4 j + l / 16
+  int roff[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) roff[j] = r16 * 128 + (((4 * j + kg) ^ r16) * 8);
+  const uint16_t* xp = X + int64_t(min(r16, M - 1)) * K + kg * 8;
+
+  // When every wave emits at most one 16x16 tile, its lanes fetch their
+  // bias values now, so the epilogue does not wait on a last dependent load.
+  constexpr bool kPre = NT <= KW;
+  f32x4 pre_b = f32x4{0.f, 0.f, 0.f, 0.f};
+  bool pre_ok = false;
+  if constexpr (kPre) {
+    if (wave < NT) {
+      const int m = r16, n = n0 + wave * 16 + kg * 4;
+      pre_ok = vec != 0 && m < M && n + 3 < N;
+      if (pre_ok) pre_b = bias4<EPI>(a, m, n);
+    }
+  }
+
+  // pairs [q0, q0 + np) of this wave
+  const int pairs = K >> 7;
+  const int per = (pairs + KW - 1) / KW;
+  const int q0 = min(pairs, wave * per);
+  const int np = min(pairs, q0 + per) - q0;
+  uint16_t* sl = slot[wave];
+
+  f32x4 acc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  u32x4 R[NT][4], XN[4], XR[4];
+  // stage (q, nt): tile nt's rows of pair q (and with tile 0, the pair's node rows)
+  auto fetch = [&](int q, auto NTc) __attribute__((always_inline)) {
+    constexpr int nt = decltype(NTc)::value;
+    const int k = q * 128;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) R[nt][i] = ld_stream(wg[nt][i] + k);
+    if constexpr (nt == 0) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) XN[j] = ld_cached(xp + k + 32 * j);
+    }
+  };
+  auto stage = [&](int q, auto NTc, bool more) __attribute__((always_inline)) {
+    constexpr int nt = decltype(NTc)::value;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(sl + woff[i]) = R[nt][i];
+    if constexpr (nt == 0) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) XR[j] = XN[j];
+    }
+    if (more) fetch(q + 1, NTc);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bf16x8 av = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(sl + roff[j]));
+      acc[nt] = mfma16(av, __builtin_bit_cast(bf16x8, XR[j]), acc[nt]);
+    }
+  };
+  if (np > 0) {
+    fetch(q0, std::integral_constant<int, 0>{});
+    fetch(q0, std::integral_constant<int, 1>{});
+    // every pair but the last fetches the next one (the loads are the same
+    // on every pass, so the compiler's waits keep two stages in flight)
+#pragma unroll 1
+    for (int q = q0; q + 1 < q0 + np; ++q) {
+      stage(q, std::integral_constant<int, 0>{}, true);
+      stage(q, std::integral_constant<int, 1>{}, true);
+    }
+    stage(q0 + np - 1, std::integral_constant<int, 0>{}, false);
+    stage(q0 + np - 1, std::integral_constant<int, 1>{}, false);
+  }
+
+  __syncthreads();  // every wave is done with its slot before the sums reuse the memory
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) red[wave][nt][lane] = acc[nt];
+  __syncthreads();
+
+  for (int nt = wave; nt < NT; nt += KW) {
+    f32x4 v = red[0][nt][lane];
+#pragma unroll
+    for (int w = 1; w < KW; ++w) v += red[w][nt][lane];
+    const int m = r16;
+    if (m < M) {
+      if (kPre && pre_ok) emit4_bias<EPI>(a, m, n0 + nt * 16 + kg * 4, v, pre_b);
+      else emit4<EPI>(a, m, n0 + nt * 16 + kg * 4, v, vec != 0);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Many rows: 128x128 output tile per block, K in steps of 64 through
 // double-buffered LDS.  Rows are padded to 72 bf16 (144 B) so that the 16-byte
 // operand reads of 16 consecutive rows fall in distinct LDS banks.
@@ -1142,6 +1270,13 @@ hipError_t launch_stream(const KArgs& k, int epi, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int KW>
+hipError_t launch_pairs(const KArgs& k, hipStream_t s) {
+  const dim3 grid((k.N + 31) / 32);
+  hipLaunchKernelGGL((proj_bf16_pairs<KW, EPI_LOGITS>), grid, dim3(64 * KW), 0, s, k, epilogue_vec_ok(k, EPI_LOGITS));
+  return hipGetLastError();
+}
+
 template <int MT>
 hipError_t launch_stream_nt(const KArgs& k, int epi, hipStream_t s) {
   // Long weight matrices (the vocabulary): 32-row blocks, 8 waves over K at
@@ -1153,6 +1288,7 @@ hipError_t launch_stream_nt(const KArgs& k, int epi, hipStream_t s) {
   // to keep HBM busy.
   if (k.N >= 32 * 2048) {
     if constexpr (MT >= 2) return launch_stream<MT, 8, 4, 1>(k, epi, s);
+    if (k.K % 128 == 0 && epi == EPI_LOGITS) return launch_pairs<4>(k, s);
     return launch_stream<MT, 2, 8, 2>(k, epi, s);
   }
   if constexpr (MT <= 2) return launch_stream<MT, 1, 16, 2>(k, epi, s);

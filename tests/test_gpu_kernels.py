@@ -83,6 +83,9 @@ def test_lse_topk(rows, vocab, k, T, dist):
     (20, 65600, 320, 4), (33, 70000, 256, 11), (64, 66000, 512, 16),
     (24, 65536, 192, 8), (18, 110000, 192, 6), (48, 100000, 128, 16), (40, 128300, 64, 8),
     (1, 151936, 64, 1),
+    # <= 16 rows against a long vocabulary, K a multiple of 128: 128-deep
+    # chunk pairs, 4 waves over K (some waves with no pairs; one pair)
+    (5, 70001, 384, 5), (12, 100003, 1152, 4), (9, 65536, 128, 3),
     # >= 512 rows against >= 16384 columns: the 512x128-tile kernel where the
     # rows are a multiple of 512 (512, 1024, 2048), else the 256x256-tile one;
     # ragged in the vocabulary, and in the rows for the 256x256 tiles
