@@ -986,22 +986,25 @@ __global__ __launch_bounds__(512, 2) void proj_bf16_wide(KArgs a, int vec, BigPl
 
 // ---------------------------------------------------------------------------
 // 17..64 rows against the vocabulary: a sweep.  One wave per block; wave w
-// owns TPW consecutive 32-row weight tiles (rows 32 TPW w ..) and keeps their
+// owns TPW consecutive 16-row weight tiles (rows 16 TPW w ..) and keeps their
 // accumulators over the whole K loop.  Every operand goes memory -> LDS by
 // buffer loads (nothing held in registers while in flight) into LDS private
-// to the wave: the weights through a ring of TPW + 1 stages of 32 rows x 64 k
-// (4 KB), in chunk-major order (c, t) = (0, 0) .. (0, TPW - 1), (1, 0) ..,
-// each stage filled one chunk (TPW stages) ahead; the node rows of a chunk
-// (MT x 32 rows x 64 k) into one of two slots, filled with the chunk before
-// and read into registers once for the chunk's TPW tiles.  Only the owning
-// wave reads its LDS, so each wait is the wave's own vmcnt: no barriers, and
-// no cross-wave reduction (the wave owns whole output columns).
+// to the wave: the weights through a ring of AHEAD + 1 stages of 16 rows x
+// 128 k (4 KB; each load instruction covers 4 rows x 256 bytes, whole
+// 256-byte row pieces, which stream from HBM faster than 128-byte ones), in
+// chunk-major order (c, t) = (0, 0) .. (0, TPW - 1), (1, 0) .., AHEAD < TPW
+// stages in flight; the node rows of a chunk (MT x 16 rows x 128 k) into one
+// slot, read into registers at the chunk's first stage (they serve its TPW
+// tiles) and refilled with the next chunk's at step TPW - AHEAD.  Only the
+// owning wave reads its LDS, so each wait is the wave's own vmcnt: no
+// barriers, and no cross-wave reduction (the wave owns whole outputs).
 // The waits count only LDS fills: register loads can complete ahead of older
-// fills, so none is in flight during the stream.  Every counted fill reads
-// memory (rows past N or M repeat the last row), and the last chunk, which
-// has no fills of its own, waits for all.
-// v_mfma_f32_32x32x16_bf16 with A = node rows, B = weight rows: lane l holds
-// output column 32 t + l % 32, so each store instruction covers whole lines.
+// fills, so none is in flight during the stream.  Every fill reads memory
+// (rows past N or M repeat the last row), and the last chunk issues only the
+// fills of its own stages, with its waits counted to match.
+// LDS rows are 256 bytes, 16-byte piece p of row r stored at position p ^ r
+// (conflict-free both ways).  v_mfma_f32_16x16x32_bf16 with A = 16 weight
+// rows, B = 16 node rows: lane l holds D[n = 4 (l >> 4) + i][m = l & 15].
 // ---------------------------------------------------------------------------
 // f(integral_constant<int, I>) for each I of the sequence, in order
 template <class F, int... I>
@@ -1010,74 +1013,44 @@ __device__ __forceinline__ void each_index(std::integer_sequence<int, I...>, F&&
 }
 
 constexpr int kAuxNT = 2;   // cache policy of the weight fills: non-temporal
-// LDS of one wave: the weight ring and two node-row slots
-constexpr int sweep_lds_bytes(int MT, int TPW) { return (TPW + 1) * 4096 + 2 * MT * 4096; }
+// LDS of one wave: the weight ring and the node-row slot
+constexpr int sweep_lds_bytes(int MT, int AHEAD) { return (AHEAD + 1) * 4096 + MT * 4096; }
 
-template <int MT, int TPW, bool PRE>
+template <int MT, int TPW, int AHEAD>
 __global__ __launch_bounds__(64) void proj_bf16_sweep(KArgs a) {
-  constexpr int S = TPW + 1;   // the fill of stage s + TPW reuses stage s - 1's slot
-  static_assert(4 * TPW + 4 * MT <= 63, "vmcnt range");
-  __shared__ __attribute__((aligned(16))) uint16_t lds[sweep_lds_bytes(MT, TPW) / 2];
+  constexpr int S = AHEAD + 1;       // the fill of stage s + AHEAD reuses stage s - 1's slot
+  constexpr int TX = TPW - AHEAD;    // step of a chunk that fills the next chunk's node rows
+  static_assert(TX >= 1, "the node-row slot is refilled after its chunk's first step");
+  static_assert(4 * AHEAD + 4 * MT <= 63, "vmcnt range");
+  __shared__ __attribute__((aligned(16))) uint16_t lds[sweep_lds_bytes(MT, AHEAD) / 2];
   LDS_AS uint16_t* const ring = (LDS_AS uint16_t*)lds;
-  LDS_AS uint16_t* const xslots = ring + S * 2048;
-  const int lane = threadIdx.x, r32 = lane & 31, kh = lane >> 5;
+  LDS_AS uint16_t* const xslot = ring + S * 2048;
+  const int lane = threadIdx.x, r16 = lane & 15, kg = lane >> 4;
   const int M = a.M, N = a.N, K = a.K;
-  const int nk = K >> 6;
-  const int row0 = int(blockIdx.x) * (32 * TPW);
-  const int rows = min(32 * TPW, N - row0);
+  const int nk = K >> 7;
+  const int row0 = int(blockIdx.x) * (16 * TPW);
+  const int rows = min(16 * TPW, N - row0);
   const unsigned rowb = unsigned(K * 2);
   const uint16_t* Wt = static_cast<const uint16_t*>(a.w);
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(Wt + int64_t(row0) * K), (short)0, rows * K * 2, 0x00020000);
   const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(a.x), (short)0, M * K * 2, 0x00020000);
-  // fill instruction i of a 32-row block: LDS rows 8 i + l / 8, 16-byte piece
-  // l % 8 of the row's 128 bytes stored at position (l % 8) ^ swz
-  // (conflict-free operand reads; rows 8 i + l / 8 and 8 (i + 2) + l / 8
-  // share the swizzle); source rows clamped to the last valid one
-  const int lrow = lane >> 3;
-  const unsigned pz0 = unsigned(((lane & 7) ^ swz16(lrow)) * 16), pz1 = unsigned(((lane & 7) ^ swz16(8 + lrow)) * 16);
-  const int sw = swz16(r32 & 15);
+  // fill instruction i of a 16-row block: LDS row 4 i + l / 16, position
+  // l % 16, holding the row's piece (l % 16) ^ row; source rows clamped to
+  // the last valid one
+  const unsigned pz = unsigned((r16 ^ kg) * 16);   // for row 4 i + kg: (l % 16) ^ (4 i + kg) = pz ^ 4 i
+  // operand j (k = 32 j .. 32 j + 31 of a chunk) of lane l: row l % 16,
+  // piece 4 j + l / 16
+  int roff[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) roff[j] = r16 * 128 + (((4 * j + kg) ^ r16) * 8);
 
-  // bias of the four 4-row groups a lane stores per tile (rows 32 mt + 8 q +
-  // 4 kh + 0..3 share a bias row when rows_per_group % 4 == 0), loaded
-  // together, before the stream (PRE; waited for before its first fill) or
-  // after it (where the stream's registers are free)
-  const bool grp4 = a.rows_per_group % 4 == 0;
-  float bz[TPW][MT][4];
-  auto load_bias = [&](auto T0, auto T1) __attribute__((always_inline)) {
-    int gq[MT][4];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) gq[mt][q] = min(32 * mt + 8 * q + 4 * kh, M - 1) / a.rows_per_group;
-    if (a.group_index) {
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) gq[mt][q] = a.group_index[gq[mt][q]];
-    }
-#pragma unroll
-    for (int t = decltype(T0)::value; t < decltype(T1)::value; ++t)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          bz[t][mt][q] = a.bias_f32[int64_t(gq[mt][q]) * a.bias_stride + min(row0 + 32 * t + r32, N - 1)];
-  };
-  if constexpr (PRE) {
-    if (grp4) load_bias(std::integral_constant<int, 0>{}, std::integral_constant<int, TPW>{});
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-    __builtin_amdgcn_sched_barrier(0);
-  }
-
-  f32x16 acc[TPW][MT];
+  f32x4 acc[TPW][MT];
 #pragma unroll
   for (int t = 0; t < TPW; ++t)
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[t][mt][v] = 0.f;
+    for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // fill of the weight stage (c, t) into ring slot `slot`
   auto fill = [&](int c, int t, int slot) __attribute__((always_inline)) {
@@ -1085,100 +1058,109 @@ __global__ __launch_bounds__(64) void proj_bf16_sweep(KArgs a) {
     LDS_AS uint16_t* base = ring + slot * 2048;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const unsigned r = unsigned(32 * t + 8 * i + lrow) * rowb;
+      const unsigned r = unsigned(16 * t + 4 * i + kg) * rowb;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (LDS_AS void*)(base + 512 * i), 16,
-                                               min(r, last) + ((i & 1) ? pz1 : pz0) + unsigned(c) * 128u, 0, 0, kAuxNT);
+                                               min(r, last) + (pz ^ unsigned(64 * i)) + unsigned(c) * 256u, 0, 0, kAuxNT);
     }
   };
-  // fill of chunk c's node rows into slot c % 2
+  // fill of chunk c's node rows into the slot
   auto fill_x = [&](int c) __attribute__((always_inline)) {
-    LDS_AS uint16_t* base = xslots + (c & 1) * (MT * 2048);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS_AS void*)(base + mt * 2048 + 512 * i), 16,
-                                                 unsigned(min(32 * mt + 8 * i + lrow, M - 1)) * rowb +
-                                                     ((i & 1) ? pz1 : pz0) + unsigned(c) * 128u, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS_AS void*)(xslot + mt * 2048 + 512 * i), 16,
+                                                 unsigned(min(16 * mt + 4 * i + kg, M - 1)) * rowb +
+                                                     (pz ^ unsigned(64 * i)) + unsigned(c) * 256u, 0, 0, 0);
   };
 
-  // chunk 0 (its node rows, then its TPW stages into slots 0 .. TPW - 1)
+  // chunk 0's node rows, then its first AHEAD stages into slots 0 .. AHEAD - 1
   fill_x(0);
 #pragma unroll
-  for (int t = 0; t < TPW; ++t) fill(0, t, t);
+  for (int t = 0; t < AHEAD; ++t) fill(0, t, t);
 
   u32x4 xf[MT][4];
   int slot = 0;   // ring slot of the current stage
-  auto chunk = [&](int c, auto FILL) __attribute__((always_inline)) {
-    constexpr bool filling = decltype(FILL)::value;
+  // LAST: the last chunk, which fills only its own stages
+  auto chunk = [&](int c, auto LAST) __attribute__((always_inline)) {
+    constexpr bool last = decltype(LAST)::value;
     each_index(std::make_integer_sequence<int, TPW>{}, [&](auto T) __attribute__((always_inline)) {
       constexpr int t = decltype(T)::value;
-      if constexpr (filling) {
-        if constexpr (t == 0) fill_x(c + 1);
-        fill(c + 1, t, slot == 0 ? S - 1 : slot - 1);
-        // stage (c, t) (and chunk c's node rows, filled before it) landed:
-        // only the TPW weight fills and chunk c + 1's node rows issued since
-        // may be in flight
-        __builtin_amdgcn_sched_barrier(0);
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * TPW + 4 * MT));
-        __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_sched_barrier(0);   // the last step's operand reads stay ahead of this step's fills
+      if constexpr (!last) {
+        if constexpr (t == TX) {
+          __builtin_amdgcn_s_waitcnt(0xC07F);   // chunk c's node rows are in registers: lgkmcnt(0)
+          fill_x(c + 1);
+        }
+        fill(c + (t + AHEAD) / TPW, (t + AHEAD) % TPW, slot == 0 ? S - 1 : slot - 1);
+      } else if constexpr (t + AHEAD < TPW) {
+        fill(c, t + AHEAD, slot == 0 ? S - 1 : slot - 1);
       }
+      // stage (c, t) (and chunk c's node rows, filled before it) landed: only
+      // the fills issued after it may be in flight
+      constexpr int after = last ? 4 * (AHEAD < TPW - 1 - t ? AHEAD : TPW - 1 - t)
+                                 : 4 * AHEAD + (t >= TX ? 4 * MT : 0);
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(after));
+      __builtin_amdgcn_sched_barrier(0);
       if constexpr (t == 0) {
-        const LDS_AS uint16_t* Xs = xslots + (c & 1) * (MT * 2048) + r32 * 64;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int sub = 0; sub < 4; ++sub)
-            xf[mt][sub] = *reinterpret_cast<const LDS_AS u32x4*>(Xs + mt * 2048 + (((2 * sub + kh) ^ sw) * 8));
+          for (int j = 0; j < 4; ++j)
+            xf[mt][j] = *reinterpret_cast<const LDS_AS u32x4*>(xslot + mt * 2048 + roff[j]);
       }
-      const LDS_AS uint16_t* Sw = ring + slot * 2048 + r32 * 64;
-      bf16x8 uf[4];
+      const LDS_AS uint16_t* Sw = ring + slot * 2048;
 #pragma unroll
-      for (int sub = 0; sub < 4; ++sub)
-        uf[sub] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const LDS_AS u32x4*>(Sw + (((2 * sub + kh) ^ sw) * 8)));
+      for (int j = 0; j < 4; ++j) {
+        const bf16x8 uf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const LDS_AS u32x4*>(Sw + roff[j]));
 #pragma unroll
-      for (int sub = 0; sub < 4; ++sub)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-          acc[t][mt] = mfma32(__builtin_bit_cast(bf16x8, xf[mt][sub]), uf[sub], acc[t][mt]);
+        for (int mt = 0; mt < MT; ++mt) acc[t][mt] = mfma16(uf, __builtin_bit_cast(bf16x8, xf[mt][j]), acc[t][mt]);
+      }
       slot = slot == S - 1 ? 0 : slot + 1;
     });
   };
 #pragma unroll 1
-  for (int c = 0; c + 1 < nk; ++c) chunk(c, std::true_type{});
-  // the last chunk was filled during the one before: wait for all of it
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-  __builtin_amdgcn_sched_barrier(0);
-  chunk(nk - 1, std::false_type{});
+  for (int c = 0; c + 1 < nk; ++c) chunk(c, std::false_type{});
+  chunk(nk - 1, std::true_type{});
 
-  // element v of acc[t][mt] in lane l: node row m = 32 mt + 8 (v / 4) +
-  // 4 (l / 32) + v % 4, weight row n = row0 + 32 t + l % 32
+  // lane l holds, of tile t and node tile mt, node row m = 16 mt + l % 16
+  // and weight rows n = row0 + 16 t + 4 (l / 16) + 0..3; the bias values of
+  // a half of the tiles are loaded together, then that half is stored
   auto store = [&](auto T0, auto T1) __attribute__((always_inline)) {
+    constexpr int t0 = decltype(T0)::value, t1 = decltype(T1)::value;
+    const bool vec = reinterpret_cast<uintptr_t>(a.bias_f32) % 16 == 0 && a.bias_stride % 4 == 0 && N % 4 == 0 &&
+                     reinterpret_cast<uintptr_t>(a.out) % 16 == 0;
+    int64_t bb[MT];
 #pragma unroll
-    for (int t = decltype(T0)::value; t < decltype(T1)::value; ++t) {
-      const int n = row0 + 32 * t + r32;
-      if (n >= N) continue;
+    for (int mt = 0; mt < MT; ++mt) bb[mt] = bias_base(a, min(16 * mt + r16, M - 1));
+    f32x4 bz[t1 - t0][MT];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+    for (int t = t0; t < t1; ++t)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int m = 32 * mt + 8 * (v >> 2) + 4 * kh + (v & 3);
-          if (m >= M) continue;
-          const float b = grp4 ? bz[t][mt][v >> 2] : a.bias_f32[bias_base(a, m) + n];
-          __builtin_nontemporal_store(acc[t][mt][v] + b, a.out + int64_t(m) * N + n);
+      for (int mt = 0; mt < MT; ++mt) {
+        const int n = min(row0 + 16 * t + 4 * kg, N - 4);
+        bz[t - t0][mt] = vec ? *reinterpret_cast<const f32x4*>(a.bias_f32 + bb[mt] + n) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+    for (int t = t0; t < t1; ++t)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = 16 * mt + r16, n = row0 + 16 * t + 4 * kg;
+        if (m >= M || n >= N) continue;
+        const f32x4 v = acc[t][mt];
+        if (vec && n + 3 < N) {
+          __builtin_nontemporal_store(v + bz[t - t0][mt], reinterpret_cast<f32x4*>(a.out + int64_t(m) * N + n));
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (n + i < N) __builtin_nontemporal_store(v[i] + a.bias_f32[bb[mt] + n + i], a.out + int64_t(m) * N + n + i);
         }
-    }
+      }
   };
-  if constexpr (PRE) {
-    store(std::integral_constant<int, 0>{}, std::integral_constant<int, TPW>{});
-  } else {
-    // in two halves, each loading its bias values together
-    constexpr int H = (TPW + 1) / 2;
-    if (grp4) load_bias(std::integral_constant<int, 0>{}, std::integral_constant<int, H>{});
-    store(std::integral_constant<int, 0>{}, std::integral_constant<int, H>{});
-    if (grp4) load_bias(std::integral_constant<int, H>{}, std::integral_constant<int, TPW>{});
-    store(std::integral_constant<int, H>{}, std::integral_constant<int, TPW>{});
-  }
+  constexpr int H = (TPW + 1) / 2;
+  store(std::integral_constant<int, 0>{}, std::integral_constant<int, H>{});
+  store(std::integral_constant<int, H>{}, std::integral_constant<int, TPW>{});
 }
 
 // The split wide tiles: 16 blocks per tile, each 32 rows x 128 columns.
@@ -1339,35 +1321,40 @@ BigPlan big_plan(const KArgs& k, float* split) {
 }
 
 // The sweep: waves per compute unit as the LDS allows (four at <= 32 node
-// rows, three at <= 64, where the node-row slots are twice as large), tiles
-// per wave so that all waves are resident at once (2 to 7).
-constexpr int sweep_waves_per_cu(int MT) { return MT == 1 ? 4 : 3; }
+// rows, three at <= 64, where the node-row slot is twice as large), tiles per
+// wave (of the instantiated counts) so that all waves are resident at once.
+constexpr int sweep_waves_per_cu(int MT) { return MT == 2 ? 4 : 3; }
+constexpr int sweep_ahead(int MT, int TPW) { return (MT == 2 ? 7 : 8) < TPW - 1 ? (MT == 2 ? 7 : 8) : TPW - 1; }
 
 template <int MT, int TPW>
 hipError_t launch_sweep(const KArgs& k, hipStream_t s) {
-  static_assert(sweep_waves_per_cu(MT) * sweep_lds_bytes(MT, TPW) <= 160 * 1024, "LDS of the resident waves");
-  const int tiles = (k.N + 31) / 32;
-  hipLaunchKernelGGL((proj_bf16_sweep<MT, TPW, MT == 1>), dim3((tiles + TPW - 1) / TPW), dim3(64), 0, s, k);
+  constexpr int AHEAD = sweep_ahead(MT, TPW);
+  static_assert(sweep_waves_per_cu(MT) * sweep_lds_bytes(MT, AHEAD) <= 160 * 1024, "LDS of the resident waves");
+  const int tiles = (k.N + 15) / 16;
+  hipLaunchKernelGGL((proj_bf16_sweep<MT, TPW, AHEAD>), dim3((tiles + TPW - 1) / TPW), dim3(64), 0, s, k);
   return hipGetLastError();
 }
 
-// Tiles per wave, 0 where more than 7 would be needed.
+// The instantiated tile count to use (the least one not below the need), 0
+// where none is large enough.
 int sweep_tpw(const KArgs& k, int MT) {
-  const int tiles = (k.N + 31) / 32;
+  const int tiles = (k.N + 15) / 16;
   const int slots = sweep_waves_per_cu(MT) * device_cus();
-  const int tpw = std::max(2, (tiles + slots - 1) / slots);
-  return tpw <= 7 ? tpw : 0;
+  const int need = (tiles + slots - 1) / slots;
+  for (int t : {4, 6, 8, 10, 13, 16})
+    if (t >= need) return t;
+  return 0;
 }
 
 template <int MT>
 hipError_t launch_sweep_tpw(const KArgs& k, int tpw, hipStream_t s) {
   switch (tpw) {
-    case 2: return launch_sweep<MT, 2>(k, s);
-    case 3: return launch_sweep<MT, 3>(k, s);
     case 4: return launch_sweep<MT, 4>(k, s);
-    case 5: return launch_sweep<MT, 5>(k, s);
     case 6: return launch_sweep<MT, 6>(k, s);
-    default: return launch_sweep<MT, 7>(k, s);
+    case 8: return launch_sweep<MT, 8>(k, s);
+    case 10: return launch_sweep<MT, 10>(k, s);
+    case 13: return launch_sweep<MT, 13>(k, s);
+    default: return launch_sweep<MT, 16>(k, s);
   }
 }
 
@@ -1440,10 +1427,10 @@ hipError_t launch_project(const ProjArgs& p, hipStream_t s) {
     else hipLaunchKernelGGL((proj_f32<EPI_HEAD>), grid, dim3(256), 0, s, k, nblk_n);
     return hipGetLastError();
   }
-  if (p.epilogue == EPI_LOGITS && k.M > 16 && k.M <= 64 && k.N >= 32 * 2048) {
-    const int mt = k.M <= 32 ? 1 : 2;
+  if (p.epilogue == EPI_LOGITS && k.M > 16 && k.M <= 64 && k.N >= 32 * 2048 && k.K % 128 == 0) {
+    const int mt = k.M <= 32 ? 2 : 4;
     const int tpw = sweep_tpw(k, mt);
-    if (tpw > 0) return mt == 1 ? launch_sweep_tpw<1>(k, tpw, s) : launch_sweep_tpw<2>(k, tpw, s);
+    if (tpw > 0) return mt == 2 ? launch_sweep_tpw<2>(k, tpw, s) : launch_sweep_tpw<4>(k, tpw, s);
   }
   if (k.M <= 16) return launch_stream_nt<1>(k, p.epilogue, s);
   if (k.M <= 32) return launch_stream_nt<2>(k, p.epilogue, s);
