@@ -1320,11 +1320,13 @@ BigPlan big_plan(const KArgs& k, float* split) {
   return BigPlan{T - rem, rem, pieces, split};
 }
 
-// The sweep: waves per compute unit as the LDS allows (four at <= 32 node
-// rows, three at <= 64, where the node-row slot is twice as large), tiles per
-// wave (of the instantiated counts) so that all waves are resident at once.
-constexpr int sweep_waves_per_cu(int MT) { return MT == 2 ? 4 : 3; }
-constexpr int sweep_ahead(int MT, int TPW) { return (MT == 2 ? 7 : 8) < TPW - 1 ? (MT == 2 ? 7 : 8) : TPW - 1; }
+// The sweep: three waves per compute unit (measured at 32 rows x 151936:
+// 13 tiles per wave with 9 stages ahead 128.3-128.9 us, 10 tiles with four
+// waves per CU 131-133 us), tiles per wave (of the instantiated counts) so
+// that all waves are resident at once, stages ahead as the LDS of three
+// waves allows.
+constexpr int sweep_waves_per_cu(int) { return 3; }
+constexpr int sweep_ahead(int MT, int TPW) { return (MT == 2 ? 9 : 8) < TPW - 1 ? (MT == 2 ? 9 : 8) : TPW - 1; }
 
 template <int MT, int TPW>
 hipError_t launch_sweep(const KArgs& k, hipStream_t s) {

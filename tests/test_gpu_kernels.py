@@ -75,13 +75,16 @@ def test_lse_topk(rows, vocab, k, T, dist):
     (1, 4099, 2560, 1), (8, 4099, 2560, 8), (13, 5000, 512, 5), (16, 151936, 2560, 8),
     (33, 3001, 1024, 11), (64, 4099, 4096, 16), (100, 4099, 512, 25), (128, 4103, 1024, 64),
     (200, 3000, 256, 50),
-    # 17..64 rows against a long vocabulary: the sweep, one wave per run of
-    # 32-row weight tiles (on 256 CUs: 2, 3, 4 tiles per wave at <= 32 rows;
-    # 3, 5, 6 at <= 64); ragged last tile and last wave; 1 to 8 64-deep chunks
-    # (a single chunk has no fills ahead); groups of 4, 6, 8, 11 (per-element
-    # bias) and 16 rows
-    (20, 65600, 320, 4), (33, 70000, 256, 11), (64, 66000, 512, 16),
-    (24, 65536, 192, 8), (18, 110000, 192, 6), (48, 100000, 128, 16), (40, 128300, 64, 8),
+    # 17..64 rows against a long vocabulary, K a multiple of 128: the sweep,
+    # one wave per run of 16-row weight tiles (on 256 CUs 6, 8, 10, 13 and 16
+    # tiles per wave); ragged last tile and last wave; 1 to 4 128-deep chunks
+    # (a single chunk fills only its own stages); groups of 4, 6, 8, 10, 11,
+    # 16 and 25 rows (bias rows with an odd stride: scalar epilogue)
+    (20, 65600, 384, 4), (33, 70000, 256, 11), (64, 66000, 512, 16),
+    (24, 65536, 256, 8), (18, 110000, 128, 6), (48, 100000, 128, 16), (40, 128300, 128, 8),
+    (30, 90000, 256, 10), (50, 80000, 128, 25), (24, 170000, 128, 8),
+    # 17..64 rows with K not a multiple of 128: the 128-row-block stream kernel
+    (20, 65600, 320, 4), (40, 70000, 192, 8),
     (1, 151936, 64, 1),
     # <= 16 rows against a long vocabulary, K a multiple of 128: 128-deep
     # chunk pairs, 4 waves over K (some waves with no pairs; one pair)
@@ -99,22 +102,32 @@ def test_lse_topk(rows, vocab, k, T, dist):
     (1024, 20000, 1024, 64), (1024, 20000, 640, 32), (1030, 16400, 768, 103),
 ])
 def test_project_bf16_within_error_bound(rows, vocab, hidden, group):
+    check_project_bf16(rows, vocab, hidden, group, pad=3)
+
+
+@pytest.mark.parametrize("rows,vocab,hidden,group", [(24, 100000, 256, 8), (40, 151936, 128, 20), (8, 151936, 256, 8)])
+def test_project_bf16_aligned_bias(rows, vocab, hidden, group):
+    """Bias rows with a stride of the vocabulary (16-byte aligned): the vector epilogues."""
+    check_project_bf16(rows, vocab, hidden, group, pad=0)
+
+
+def check_project_bf16(rows, vocab, hidden, group, pad):
     rng = np.random.default_rng(rows + vocab + hidden)
     x = W.fp32_to_bf16_bits(np.tanh(rng.normal(0, 1.4, size=(rows, hidden))).astype(np.float32))
     U = W.fp32_to_bf16_bits(rng.normal(0, 0.02, size=(vocab, hidden)).astype(np.float32))
     groups = (rows + group - 1) // group
-    bias = rng.normal(0, 2, size=(groups, vocab + 3)).astype(np.float32)  # stride vocab + 3
+    bias = rng.normal(0, 2, size=(groups, vocab + pad)).astype(np.float32)  # stride vocab + pad
     dev = device()
     z = torch.empty(rows, vocab, dtype=torch.float32, device=dev)
     nws = D.project_workspace_size(D.BF16, rows, vocab, hidden)
     ws = torch.empty(nws, dtype=torch.uint8, device=dev) if nws else None
     say(f"project bf16 rows={rows} vocab={vocab} hidden={hidden} group={group} ws={nws}")
     xd, Ud, bd = to_dev(x), to_dev(U), to_dev(bias)
-    D.project(D.BF16, xd, Ud, bd, vocab + 3, z, group, ws)
+    D.project(D.BF16, xd, Ud, bd, vocab + pad, z, group, ws)
     if ws is not None:  # deterministic: a second call (stale scratch) gives the same bits
         z2 = torch.empty_like(z)
         ws.fill_(0x7F)
-        D.project(D.BF16, xd, Ud, bd, vocab + 3, z2, group, ws)
+        D.project(D.BF16, xd, Ud, bd, vocab + pad, z2, group, ws)
         torch.cuda.synchronize()
         assert torch.equal(z, z2)
     torch.cuda.synchronize()
