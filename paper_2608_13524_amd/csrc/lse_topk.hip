@@ -21,6 +21,7 @@ namespace dartree {
 namespace {
 
 constexpr int kBlock = 256;
+constexpr int kMidSegment = 4 * kBlock * 8;   // elements of a register-held segment at 8 float4 per thread
 
 // Block-wide merge of the threads' (Partial, top-K).  Every wave reduces its
 // own lists; the 4k wave winners are then ranked by counting (ties of equal
@@ -319,10 +320,16 @@ __global__ __launch_bounds__(kBlock) void lse_topk_merge(int nseg, int k, float 
   emit_row(row, p, key, slot, k, tau, lse, cand_logp, cand_ids);
 }
 
-// Segments per row: about 1024 blocks (four per CU), but no segment shorter
-// than 2048 elements and at most 64 segments (one record per lane when a
-// wave merges a row).
+// Segments per row (at most 64: one record per lane when a wave merges a
+// row).  Up to 16 rows: about 1024 blocks (four per CU), no segment shorter
+// than 2048 elements.  17..511 rows: segments of at most 8192 elements, each
+// held in registers in one pass (measured at 32 and 64 rows x 151936: 19
+// segments per row 15.4 / 21.6 us per launch, against 32 / 16 segments
+// streamed in 4096-element passes, 19.0 / 24.0 us, and 38 segments of 4000
+// in registers, 19.0 / 28.2 us).  From 512 rows one segment per row.
 int num_segments(int64_t rows, int64_t vocab) {
+  if (rows > 16 && rows < 512)
+    return int(std::max<int64_t>(1, std::min<int64_t>((vocab + kMidSegment - 1) / kMidSegment, 64)));
   const int64_t want = (1024 + rows - 1) / rows;
   const int64_t most = std::min<int64_t>((vocab + 2047) / 2048, 64);
   return int(std::max<int64_t>(1, std::min(want, most)));
@@ -338,6 +345,9 @@ hipError_t launch_k(const float* z, int64_t rows, int64_t vocab, int k, float ta
   const dim3 grid(unsigned(rows * nseg));
   if (vec && rows >= 512)  // z (R V floats) far exceeds the caches: stream it, 8 float4 per thread in flight
     hipLaunchKernelGGL((lse_topk_rows<K, true, 8, true>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
+                       tau, lse, cand_logp, cand_ids, part);
+  else if (vec && rows > 16 && seg_len <= kMidSegment)  // one pass of 8 float4 per thread, held in registers
+    hipLaunchKernelGGL((lse_topk_rows<K, true, 8, false>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
                        tau, lse, cand_logp, cand_ids, part);
   else if (vec)
     hipLaunchKernelGGL((lse_topk_rows<K, true, 4, false>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,

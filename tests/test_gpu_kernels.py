@@ -33,6 +33,10 @@ LSE_CASES = [
     (4, 9, 9, 2.0, "normal"),           # k = V
     # a segment held in registers where fewer than k threads hold values
     (3, 16, 8, 1.0, "ties"), (2, 28, 8, 0.0, "normal"),
+    # 17..511 rows: segments of at most 8192 held in registers (13 ragged
+    # segments with exact ties; one segment per row; k = 16; 300 rows)
+    (24, 100000, 8, 1.0, "ties"), (40, 5000, 8, 0.7, "normal"), (17, 151936, 16, 0.0, "normal"),
+    (300, 20004, 8, 1.0, "normal"),
 ]
 
 
