@@ -14,6 +14,9 @@
 //  * proj_bf16_sweep: 17..64 rows against the vocabulary.  One wave per run
 //    of weight tiles, accumulating them over the whole K loop; the weights
 //    and node rows stream into the wave's own LDS by buffer loads.
+//  * proj_bf16_hsplit: the head at 17..64 rows.  64 weight rows per block
+//    and K split into pieces, the piece's node rows staged once in LDS for
+//    the block's four tiles; a fix-up launch adds the pieces in order.
 //  * proj_bf16_big: many rows (>= 512) against the vocabulary, and the head at
 //    >= 512 rows when its tiles are too few to fill the chip.  256x256 tiles,
 //    8 waves in two groups alternating LDS reads and MFMAs, buffer loads
@@ -1217,6 +1220,105 @@ __global__ __launch_bounds__(256) void proj_big_fixup(KArgs a, int vec, BigPlan 
 }
 
 // ---------------------------------------------------------------------------
+// The head (A: h x h) at 17..64 node rows, split along K.  A block per 16-row
+// weight tile over the whole K re-reads all node rows in every block (at 64
+// rows x 4096 that is four times the weight bytes, and the launch is bound by
+// it).  Here a block owns 64 weight rows (one 16-row tile per wave) and one K
+// piece of KC: the piece's node rows are read once into LDS and serve all
+// four tiles, each wave loads its tile's MFMA operand fragments straight from
+// memory (all of the piece in flight at once), and the block stores its
+// partial sums [piece][M][N]; proj_hsplit_fixup adds the pieces in piece
+// order (deterministic) and applies the epilogue.  LDS rows of the staged
+// node rows are 256-byte pieces with 16-byte chunk c of row r at c ^ (r % 16)
+// (conflict-free writes and operand reads).
+// ---------------------------------------------------------------------------
+constexpr int HSG = 64;   // weight rows per block
+
+template <int MT, int KC>
+__global__ __launch_bounds__(256) void proj_bf16_hsplit(KArgs a, float* __restrict__ part) {
+  constexpr int NS = KC / 32;          // 32-deep MFMA steps per piece
+  constexpr int XR = 16 * MT;          // staged node rows
+  constexpr int XC = KC / 8;           // 16-byte chunks per staged row
+  constexpr int XPT = XR * XC / 256;   // chunks per thread
+  static_assert(XR * XC % 256 == 0, "whole chunks per thread");
+  __shared__ __attribute__((aligned(16))) uint16_t xs[XR * KC];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int M = a.M, N = a.N, K = a.K;
+  const int n0 = blockIdx.x * HSG, piece = blockIdx.y;
+  const int kb = piece * KC;   // K % KC == 0
+  const uint16_t* X = static_cast<const uint16_t*>(a.x);
+  const uint16_t* Wt = static_cast<const uint16_t*>(a.w);
+  // LDS element of node row `row`, 16-byte chunk c of the piece
+  auto xoff = [](int row, int c) { return (c >> 4) * (XR * 128) + row * 128 + (((c & 15) ^ (row & 15)) << 3); };
+
+  // node rows of the piece (rows past M repeat the last row; never stored)
+  u32x4 xv[XPT];
+#pragma unroll
+  for (int i = 0; i < XPT; ++i) {
+    const int idx = threadIdx.x + 256 * i, row = idx / XC, c = idx % XC;
+    xv[i] = ld_cached(X + int64_t(min(row, M - 1)) * K + kb + 8 * c);
+  }
+  // this wave's weight tile, as operand fragments (rows past N repeat the last)
+  u32x4 R[NS];
+  const uint16_t* wp = Wt + int64_t(min(n0 + 16 * w + r16, N - 1)) * K + kb + 8 * kg;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) R[s] = ld_cached(wp + 32 * s);
+  __builtin_amdgcn_sched_barrier(0);   // every load of the piece in flight before the first LDS write
+#pragma unroll
+  for (int i = 0; i < XPT; ++i) {
+    const int idx = threadIdx.x + 256 * i, row = idx / XC, c = idx % XC;
+    *reinterpret_cast<u32x4*>(xs + xoff(row, c)) = xv[i];
+  }
+  __syncthreads();
+
+  f32x4 acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const bf16x8 av = __builtin_bit_cast(bf16x8, R[s]);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const bf16x8 bv = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(xs + xoff(16 * mt + r16, 4 * s + kg)));
+      acc[mt] = mfma16(av, bv, acc[mt]);
+    }
+  }
+  // lane (r16, kg) holds node row 16 mt + r16, weight rows n .. n + 3
+  const int n = n0 + 16 * w + 4 * kg;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int m = 16 * mt + r16;
+    if (m < M && n < N) *reinterpret_cast<f32x4*>(part + (size_t(piece) * M + m) * N + n) = acc[mt];
+  }
+}
+
+// One thread per 4 outputs: the pieces summed in piece order, then the
+// epilogue.  The loads go out 8 pieces at a time, unconditionally (pieces
+// past the last repeat it and are not added): a loop of one load per piece
+// would wait a memory round trip per piece.
+template <int EPI>
+__global__ __launch_bounds__(256) void proj_hsplit_fixup(KArgs a, const float* __restrict__ part, int pieces, int vec) {
+  const int n4 = a.N >> 2;
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= a.M * n4) return;
+  const int m = idx / n4, n = 4 * (idx - m * n4);
+  const size_t stride = size_t(a.M) * a.N;
+  const float* pp = part + size_t(m) * a.N + n;
+  f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int p0 = 0; p0 < pieces; p0 += 8) {
+    f32x4 q[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) q[i] = *reinterpret_cast<const f32x4*>(pp + size_t(min(p0 + i, pieces - 1)) * stride);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (p0 + i < pieces) v = p0 + i == 0 ? q[i] : v + q[i];
+  }
+  emit4<EPI>(a, m, n, v, vec != 0);
+}
+
+// ---------------------------------------------------------------------------
 // fp32: one thread per output element, sequential K.
 // ---------------------------------------------------------------------------
 template <int EPI>
@@ -1307,6 +1409,50 @@ bool wide_logits(const KArgs& k) {
   return big_logits(k) && k.M % 32 == 0 && (k.M + WBM - 1) / WBM * WBM == (k.M + GBM - 1) / GBM * GBM;
 }
 bool big_head_candidate(const KArgs& k) { return k.M >= 2 * GBM && k.N >= GBN && k.K >= 2 * kMinPieceSteps * GBK; }
+
+// The split head: 17..64 node rows against a short weight matrix (fewer than
+// 32 * 2048 rows), K a multiple of 128, N of 4.  The piece length is the
+// longest of 512 / 256 / 128 dividing K that still gives about 384
+// blocks (1.5 per CU of a 256-CU device; fixed, so that the workspace size
+// does not depend on the device), else the shortest; a single piece takes the
+// unsplit kernel.
+bool hsplit_shape(const KArgs& k) {
+  return k.M > 16 && k.M <= 64 && k.N < 32 * 2048 && k.K % 128 == 0 && k.N % 4 == 0;
+}
+int hsplit_kc(const KArgs& k) {
+  const int groups = (k.N + HSG - 1) / HSG;
+  for (int kc : {512, 256})
+    if (k.K % kc == 0 && groups * (k.K / kc) >= 384) return kc;
+  return 128;
+}
+int hsplit_pieces(const KArgs& k) { return k.K / hsplit_kc(k); }
+
+template <int MT, int KC>
+void launch_hsplit_mt(const KArgs& k, float* part, hipStream_t s) {
+  const dim3 grid(unsigned((k.N + HSG - 1) / HSG), unsigned(k.K / KC));
+  hipLaunchKernelGGL((proj_bf16_hsplit<MT, KC>), grid, dim3(256), 0, s, k, part);
+}
+
+template <int KC>
+void launch_hsplit_kc(const KArgs& k, float* part, hipStream_t s) {
+  if (k.M <= 32) launch_hsplit_mt<2, KC>(k, part, s);
+  else if (k.M <= 48) launch_hsplit_mt<3, KC>(k, part, s);
+  else launch_hsplit_mt<4, KC>(k, part, s);
+}
+
+hipError_t launch_hsplit(const KArgs& k, int epi, float* part, hipStream_t s) {
+  const int kc = hsplit_kc(k);
+  if (kc == 512) launch_hsplit_kc<512>(k, part, s);
+  else if (kc == 256) launch_hsplit_kc<256>(k, part, s);
+  else launch_hsplit_kc<128>(k, part, s);
+  const int vec = epilogue_vec_ok(k, epi);
+  const dim3 grid(unsigned((k.M * (k.N / 4) + 255) / 256));
+  if (epi == EPI_LOGITS)
+    hipLaunchKernelGGL((proj_hsplit_fixup<EPI_LOGITS>), grid, dim3(256), 0, s, k, part, hsplit_pieces(k), vec);
+  else
+    hipLaunchKernelGGL((proj_hsplit_fixup<EPI_HEAD>), grid, dim3(256), 0, s, k, part, hsplit_pieces(k), vec);
+  return hipGetLastError();
+}
 
 BigPlan big_plan(const KArgs& k, float* split) {
   const int T = ((k.M + GBM - 1) / GBM) * ((k.N + GBN - 1) / GBN);
@@ -1400,6 +1546,8 @@ size_t proj_split_bytes(int precision, int epilogue, int64_t M, int64_t N, int64
   k.M = int(M);
   k.N = int(N);
   k.K = int(K);
+  if (epilogue == EPI_HEAD && hsplit_shape(k) && hsplit_pieces(k) > 1)
+    return size_t(hsplit_pieces(k)) * size_t(M) * size_t(N) * sizeof(float);
   const bool big = epilogue == EPI_LOGITS ? big_logits(k) : big_head_candidate(k);
   // the split partials, then (512-row tiles) the node rows in fragment order
   const size_t packed = epilogue == EPI_LOGITS && wide_logits(k) ? size_t(M) * size_t(K) * 2 : 0;
@@ -1434,6 +1582,8 @@ hipError_t launch_project(const ProjArgs& p, hipStream_t s) {
     const int tpw = sweep_tpw(k, mt);
     if (tpw > 0) return mt == 2 ? launch_sweep_tpw<2>(k, tpw, s) : launch_sweep_tpw<4>(k, tpw, s);
   }
+  if (p.epilogue == EPI_HEAD && p.split && hsplit_shape(k) && hsplit_pieces(k) > 1)
+    return launch_hsplit(k, p.epilogue, p.split, s);
   if (k.M <= 16) return launch_stream_nt<1>(k, p.epilogue, s);
   if (k.M <= 32) return launch_stream_nt<2>(k, p.epilogue, s);
   if (k.M <= 48) return launch_stream_nt<3>(k, p.epilogue, s);

@@ -41,6 +41,15 @@ SMALL = {
     "bf16-B1": small(budget=1, seed=39),
     "bf16-k12": small(branch=12, width=20, budget=50, seed=47),       # top-k bucket 16, row segments merged
     "bf16-k20": small(branch=20, width=24, budget=70, seed=48),       # top-k bucket 32
+    # 17..64 parent rows: the head's 64-row blocks split along K and summed by the fix-up launch
+    # (48 rows = three node tiles, h = 384 in 3 pieces; 57 rows, a ragged last tile, h = 640 in 5;
+    # 17 rows, one row past the few-row kernel)
+    "bf16-head-pieces-48": small(batch=2, width=24, branch=8, depth=4, budget=60, vocab=3001, hidden=384,
+                                 seed=66),
+    "bf16-head-pieces-57": small(batch=3, width=19, branch=8, depth=4, budget=60, vocab=2053, hidden=640,
+                                 seed=67),
+    "bf16-head-pieces-17": small(batch=1, width=17, branch=8, depth=4, budget=40, vocab=3001, hidden=256,
+                                 seed=68),
     # >= 512 parent rows: the head's 256x256 tiles split along K (512 rows: 4 tiles in 2 pieces each)
     "bf16-head-split": small(batch=8, width=64, branch=8, depth=4, budget=120, vocab=4099, hidden=512, seed=42),
     # 540 rows in groups of 60 (not a multiple of 32): the head's 256x256 tiles split along K with
@@ -137,7 +146,9 @@ def test_batch_and_repeat_determinism():
     same bits while the parent rows of a depth stay within one kernel regime
     (at most 16 rows: the same softmax segmentation and product blocking);
     across it (a batch of 4 x W = 6 = 24 rows) the same tree, with scores
-    within fp32 rounding of the normaliser's other summation order."""
+    within 1e-3: the normaliser is summed in another order and the head's
+    product splits K into pieces, so a few bf16 states can round the other
+    way and move later scores by a few 1e-5 (7.3e-5 measured)."""
     cfg = small(seed=43, batch=4)
     inputs = W.make_inputs(cfg)
     t1, s1, _ = run_build(cfg, inputs)
@@ -150,7 +161,7 @@ def test_batch_and_repeat_determinism():
     t3, _, _ = run_build(one.cfg, one, export=False)
     for k in ("tokens", "parents", "depths", "mask"):
         assert np.array_equal(t1[k][2], t3[k][0]), k
-    assert np.abs(t1["scores"][2] - t3["scores"][0]).max() <= 1e-5
+    assert np.abs(t1["scores"][2] - t3["scores"][0]).max() <= 1e-3
     pair = W.make_inputs(cfg, requests=[1, 2])   # 12 rows per depth
     t4, _, _ = run_build(pair.cfg, pair, export=False)
     for k in ("tokens", "parents", "depths", "scores", "mask"):
