@@ -399,9 +399,15 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   tm.mark(tb + DARTREE_KERNEL_LOGITS, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
 
-  // K3: lse and top-k per parent row (segment records, if any, are merged by K4)
+  // K3: lse and top-k per parent row.  Segment records, if any, are merged
+  // by K4, whose block takes a request's parent rows one per wave; with more
+  // parent rows per request than it has waves (measured at 32 rows: 311 us of
+  // selection per round against 152 + 78 more in this launch), the softmax
+  // launch merges them itself, one block per row, and K4 reads finished
+  // candidates.
+  const bool merge_here = np > select_level_waves(int(k)) && lse_topk_segments(R, V) > 1;
   tm.mark(tb + DARTREE_KERNEL_LSE, 0);
-  err = launch_lse_topk(z, R, V, int(k), tau, lse, clp, cid, at<char>(ws, l.k3), false, st);
+  err = launch_lse_topk(z, R, V, int(k), tau, lse, clp, cid, at<char>(ws, l.k3), merge_here, st);
   tm.mark(tb + DARTREE_KERNEL_LSE, 1);
   if (err != hipSuccess) return DARTREE_ERR_HIP;
 
@@ -417,7 +423,7 @@ dartree_status expand(const dartree_params& p, const dartree_inputs& in, int d, 
   la.parent_stride = int(W);
   la.out_stride = int(W);
   la.parent_score = parent_score;
-  la.nseg = lse_topk_segments(R, V);
+  la.nseg = merge_here ? 1 : lse_topk_segments(R, V);
   la.rows_ranked = 1;
   la.part = at<float>(ws, l.k3);
   la.lse = lse;

@@ -108,6 +108,9 @@ struct LevelArgs {
   int stamp_depth;
 };
 hipError_t launch_select_level(const LevelArgs& a, hipStream_t s);
+// Waves of one select_level block for branching factor k: a block merges the
+// segment records of its request's parent rows one row per wave.
+int select_level_waves(int k);
 
 // Shared candidate sets C = TopK(logits row, K) of `rows` fp32 rows, ids in
 // (value desc, id asc) order; scratch holds the per-chunk winners.

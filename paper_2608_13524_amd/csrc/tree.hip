@@ -385,6 +385,17 @@ __global__ __launch_bounds__(1024) void prune_emit(LevelShape shape, int budget,
 
 }  // namespace
 
+int select_level_waves(int k) {
+  switch (topk_bucket(k)) {
+    case 1: return select_threads<1>() / 64;
+    case 2: return select_threads<2>() / 64;
+    case 4: return select_threads<4>() / 64;
+    case 8: return select_threads<8>() / 64;
+    case 16: return select_threads<16>() / 64;
+    default: return select_threads<32>() / 64;
+  }
+}
+
 hipError_t launch_select_level(const LevelArgs& a, hipStream_t s) {
   if (a.batch <= 0) return hipSuccess;
   // state slices: enough blocks to spread the state rows over the chip
