@@ -172,7 +172,9 @@ dartree_status dartree_workspace_size(const dartree_params* p, size_t* bytes);
  * dartree_build_tree on the host.  dartree_expand_depth(d > 1) on a
  * workspace whose record is not (the same parameters, d - 1), and
  * dartree_prune on one whose record is not depth L, return DARTREE_ERR_ORDER
- * with nothing enqueued; d = 1 always starts a new round.  Replays of a
+ * with nothing enqueued; d = 1 always starts a new round.  Memory that held
+ * a round of the same parameters at the same address keeps that round's
+ * record until depth 1 runs on it again.  Replays of a
  * captured graph do not update the record.  Each depth's selection kernel
  * also writes {parameters, d} into the workspace; with the environment
  * variable DARTREE_DEBUG=1 (read once per process) dartree_expand_depth and

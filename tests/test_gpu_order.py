@@ -30,7 +30,10 @@ def _status(fn, *args):
 
 @pytest.mark.parametrize("shared", [0, 16])
 def test_out_of_order_calls_write_nothing(shared):
-    cfg = small(seed=91, candidates=shared, branch=8 if shared else 4)
+    # a budget no other test uses: the library keys its order record by the
+    # workspace's address and the parameters, and the allocator may hand this
+    # test memory where another test completed a round of the same parameters
+    cfg = small(seed=91, candidates=shared, branch=8 if shared else 4, budget=19)
     dev = device()
     p = D.Params.of(cfg)
     di = D.DeviceInputs.from_host(W.make_inputs(cfg), dev)
