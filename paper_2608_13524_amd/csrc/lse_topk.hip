@@ -320,6 +320,22 @@ __global__ __launch_bounds__(kBlock) void lse_topk_merge(int nseg, int k, float 
   emit_row(row, p, key, slot, k, tau, lse, cand_logp, cand_ids);
 }
 
+// The register-resident path alone, for segments known to fit one pass:
+// without the streaming path's staging rows its LDS is a few KB, so more
+// blocks fit on a compute unit (the 1216 segments of 64 rows x 151936 are
+// resident at once instead of 1024 and a second wave).
+template <int K, int CH>
+__global__ __launch_bounds__(kBlock) void lse_topk_regs(const float* __restrict__ z, int vocab, int nseg,
+                                                        int seg_len, int k, float tau, float* lse,
+                                                        float* cand_logp, int32_t* cand_ids, float* part) {
+  const int64_t row = blockIdx.x / nseg;
+  const int seg = blockIdx.x % nseg;
+  const int v0 = seg * seg_len;
+  const int v1 = min(vocab, v0 + seg_len);
+  segment_in_registers<K, CH, false>(z + row * int64_t(vocab), v0, v1, nseg, k, tau, kLog2e / tau, row, seg, lse,
+                                     cand_logp, cand_ids, part);
+}
+
 // Segments per row (at most 64: one record per lane when a wave merges a
 // row).  Up to 16 rows: about 1024 blocks (four per CU), no segment shorter
 // than 2048 elements.  17..511 rows: segments of at most 8192 elements, each
@@ -347,8 +363,8 @@ hipError_t launch_k(const float* z, int64_t rows, int64_t vocab, int k, float ta
     hipLaunchKernelGGL((lse_topk_rows<K, true, 8, true>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
                        tau, lse, cand_logp, cand_ids, part);
   else if (vec && rows > 16 && seg_len <= kMidSegment)  // one pass of 8 float4 per thread, held in registers
-    hipLaunchKernelGGL((lse_topk_rows<K, true, 8, false>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
-                       tau, lse, cand_logp, cand_ids, part);
+    hipLaunchKernelGGL((lse_topk_regs<K, 8>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k, tau, lse,
+                       cand_logp, cand_ids, part);
   else if (vec)
     hipLaunchKernelGGL((lse_topk_rows<K, true, 4, false>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
                        tau, lse, cand_logp, cand_ids, part);
