@@ -365,9 +365,6 @@ hipError_t launch_k(const float* z, int64_t rows, int64_t vocab, int k, float ta
   else if (vec && rows > 16 && seg_len <= kMidSegment)  // one pass of 8 float4 per thread, held in registers
     hipLaunchKernelGGL((lse_topk_regs<K, 8>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k, tau, lse,
                        cand_logp, cand_ids, part);
-  else if (vec && seg_len <= 4 * kBlock * 4)  // one pass of 4 float4 per thread, held in registers
-    hipLaunchKernelGGL((lse_topk_regs<K, 4>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k, tau, lse,
-                       cand_logp, cand_ids, part);
   else if (vec)
     hipLaunchKernelGGL((lse_topk_rows<K, true, 4, false>), grid, dim3(kBlock), 0, s, z, int(vocab), nseg, seg_len, k,
                        tau, lse, cand_logp, cand_ids, part);
