@@ -109,7 +109,7 @@ __device__ __forceinline__ void segment_in_registers(const float* zr, int v0, in
                                                      int32_t* cand_ids, float* part) {
   constexpr int kWaves = kBlock / 64;
   constexpr int kCap = K * 4 * CH;
-  __shared__ __attribute__((aligned(16))) uint64_t tkey[kBlock];
+  __shared__ __attribute__((aligned(16))) uint64_t wkey[kWaves * K];
   __shared__ uint64_t cand[kCap];
   __shared__ Partial sp[kWaves];
   __shared__ uint64_t thr_s;
@@ -141,24 +141,33 @@ __device__ __forceinline__ void segment_in_registers(const float* zr, int v0, in
   }
   const Partial wp = wave_partial(p, scale);
   if (lane == 0) sp[wave] = wp;
-  tkey[tid] = best;
+  // the k-th largest thread key (keys of threads holding values are distinct:
+  // one id each; the others hold the empty key, the least of all): every
+  // wave's k largest by k rounds of a wave arg-max, then the kWaves k wave
+  // winners, which hold the block's k largest, ranked by counting (ranking
+  // all kBlock keys against each other read 512 KB of LDS per block)
+  {
+    uint64_t one[K], wout[K];
+    one[0] = best;
+#pragma unroll
+    for (int r = 1; r < K; ++r) one[r] = rank_key(-INFINITY, INT32_MAX);
+    wave_topk<K>(one, k, wout);
+    if (lane == 0) {
+#pragma unroll
+      for (int r = 0; r < K; ++r)
+        if (r < k) wkey[wave * k + r] = wout[r];
+    }
+  }
   if (tid == 0) {
     count = 0;
     thr_s = rank_key(-INFINITY, INT32_MAX);   // fewer than k threads hold values: take them all
   }
   __syncthreads();
-  // the k-th largest thread key (keys of threads holding values are distinct:
-  // one id each; the others hold the empty key, the least of all)
-  {
-    typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
-    const u64x2* t2 = reinterpret_cast<const u64x2*>(tkey);
+  if (tid < kWaves * k) {
+    const uint64_t e = wkey[tid];
     int rank = 0;
-#pragma unroll 8
-    for (int j = 0; j < kBlock / 2; ++j) {
-      const u64x2 o = t2[j];
-      rank += int(o.x > best) + int(o.y > best);
-    }
-    if (rank == k - 1) thr_s = best;
+    for (int j = 0; j < kWaves * k; ++j) rank += int(wkey[j] > e);
+    if (rank == k - 1) thr_s = e;
   }
   __syncthreads();
   const uint64_t thr = thr_s;
