@@ -51,11 +51,16 @@ SMALL = {
     "bf16-head-pieces-17": small(batch=1, width=17, branch=8, depth=4, budget=40, vocab=3001, hidden=256,
                                  seed=68),
     # more parent rows per request than the selection block has waves: the softmax launch merges
-    # its row segments itself (24 rows in 3 segments of <= 8192; k = 16: 12 rows in 10 segments)
+    # its row segments itself (24 rows in 3 segments of <= 8192; k = 16: 12 rows in 10 and in 35
+    # segments, 8 waves; k = 32: 10 rows, 4 waves)
     "bf16-merged-rows": small(batch=2, width=24, branch=8, depth=4, budget=60, vocab=20011, hidden=128,
                               seed=69),
     "bf16-merged-k16": small(batch=1, width=12, branch=16, depth=4, budget=40, vocab=20011, hidden=128,
                              seed=70),
+    "bf16-merged-lse-side": small(batch=1, width=12, branch=16, depth=3, budget=40, vocab=70001, hidden=128,
+                                  seed=75),
+    "bf16-merged-k32": small(batch=1, width=10, branch=32, depth=3, budget=30, vocab=20011, hidden=128,
+                             seed=76),
     # >= 512 parent rows: the head's 256x256 tiles split along K (512 rows: 4 tiles in 2 pieces each)
     "bf16-head-split": small(batch=8, width=64, branch=8, depth=4, budget=120, vocab=4099, hidden=512, seed=42),
     # 540 rows in groups of 60 (not a multiple of 32): the head's 256x256 tiles split along K with
