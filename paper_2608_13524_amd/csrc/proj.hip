@@ -1296,28 +1296,39 @@ __global__ __launch_bounds__(256) void proj_bf16_hsplit(KArgs a, float* __restri
   }
 }
 
-// One thread per 4 outputs: the pieces summed in piece order, then the
-// epilogue.  The loads go out 8 pieces at a time, unconditionally (pieces
-// past the last repeat it and are not added): a loop of one load per piece
-// would wait a memory round trip per piece.
-template <int EPI>
-__global__ __launch_bounds__(256) void proj_hsplit_fixup(KArgs a, const float* __restrict__ part, int pieces, int vec) {
-  const int n4 = a.N >> 2;
-  const int idx = blockIdx.x * 256 + threadIdx.x;
-  if (idx >= a.M * n4) return;
-  const int m = idx / n4, n = 4 * (idx - m * n4);
-  const size_t stride = size_t(a.M) * a.N;
-  const float* pp = part + size_t(m) * a.N + n;
+// The pieces summed in piece order, then the epilogue.  Block b takes column
+// group b % G (the 64 weight rows of one main-kernel group) and rows
+// 16 (b / G) .. + 15, a thread 4 outputs (with G a multiple of 8 on the XCD
+// whose main-kernel blocks wrote that group: about 1% faster per round than
+// a row per block, though the counters show the partial sums still fetched
+// from beyond the L2).  The loads go out BATCH pieces at a time (8, or 16
+// past 8 pieces), unconditionally (pieces past the last repeat it and are not
+// added): a loop of one load per piece would wait a memory round trip per
+// piece.
+template <int BATCH>
+__device__ __forceinline__ f32x4 sum_pieces(const float* pp, size_t stride, int pieces) {
   f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int p0 = 0; p0 < pieces; p0 += 8) {
-    f32x4 q[8];
+  for (int p0 = 0; p0 < pieces; p0 += BATCH) {
+    f32x4 q[BATCH];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) q[i] = *reinterpret_cast<const f32x4*>(pp + size_t(min(p0 + i, pieces - 1)) * stride);
+    for (int i = 0; i < BATCH; ++i) q[i] = *reinterpret_cast<const f32x4*>(pp + size_t(min(p0 + i, pieces - 1)) * stride);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < BATCH; ++i)
       if (p0 + i < pieces) v = p0 + i == 0 ? q[i] : v + q[i];
   }
+  return v;
+}
+
+template <int EPI>
+__global__ __launch_bounds__(256) void proj_hsplit_fixup(KArgs a, const float* __restrict__ part, int pieces, int vec) {
+  const int G = (a.N + HSG - 1) / HSG;
+  const int g = blockIdx.x % G, r16 = blockIdx.x / G;
+  const int m = 16 * r16 + (threadIdx.x >> 4), n = HSG * g + 4 * (threadIdx.x & 15);
+  if (m >= a.M || n >= a.N) return;
+  const size_t stride = size_t(a.M) * a.N;
+  const float* pp = part + size_t(m) * a.N + n;
+  const f32x4 v = pieces <= 8 ? sum_pieces<8>(pp, stride, pieces) : sum_pieces<16>(pp, stride, pieces);
   emit4<EPI>(a, m, n, v, vec != 0);
 }
 
@@ -1370,15 +1381,15 @@ hipError_t launch_stream_nt(const KArgs& k, int epi, hipStream_t s) {
   // 16 node rows; from 17 node rows on, 128-row blocks and 4 waves over K, so
   // that every node-row operand a wave loads serves 8 weight tiles (measured
   // at 32 and 64 rows: 1.36x and 1.47x the 32-row blocks' stream rate).
-  // Short ones (A, h rows): 16-row blocks, 16 waves over K (8 when the node
-  // rows need more registers), so that even h = 2560 rows give enough waves
-  // to keep HBM busy.
+  // Short ones (A, h rows): 16-row blocks, 8 waves over K (16 at 17-32 rows;
+  // measured at 8 rows x 2560: 8 waves 129.7 us of head per round against
+  // 135.8 with 16).
   if (k.N >= 32 * 2048) {
     if constexpr (MT >= 2) return launch_stream<MT, 8, 4, 1>(k, epi, s);
     if (k.K % 128 == 0 && epi == EPI_LOGITS) return launch_pairs<4>(k, s);
     return launch_stream<MT, 2, 8, 2>(k, epi, s);
   }
-  if constexpr (MT <= 2) return launch_stream<MT, 1, 16, 2>(k, epi, s);
+  if constexpr (MT == 2) return launch_stream<MT, 1, 16, 2>(k, epi, s);
   return launch_stream<MT, 1, 8, 2>(k, epi, s);
 }
 
@@ -1449,7 +1460,7 @@ hipError_t launch_hsplit(const KArgs& k, int epi, float* part, hipStream_t s) {
   else if (kc == 256) launch_hsplit_kc<256>(k, part, s);
   else launch_hsplit_kc<128>(k, part, s);
   const int vec = epilogue_vec_ok(k, epi);
-  const dim3 grid(unsigned((k.M * (k.N / 4) + 255) / 256));
+  const dim3 grid(unsigned(((k.N + HSG - 1) / HSG) * ((k.M + 15) / 16)));
   if (epi == EPI_LOGITS)
     hipLaunchKernelGGL((proj_hsplit_fixup<EPI_LOGITS>), grid, dim3(256), 0, s, k, part, hsplit_pieces(k), vec);
   else
