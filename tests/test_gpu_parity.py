@@ -50,6 +50,10 @@ SMALL = {
                                  seed=67),
     "bf16-head-pieces-17": small(batch=1, width=17, branch=8, depth=4, budget=40, vocab=3001, hidden=256,
                                  seed=68),
+    # h = 2176 = 17 x 128 in 17 pieces: the fix-up's loads in two batches of 16, the second
+    # repeating the last piece 15 times (not added)
+    "bf16-head-pieces-many": small(batch=1, width=24, branch=8, depth=4, budget=48, vocab=3001, hidden=2176,
+                                   seed=77),
     # more parent rows per request than the selection block has waves: the softmax launch merges
     # its row segments itself (24 rows in 3 segments of <= 8192; k = 16: 12 rows in 10 and in 35
     # segments, 8 waves; k = 32: 10 rows, 4 waves)
