@@ -54,6 +54,11 @@ SMALL = {
     # repeating the last piece 15 times (not added)
     "bf16-head-pieces-many": small(batch=1, width=24, branch=8, depth=4, budget=48, vocab=3001, hidden=2176,
                                    seed=77),
+    # h = 320, not a multiple of 128, against more than 65536 tokens: the logits at 8 rows on the
+    # 16-row-block stream kernel and at 24 rows on the 128-row-block one (the pair and sweep
+    # kernels need 128-deep chunks), the 24-row head on the few-row kernel (no K pieces)
+    "bf16-h320-long-vocab": small(batch=1, width=24, branch=8, depth=4, budget=48, vocab=70001, hidden=320,
+                                  seed=78),
     # more parent rows per request than the selection block has waves: the softmax launch merges
     # its row segments itself (24 rows in 3 segments of <= 8192; k = 16: 12 rows in 10 and in 35
     # segments, 8 waves; k = 32: 10 rows, 4 waves)
